@@ -1,0 +1,34 @@
+"""fp64 CPU oracle for block-causal attention and the rolling KV cache.
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import or call
+this package: it exists so that tests, the smoke check and the benchmark's
+CPU-baseline leg can check the HIP kernels against a plain, slow, obviously
+correct implementation of what the paper defines.  It shares no code with the
+HIP path (it imports numpy only).
+
+Contents
+- attention.py: block-causal multi-head attention, forward and analytic
+  backward, with an explicit mask over all keys (paper Sec. 3.2); cached chunk
+  attention for queued in-flight chunks over a window of committed chunks
+  (paper Sec. 3.5).
+- ring.py: the integer model of the ring-buffered FIFO KV cache
+  (paper Sec. 3.5, "Structured Rolling KV Cache").
+
+Parity status: every function here is pinned by the not-gpu tests in
+tests/test_oracle.py (library special cases, closed forms, invariants,
+finite differences, brute force); none is "parity unpinned".
+"""
+from .attention import (  # noqa: F401
+    chunk_of,
+    block_causal_visible,
+    attention_fwd,
+    attention_bwd,
+    block_causal_attn_fwd,
+    block_causal_attn_bwd,
+    block_causal_attn_fwd_rows,
+    cached_visible,
+    cached_chunk_attn,
+    QUEUED_CAUSAL,
+    QUEUED_ISOLATED,
+)
+from .ring import RingModel, RingError  # noqa: F401
