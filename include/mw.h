@@ -1,0 +1,177 @@
+/*
+ * mw.h -- C ABI of the block-causal attention library for MI355X (gfx950).
+ *
+ * Operations (from "MiniWorld: Democratizing the Training of Video World
+ * Models from Scratch"):
+ *   - block-causal multi-head self-attention, forward and backward
+ *     (Sec. 3.2, "Block-Causal Video DiT"): the token sequence is split into
+ *     temporally ordered chunks of chunk_len tokens; a token attends to every
+ *     token of its own chunk and of all earlier chunks, never to later chunks;
+ *   - the rolling KV cache of committed chunks and the attention of queued
+ *     in-flight chunks over it (Sec. 3.5, "Streaming Inference",
+ *     "Structured Rolling KV Cache", "Pipelined Denoising").
+ *
+ * Conventions (every entry point):
+ *   - Tensors are device pointers to contiguous row-major arrays.  bf16 means
+ *     IEEE bfloat16 stored as 16-bit words.  Every pointer must be 16-byte
+ *     aligned.  The caller allocates and owns every buffer, including the
+ *     backward workspace; the library never allocates or frees device memory.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the legacy default
+ *     stream) and the call returns without waiting.  Faults during kernel
+ *     execution surface at the caller's next synchronisation.
+ *   - Arguments are validated before anything is enqueued; on error nothing
+ *     is enqueued, no state changes, and a negative mw_status is returned.
+ *     mw_last_error() then describes the problem (per-thread message).
+ *   - No C++ exception crosses this boundary.  Calls are reentrant, except
+ *     that one mw_kvcache must not be used by two threads at once.
+ */
+#ifndef MW_H
+#define MW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef void* mw_stream_t; /* a hipStream_t */
+
+typedef enum {
+  MW_OK = 0,
+  MW_EINVAL = -1,        /* null pointer, non-positive size, inconsistent sizes */
+  MW_EUNSUPPORTED = -2,  /* head dimension other than 64 or 128, or a limit exceeded */
+  MW_EALIGN = -3,        /* a pointer that is not 16-byte aligned */
+  MW_EFULL = -4,         /* append to a ring whose slots are all live */
+  MW_EEMPTY = -5,        /* evict more chunks than are live */
+  MW_EHIP = -6           /* the HIP runtime reported an error at launch */
+} mw_status;
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char* mw_last_error(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int mw_version(void);
+
+/* Largest supported window (committed chunks attended to) and queued-chunk count. */
+#define MW_MAX_WINDOW 64
+#define MW_MAX_QUEUED 64
+
+/* ------------------------------------------------------------------------
+ * Training: block-causal attention (Sec. 3.2).
+ *
+ * Query row i and key j (0-based positions in the sequence) lie in chunks
+ * floor(i/chunk_len) and floor(j/chunk_len); key j is visible to row i iff
+ * floor(j/chunk_len) <= floor(i/chunk_len).  T need not be a multiple of
+ * chunk_len (the last chunk is then shorter).  With S = scale * Q K^T masked
+ * to -inf on hidden pairs:
+ *     O   = softmax(S) V                          (row-wise softmax)
+ *     LSE = log(sum_j exp(S_ij)) over visible j   (natural log)
+ *
+ * q, k, v, o : bf16 [B, H, T, D]
+ * lse        : fp32 [B, H, T]  (needed by the backward pass)
+ * D          : 64 or 128.  scale > 0 (the usual choice is 1/sqrt(D)).
+ * Arithmetic: bf16 products, fp32 accumulation and softmax; the softmax
+ * probabilities are rounded to bf16 before the product with V; O is rounded
+ * to bf16 (nearest even).
+ * Errors: MW_EINVAL (null pointer, B/H/T/chunk_len < 1, scale <= 0),
+ * MW_EALIGN, MW_EUNSUPPORTED (D), MW_EHIP.
+ * ---------------------------------------------------------------------- */
+int mw_block_causal_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
+                             int B, int H, int T, int D, int chunk_len, float scale,
+                             mw_stream_t stream);
+
+/* Bytes of device workspace mw_block_causal_attn_bwd needs (fp32 row terms). */
+size_t mw_block_causal_attn_bwd_workspace_size(int B, int H, int T, int D);
+
+/* Backward of the forward above for the loss sum(dO * O): the analytic softmax
+ * gradient
+ *     dV = P^T dO,  dP = dO V^T,  Delta_i = sum_d dO_id O_id,
+ *     dS = P * (dP - Delta),  dQ = scale dS K,  dK = scale dS^T Q,
+ * with P recomputed from q, k and the forward's lse.
+ *
+ * q, k, v, o, d_o : bf16 [B, H, T, D] (o and lse from mw_block_causal_attn_fwd)
+ * lse             : fp32 [B, H, T]
+ * dq, dk, dv      : bf16 [B, H, T, D], written (not accumulated)
+ * workspace       : device buffer of at least
+ *                   mw_block_causal_attn_bwd_workspace_size(B, H, T, D) bytes;
+ *                   its contents on entry do not matter.
+ * The result is deterministic (no atomics).
+ * Errors: as the forward, plus MW_EINVAL if workspace_bytes is too small.
+ */
+int mw_block_causal_attn_bwd(const void* q, const void* k, const void* v, const void* o,
+                             const void* d_o, const float* lse, void* dq, void* dk, void* dv,
+                             void* workspace, size_t workspace_bytes,
+                             int B, int H, int T, int D, int chunk_len, float scale,
+                             mw_stream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Rolling KV cache (Sec. 3.5, "Structured Rolling KV Cache").
+ *
+ * Committed chunks enter a FIFO of capacity S chunks kept as a ring of S
+ * slots over caller-owned device buffers k_slots and v_slots, each bf16
+ * [S, B, H, L, D].  Chunks are numbered by commit order c = 0, 1, ...; head
+ * counts commits and tail counts evictions, so the live chunks are
+ * [tail, head) and chunk c lives in slot c mod S.  A committed chunk's keys
+ * and values are never modified afterwards.  The struct is plain data: it can
+ * be copied to snapshot the ring state and restored by copying it back
+ * (together with the slot buffers' contents).
+ * ---------------------------------------------------------------------- */
+typedef struct {
+  void* k_slots;
+  void* v_slots;
+  int S, B, H, L, D;
+  int64_t head; /* chunks committed so far */
+  int64_t tail; /* chunks evicted so far  */
+} mw_kvcache;
+
+/* Initialise an empty ring over k_slots/v_slots (bf16 [S,B,H,L,D]); no device work.
+ * Errors: MW_EINVAL (null, sizes < 1), MW_EALIGN, MW_EUNSUPPORTED (D not 64/128). */
+int mw_kvcache_init(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, int H, int L, int D);
+
+/* Commit one chunk: enqueue a copy of k_chunk and v_chunk (bf16 [B,H,L,D]) into
+ * slot head mod S, then head += 1 (host state changes at call time).
+ * Errors: MW_EINVAL, MW_EALIGN, MW_EFULL (head - tail == S), MW_EHIP. */
+int mw_kvcache_append(mw_kvcache* c, const void* k_chunk, const void* v_chunk, mw_stream_t stream);
+
+/* Discard the n_chunks oldest live chunks (tail += n_chunks).  Host only.
+ * Errors: MW_EINVAL (null, n_chunks < 0), MW_EEMPTY (n_chunks > head - tail). */
+int mw_kvcache_evict(mw_kvcache* c, int n_chunks);
+
+/* Number of live chunks (head - tail), or a negative mw_status for a null cache. */
+int mw_kvcache_live(const mw_kvcache* c);
+
+/* Slot holding logical chunk `chunk` if it is live, else -1 (also for a null cache). */
+int mw_kvcache_slot_of(const mw_kvcache* c, int64_t chunk);
+
+/* ------------------------------------------------------------------------
+ * Cached chunk attention for the pipelined denoiser (Sec. 3.5).
+ *
+ * n_queued in-flight chunks of q_len tokens each attend to the `window`
+ * newest live committed chunks (window = -1: all live chunks) and to the
+ * in-flight chunks' own keys.  The keys form the virtual sequence
+ *   [window chunks, oldest first (window * L tokens)] ++ [queued chunks 0..n_queued-1]
+ * and queued chunk j sees
+ *   MW_QUEUED_CAUSAL  : the window and queued chunks 0..j (the committed history
+ *                       plus the preceding chunks of the active window; the
+ *                       chunk-wise causal rule of Sec. 3.5);
+ *   MW_QUEUED_ISOLATED: the window and itself only.
+ *
+ * q, k_new, v_new, o : bf16 [B, H, n_queued*q_len, D] with B, H, D those of the cache
+ * lse                : fp32 [B, H, n_queued*q_len] or NULL
+ * Keys are visited in logical order whatever the ring offset, so the result
+ * for a given window content does not depend on where the ring wrapped.
+ * Errors: MW_EINVAL (null pointers, n_queued/q_len < 1, window > live,
+ * window < -1, unknown flags, scale <= 0), MW_EALIGN,
+ * MW_EUNSUPPORTED (window > MW_MAX_WINDOW or n_queued > MW_MAX_QUEUED), MW_EHIP.
+ * ---------------------------------------------------------------------- */
+enum { MW_QUEUED_CAUSAL = 0, MW_QUEUED_ISOLATED = 1 };
+
+int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new,
+                         int n_queued, int q_len, const mw_kvcache* c, int window, int flags,
+                         void* o, float* lse, float scale, mw_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MW_H */

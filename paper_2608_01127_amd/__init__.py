@@ -1,0 +1,32 @@
+"""MI355X-native block-causal attention for streaming video world models.
+
+Python face of libmw.so (C ABI in include/mw.h): block-causal multi-head
+attention forward/backward (paper Sec. 3.2), the ring-buffered rolling KV
+cache and cached attention of queued in-flight chunks (paper Sec. 3.5).
+The functions carry the C entry points' names; all compute runs in the HIP
+kernels of csrc/.
+"""
+from ._lib import (  # noqa: F401
+    KVCache,
+    MWError,
+    MW_EALIGN,
+    MW_EEMPTY,
+    MW_EFULL,
+    MW_EHIP,
+    MW_EINVAL,
+    MW_EUNSUPPORTED,
+    MW_MAX_QUEUED,
+    MW_MAX_WINDOW,
+    MW_OK,
+    MW_QUEUED_CAUSAL,
+    MW_QUEUED_ISOLATED,
+    load,
+    mw_block_causal_attn_bwd,
+    mw_block_causal_attn_bwd_workspace_size,
+    mw_block_causal_attn_fwd,
+    mw_chunk_attn_cached,
+    mw_kvcache,
+    mw_kvcache_append,
+    mw_kvcache_evict,
+    mw_kvcache_slot_of,
+)

@@ -1,0 +1,258 @@
+"""ctypes binding of libmw.so (include/mw.h).  Argument marshalling only.
+
+Every function here forwards torch tensors' device pointers and the current
+HIP stream to the C ABI; all arithmetic runs in the library's HIP kernels.
+There is no fallback: if the library is missing or a call fails, an
+exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmw.so")
+
+MW_OK = 0
+MW_EINVAL = -1
+MW_EUNSUPPORTED = -2
+MW_EALIGN = -3
+MW_EFULL = -4
+MW_EEMPTY = -5
+MW_EHIP = -6
+MW_QUEUED_CAUSAL = 0
+MW_QUEUED_ISOLATED = 1
+MW_MAX_WINDOW = 64
+MW_MAX_QUEUED = 64
+
+STATUS_NAMES = {0: "MW_OK", -1: "MW_EINVAL", -2: "MW_EUNSUPPORTED", -3: "MW_EALIGN", -4: "MW_EFULL",
+                -5: "MW_EEMPTY", -6: "MW_EHIP"}
+
+
+class MWError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+class mw_kvcache(ctypes.Structure):
+    _fields_ = [("k_slots", ctypes.c_void_p), ("v_slots", ctypes.c_void_p),
+                ("S", ctypes.c_int), ("B", ctypes.c_int), ("H", ctypes.c_int), ("L", ctypes.c_int),
+                ("D", ctypes.c_int), ("head", ctypes.c_int64), ("tail", ctypes.c_int64)]
+
+
+# Exported symbols and their signatures (mirrors include/mw.h).
+_vp, _i, _f, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+_cache_p = ctypes.POINTER(mw_kvcache)
+SIGNATURES = {
+    "mw_last_error": ([], ctypes.c_char_p),
+    "mw_version": ([], _i),
+    "mw_block_causal_attn_fwd": ([_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _f, _vp], _i),
+    "mw_block_causal_attn_bwd_workspace_size": ([_i, _i, _i, _i], _sz),
+    "mw_block_causal_attn_bwd": ([_vp] * 9 + [_vp, _sz, _i, _i, _i, _i, _i, _f, _vp], _i),
+    "mw_kvcache_init": ([_cache_p, _vp, _vp, _i, _i, _i, _i, _i], _i),
+    "mw_kvcache_append": ([_cache_p, _vp, _vp, _vp], _i),
+    "mw_kvcache_evict": ([_cache_p, _i], _i),
+    "mw_kvcache_live": ([_cache_p], _i),
+    "mw_kvcache_slot_of": ([_cache_p, ctypes.c_int64], _i),
+    "mw_chunk_attn_cached": ([_vp, _vp, _vp, _i, _i, _cache_p, _i, _i, _vp, _vp, _f, _vp], _i),
+}
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libmw.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libmw.so not found at {path}: build it with "
+                           f"`python -m paper_2608_01127_amd.build` (no CPU fallback exists)")
+    lib = ctypes.CDLL(path)
+    for name, (args, res) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def _check(code: int) -> int:
+    if code < 0:
+        msg = load().mw_last_error().decode(errors="replace")
+        raise MWError(code, msg)
+    return code
+
+
+# ----------------------------------------------------------------------------- torch glue
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_handle(device) -> int:
+    torch = _torch()
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else t.data_ptr()
+
+
+def _bf16_4d(name, t):
+    torch = _torch()
+    if t.dtype != torch.bfloat16:
+        raise TypeError(f"{name} must be bfloat16, got {t.dtype}")
+    if t.dim() != 4:
+        raise ValueError(f"{name} must be [B,H,T,D], got shape {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a GPU device")
+
+
+def _same_device(*ts):
+    dev = ts[0].device
+    for t in ts:
+        if t is not None and t.device != dev:
+            raise ValueError("all tensors must be on the same device")
+    return dev
+
+
+def mw_block_causal_attn_fwd(q, k, v, chunk_len: int, scale=None, out=None, lse=None):
+    """Block-causal attention forward.  q, k, v: bf16 [B,H,T,D].  Returns (o, lse)."""
+    torch = _torch()
+    for n, t in (("q", q), ("k", k), ("v", v)):
+        _bf16_4d(n, t)
+    if k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k, v must have the same shape")
+    B, H, T, D = q.shape
+    dev = _same_device(q, k, v)
+    scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    o = torch.empty_like(q) if out is None else out
+    lse = torch.empty((B, H, T), dtype=torch.float32, device=dev) if lse is None else lse
+    _bf16_4d("out", o)
+    if o.shape != q.shape or lse.shape != (B, H, T) or lse.dtype != torch.float32 or not lse.is_contiguous():
+        raise ValueError("out/lse have the wrong shape or dtype")
+    _same_device(q, o, lse)
+    _check(load().mw_block_causal_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, T, D,
+                                           int(chunk_len), scale, _stream_handle(dev)))
+    return o, lse
+
+
+def mw_block_causal_attn_bwd_workspace_size(B: int, H: int, T: int, D: int) -> int:
+    return int(load().mw_block_causal_attn_bwd_workspace_size(B, H, T, D))
+
+
+def mw_block_causal_attn_bwd(q, k, v, o, d_o, lse, chunk_len: int, scale=None, workspace=None,
+                             dq=None, dk=None, dv=None):
+    """Backward of mw_block_causal_attn_fwd.  Returns (dq, dk, dv), bf16 [B,H,T,D]."""
+    torch = _torch()
+    for n, t in (("q", q), ("k", k), ("v", v), ("o", o), ("d_o", d_o)):
+        _bf16_4d(n, t)
+        if t.shape != q.shape:
+            raise ValueError(f"{n} must have the shape of q")
+    B, H, T, D = q.shape
+    if lse.shape != (B, H, T) or lse.dtype != torch.float32 or not lse.is_contiguous():
+        raise ValueError("lse must be fp32 [B,H,T] contiguous")
+    dev = _same_device(q, k, v, o, d_o, lse)
+    scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    need = mw_block_causal_attn_bwd_workspace_size(B, H, T, D)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    for n, t in (("dq", dq), ("dk", dk), ("dv", dv)):
+        _bf16_4d(n, t)
+    _same_device(q, workspace, dq, dk, dv)
+    nbytes = workspace.numel() * workspace.element_size()
+    _check(load().mw_block_causal_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(d_o), _ptr(lse), _ptr(dq),
+                                           _ptr(dk), _ptr(dv), _ptr(workspace), nbytes, B, H, T, D,
+                                           int(chunk_len), scale, _stream_handle(dev)))
+    return dq, dk, dv
+
+
+class KVCache:
+    """Ring-buffered rolling KV cache over torch-owned slot tensors (bf16 [S,B,H,L,D]).
+
+    Wraps the mw_kvcache descriptor; `head`/`tail` count commits/evictions.
+    """
+
+    def __init__(self, S: int, B: int, H: int, L: int, D: int, device="cuda", k_slots=None, v_slots=None):
+        torch = _torch()
+        shape = (S, B, H, L, D)
+        self.k_slots = torch.empty(shape, dtype=torch.bfloat16, device=device) if k_slots is None else k_slots
+        self.v_slots = torch.empty(shape, dtype=torch.bfloat16, device=device) if v_slots is None else v_slots
+        for n, t in (("k_slots", self.k_slots), ("v_slots", self.v_slots)):
+            if t.shape != shape or t.dtype != torch.bfloat16 or not t.is_contiguous():
+                raise ValueError(f"{n} must be bf16 contiguous {shape}")
+        self.desc = mw_kvcache()
+        _check(load().mw_kvcache_init(ctypes.byref(self.desc), _ptr(self.k_slots), _ptr(self.v_slots),
+                                      S, B, H, L, D))
+
+    @property
+    def head(self) -> int:
+        return int(self.desc.head)
+
+    @property
+    def tail(self) -> int:
+        return int(self.desc.tail)
+
+    @property
+    def live(self) -> int:
+        return _check(load().mw_kvcache_live(ctypes.byref(self.desc)))
+
+    def slot_of(self, chunk: int) -> int:
+        return int(load().mw_kvcache_slot_of(ctypes.byref(self.desc), int(chunk)))
+
+    def snapshot(self) -> tuple:
+        return (int(self.desc.head), int(self.desc.tail))
+
+    def restore(self, snap) -> None:
+        self.desc.head, self.desc.tail = snap
+
+
+def mw_kvcache_append(cache: KVCache, k_chunk, v_chunk) -> int:
+    """Commit one chunk (bf16 [B,H,L,D]); returns the slot it was written to."""
+    d = cache.desc
+    for n, t in (("k_chunk", k_chunk), ("v_chunk", v_chunk)):
+        _bf16_4d(n, t)
+        if tuple(t.shape) != (d.B, d.H, d.L, d.D):
+            raise ValueError(f"{n} must be [B,H,L,D] = {(d.B, d.H, d.L, d.D)}")
+    dev = _same_device(cache.k_slots, k_chunk, v_chunk)
+    slot = int(d.head % d.S)
+    _check(load().mw_kvcache_append(ctypes.byref(d), _ptr(k_chunk), _ptr(v_chunk), _stream_handle(dev)))
+    return slot
+
+
+def mw_kvcache_evict(cache: KVCache, n_chunks: int) -> None:
+    _check(load().mw_kvcache_evict(ctypes.byref(cache.desc), int(n_chunks)))
+
+
+def mw_kvcache_slot_of(cache: KVCache, chunk: int) -> int:
+    return cache.slot_of(chunk)
+
+
+def mw_chunk_attn_cached(q, k_new, v_new, n_queued: int, q_len: int, cache: KVCache, window: int = -1,
+                         flags: int = MW_QUEUED_CAUSAL, scale=None, out=None, lse=None, want_lse: bool = False):
+    """Cached chunk attention of n_queued in-flight chunks.  Returns (o, lse or None)."""
+    torch = _torch()
+    d = cache.desc
+    for n, t in (("q", q), ("k_new", k_new), ("v_new", v_new)):
+        _bf16_4d(n, t)
+        if tuple(t.shape) != (d.B, d.H, n_queued * q_len, d.D):
+            raise ValueError(f"{n} must be [B,H,n_queued*q_len,D] = {(d.B, d.H, n_queued * q_len, d.D)}")
+    dev = _same_device(cache.k_slots, q, k_new, v_new)
+    scale = 1.0 / math.sqrt(d.D) if scale is None else float(scale)
+    o = torch.empty_like(q) if out is None else out
+    _bf16_4d("out", o)
+    if want_lse and lse is None:
+        lse = torch.empty((d.B, d.H, n_queued * q_len), dtype=torch.float32, device=dev)
+    _check(load().mw_chunk_attn_cached(_ptr(q), _ptr(k_new), _ptr(v_new), int(n_queued), int(q_len),
+                                       ctypes.byref(d), int(window), int(flags), _ptr(o), _ptr(lse), scale,
+                                       _stream_handle(dev)))
+    return o, lse

@@ -1,0 +1,213 @@
+// Block-causal attention forward and cached chunk attention (gfx950).
+//
+// One workgroup of 4 waves computes 128 query rows (32 per wave) of one
+// (batch, head).  Keys are visited in steps of 64; each step stages the K and
+// V tile in LDS once for all four waves.  Per wave and step:
+//   S^T[key][q] = K Q^T              (bf16 MFMA 32x32x16, fp32 accumulate;
+//                                     Q stays in registers as the B operand)
+//   online softmax over keys         (a query is one lane column of S^T, so
+//                                     the row max/sum are in-lane reductions
+//                                     plus one exchange with lane l^32)
+//   O^T[d][q] += V^T P^T             (P^T feeds the MFMA B operand from the
+//                                     accumulator registers; V^T is read from
+//                                     the row-major V tile with transposing
+//                                     LDS reads)
+// Key steps wholly above the chunk diagonal are never visited; steps wholly
+// below it skip the mask; only steps that straddle a chunk edge (or the end of
+// the keys) evaluate it per element.
+//
+// Visibility rule: paper Sec. 3.2 (block-causal chunks) for training and
+// Sec. 3.5 (queued in-flight chunks over committed history) for the cached
+// variant; see Vis in mw_device.h.
+#include "mw_device.h"
+#include "mw_kernels.h"
+
+namespace mw {
+
+// XCD-aware order: consecutive workgroup ids are dealt round-robin to the 8
+// XCDs; remap so that each XCD receives one contiguous range of logical work
+// items (whole heads, heaviest query tiles first), which keeps a head's K/V in
+// one XCD's L2.
+__device__ __forceinline__ int xcd_remap(int bid, int n) {
+  if (n % 8) return bid;
+  return (bid % 8) * (n / 8) + bid / 8;
+}
+
+template <int D, bool CACHED>
+__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
+  constexpr int BM = FWD_BM, BN = FWD_BN, NT = 256;
+  constexpr int KK = D / 16;  // contraction steps over D
+  constexpr int DB = D / 32;  // 32-wide column blocks of D
+  constexpr int CPR = D / 8;  // 16-byte chunks per row
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[BN * D];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[BN * D];
+
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int bh = logical / p.n_qtiles;
+  const int qt = p.n_qtiles - 1 - logical % p.n_qtiles;  // heaviest (last) query tile first
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int q0 = qt * BM;
+  const int qrow = q0 + wave * 32 + (lane & 31);
+  const long long qoff = (long long)bh * p.Tq * D;
+
+  Vis vis{p.vis_mode, p.L, p.Tk, p.qlen, p.wL};
+
+  // Q fragments: B operand of S^T = K Q^T (lane holds Q[qrow][16kk + 8(l/32) + 0..7]).
+  bf16x8 qf[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    if (qrow < p.Tq) {
+      qf[kk] = *reinterpret_cast<const bf16x8*>(p.q + qoff + (long long)qrow * D + 16 * kk + 8 * (lane >> 5));
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) qf[kk][j] = (__bf16)0.f;
+    }
+  }
+
+  int e1, s2, e2;
+  vis.range(min(qrow, p.Tq - 1), e1, s2, e2);
+  int e1f, s2f, e2f, e1l, s2l, e2l;
+  vis.range(q0, e1f, s2f, e2f);
+  vis.range(min(q0 + BM, p.Tq) - 1, e1l, s2l, e2l);
+  const int kend = max(e1l, e2l);
+
+  f32x16 o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) o[db] = zero16();
+  float m = -INFINITY, lsum = 0.f;
+  const float c = p.scale_log2;
+
+  const long long kvoff = (long long)bh * (CACHED ? (long long)p.Tq * D : (long long)p.Tk * D);
+
+  for (int k0 = 0; k0 < kend; k0 += BN) {
+    const bool skip = (k0 >= e1l) && (k0 + BN <= s2f || k0 >= e2l);
+    if (skip) continue;
+    const bool full = (k0 + BN <= e1f) || (s2l <= k0 && k0 + BN <= e2f);
+
+    __syncthreads();  // previous tile fully consumed
+#pragma unroll
+    for (int it = 0; it < BN * CPR / NT; ++it) {
+      const int ci = tid + NT * it;
+      const int r = ci / CPR, cc = (ci % CPR) * 8;
+      const int key = k0 + r;
+      u32x4 kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
+      if (key < p.Tk) {
+        const uint16_t *ksrc, *vsrc;
+        if constexpr (CACHED) {
+          if (key < p.wL) {
+            const int w = key / p.L, off = key - w * p.L;
+            int slot = p.first_slot + w;
+            slot = slot >= p.S ? slot - p.S : slot;
+            const long long base = (long long)slot * p.slot_stride + (long long)bh * p.L * D + (long long)off * D + cc;
+            ksrc = p.k_slots + base;
+            vsrc = p.v_slots + base;
+          } else {
+            const long long base = kvoff + (long long)(key - p.wL) * D + cc;
+            ksrc = p.k + base;
+            vsrc = p.v + base;
+          }
+        } else {
+          const long long base = kvoff + (long long)key * D + cc;
+          ksrc = p.k + base;
+          vsrc = p.v + base;
+        }
+        kv = *reinterpret_cast<const u32x4*>(ksrc);
+        vv = *reinterpret_cast<const u32x4*>(vsrc);
+      }
+      *reinterpret_cast<u32x4*>(Ks + Tile<D>::off(r, cc)) = kv;
+      *reinterpret_cast<u32x4*>(Vs + Tile<D>::off(r, cc)) = vv;
+    }
+    __syncthreads();
+
+    // S^T for two 32-key blocks
+    f32x16 s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      s[kb] = zero16();
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk)
+        s[kb] = mfma32(lds_row8<D>(Ks, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), qf[kk], s[kb]);
+    }
+
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        float x = s[kb][i] * c;
+        if (!full) {
+          const int key = k0 + kb * 32 + acc_row(i, lane);
+          const bool ok = key < e1 || (key >= s2 && key < e2);
+          x = ok ? x : -INFINITY;
+        }
+        s[kb][i] = x;
+        mx = fmaxf(mx, x);
+      }
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mnew = fmaxf(m, mx);
+    const float msafe = (mnew == -INFINITY) ? 0.f : mnew;
+    const float alpha = exp2f(m - msafe);
+    float ls = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float pv = exp2f(s[kb][i] - msafe);
+        s[kb][i] = pv;
+        ls += pv;
+      }
+    }
+    lsum = lsum * alpha + ls;
+    m = mnew;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
+    }
+
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const bf16x8 pb = pack8(s[kb], t);
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          o[db] = mfma32(lds_tr8<D>(Vs, kb * 32, t, db * 32, lane), pb, o[db]);
+      }
+    }
+  }
+
+  lsum += __shfl_xor(lsum, 32);
+  if (qrow < p.Tq) {
+    const float inv = 1.f / lsum;
+    bf16_t* orow = p.o + qoff + (long long)qrow * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        bf16x4 w;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w[j] = to_bf16(o[db][4 * g + j] * inv);
+        *reinterpret_cast<bf16x4*>(orow + db * 32 + 8 * g + 4 * (lane >> 5)) = w;
+      }
+    }
+    if (p.lse != nullptr && lane < 32) {
+      p.lse[(long long)bh * p.Tq + qrow] = (m + __log2f(lsum)) * 0.69314718055994530942f;
+    }
+  }
+}
+
+hipError_t launch_fwd(const FwdParams& p, int D, bool cached, hipStream_t stream) {
+  const dim3 grid(p.n_qtiles * p.BH), block(256);
+  if (D == 64) {
+    if (cached) hipLaunchKernelGGL((attn_fwd_kernel<64, true>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((attn_fwd_kernel<64, false>), grid, block, 0, stream, p);
+  } else {
+    if (cached) hipLaunchKernelGGL((attn_fwd_kernel<128, true>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((attn_fwd_kernel<128, false>), grid, block, 0, stream, p);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mw

@@ -1,0 +1,250 @@
+// C ABI of the library (declared in include/mw.h): argument validation, ring
+// bookkeeping and kernel launches.  No device memory is allocated here.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "../../include/mw.h"
+#include "mw_kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return MW_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int kMaxT = 1 << 24;  // keeps every in-kernel row * D index within 32 bits
+
+int check_ptrs(const char* fn, std::initializer_list<std::pair<const char*, const void*>> ptrs) {
+  for (auto& pr : ptrs)
+    if (pr.second == nullptr) return fail(MW_EINVAL, "%s: %s is NULL", fn, pr.first);
+  for (auto& pr : ptrs)
+    if (!aligned16(pr.second)) return fail(MW_EALIGN, "%s: %s is not 16-byte aligned", fn, pr.first);
+  return MW_OK;
+}
+
+int check_train_dims(const char* fn, int B, int H, int T, int D, int chunk_len, float scale) {
+  if (B < 1 || H < 1 || T < 1 || chunk_len < 1)
+    return fail(MW_EINVAL, "%s: B, H, T and chunk_len must be >= 1 (got %d, %d, %d, %d)", fn, B, H, T, chunk_len);
+  if (D != 64 && D != 128) return fail(MW_EUNSUPPORTED, "%s: head dimension %d is not supported (64 or 128)", fn, D);
+  if (T > kMaxT) return fail(MW_EUNSUPPORTED, "%s: T = %d exceeds %d", fn, T, kMaxT);
+  if ((long long)B * H > (1LL << 24)) return fail(MW_EUNSUPPORTED, "%s: B*H too large", fn);
+  if (!(scale > 0.f) || !std::isfinite(scale)) return fail(MW_EINVAL, "%s: scale must be finite and > 0", fn);
+  return MW_OK;
+}
+
+int hip_status(const char* fn, hipError_t e) {
+  if (e != hipSuccess) return fail(MW_EHIP, "%s: HIP error %s", fn, hipGetErrorString(e));
+  return ok();
+}
+
+const float kLog2e = 1.4426950408889634f;
+
+}  // namespace
+
+extern "C" {
+
+const char* mw_last_error(void) { return g_err.c_str(); }
+
+int mw_version(void) { return 100; }
+
+int mw_block_causal_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int T,
+                             int D, int chunk_len, float scale, mw_stream_t stream) {
+  const char* fn = "mw_block_causal_attn_fwd";
+  int st = check_ptrs(fn, {{"q", q}, {"k", k}, {"v", v}, {"o", o}, {"lse", lse}});
+  if (st) return st;
+  st = check_train_dims(fn, B, H, T, D, chunk_len, scale);
+  if (st) return st;
+  mw::FwdParams p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k);
+  p.v = static_cast<const uint16_t*>(v);
+  p.o = static_cast<uint16_t*>(o);
+  p.lse = lse;
+  p.BH = B * H;
+  p.Tq = T;
+  p.n_qtiles = (T + mw::FWD_BM - 1) / mw::FWD_BM;
+  p.vis_mode = 0;
+  p.L = chunk_len > T ? T : chunk_len;
+  p.Tk = T;
+  p.qlen = 1;
+  p.wL = 0;
+  p.scale_log2 = scale * kLog2e;
+  p.scale_ln = scale;
+  return hip_status(fn, mw::launch_fwd(p, D, false, static_cast<hipStream_t>(stream)));
+}
+
+size_t mw_block_causal_attn_bwd_workspace_size(int B, int H, int T, int D) {
+  (void)D;
+  if (B < 1 || H < 1 || T < 1) return 0;
+  const size_t bytes = (size_t)B * H * T * sizeof(float);
+  return (bytes + 255) & ~(size_t)255;
+}
+
+int mw_block_causal_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* d_o,
+                             const float* lse, void* dq, void* dk, void* dv, void* workspace, size_t workspace_bytes,
+                             int B, int H, int T, int D, int chunk_len, float scale, mw_stream_t stream) {
+  const char* fn = "mw_block_causal_attn_bwd";
+  int st = check_ptrs(fn, {{"q", q}, {"k", k}, {"v", v}, {"o", o}, {"d_o", d_o}, {"lse", lse}, {"dq", dq},
+                           {"dk", dk}, {"dv", dv}, {"workspace", workspace}});
+  if (st) return st;
+  st = check_train_dims(fn, B, H, T, D, chunk_len, scale);
+  if (st) return st;
+  const size_t need = mw_block_causal_attn_bwd_workspace_size(B, H, T, D);
+  if (workspace_bytes < need)
+    return fail(MW_EINVAL, "%s: workspace of %zu bytes is smaller than the %zu bytes needed", fn, workspace_bytes,
+                need);
+  mw::BwdParams p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k);
+  p.v = static_cast<const uint16_t*>(v);
+  p.o = static_cast<const uint16_t*>(o);
+  p.d_o = static_cast<const uint16_t*>(d_o);
+  p.lse = lse;
+  p.delta = static_cast<float*>(workspace);
+  p.dq = static_cast<uint16_t*>(dq);
+  p.dk = static_cast<uint16_t*>(dk);
+  p.dv = static_cast<uint16_t*>(dv);
+  p.BH = B * H;
+  p.T = T;
+  p.L = chunk_len > T ? T : chunk_len;
+  p.scale = scale;
+  p.scale_log2 = scale * kLog2e;
+  return hip_status(fn, mw::launch_bwd(p, D, static_cast<hipStream_t>(stream)));
+}
+
+int mw_kvcache_init(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, int H, int L, int D) {
+  const char* fn = "mw_kvcache_init";
+  if (c == nullptr) return fail(MW_EINVAL, "%s: cache is NULL", fn);
+  int st = check_ptrs(fn, {{"k_slots", k_slots}, {"v_slots", v_slots}});
+  if (st) return st;
+  if (S < 1 || B < 1 || H < 1 || L < 1)
+    return fail(MW_EINVAL, "%s: S, B, H and L must be >= 1 (got %d, %d, %d, %d)", fn, S, B, H, L);
+  if (D != 64 && D != 128) return fail(MW_EUNSUPPORTED, "%s: head dimension %d is not supported (64 or 128)", fn, D);
+  if ((long long)L * S > kMaxT) return fail(MW_EUNSUPPORTED, "%s: S*L exceeds %d tokens", fn, kMaxT);
+  c->k_slots = k_slots;
+  c->v_slots = v_slots;
+  c->S = S;
+  c->B = B;
+  c->H = H;
+  c->L = L;
+  c->D = D;
+  c->head = 0;
+  c->tail = 0;
+  return ok();
+}
+
+static int check_cache(const char* fn, const mw_kvcache* c) {
+  if (c == nullptr) return fail(MW_EINVAL, "%s: cache is NULL", fn);
+  if (c->k_slots == nullptr || c->v_slots == nullptr || c->S < 1 || c->B < 1 || c->H < 1 || c->L < 1 ||
+      (c->D != 64 && c->D != 128) || c->tail < 0 || c->head < c->tail || c->head - c->tail > c->S)
+    return fail(MW_EINVAL, "%s: cache descriptor is not initialised or is corrupt", fn);
+  return MW_OK;
+}
+
+int mw_kvcache_append(mw_kvcache* c, const void* k_chunk, const void* v_chunk, mw_stream_t stream) {
+  const char* fn = "mw_kvcache_append";
+  int st = check_cache(fn, c);
+  if (st) return st;
+  st = check_ptrs(fn, {{"k_chunk", k_chunk}, {"v_chunk", v_chunk}});
+  if (st) return st;
+  if (c->head - c->tail == c->S) return fail(MW_EFULL, "%s: all %d slots hold live chunks; evict first", fn, c->S);
+  const long long n = (long long)c->B * c->H * c->L * c->D;
+  const int slot = (int)(c->head % c->S);
+  uint16_t* kd = static_cast<uint16_t*>(c->k_slots) + (long long)slot * n;
+  uint16_t* vd = static_cast<uint16_t*>(c->v_slots) + (long long)slot * n;
+  hipError_t e = mw::launch_kv_copy(static_cast<const uint16_t*>(k_chunk), static_cast<const uint16_t*>(v_chunk),
+                                    kd, vd, n, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_status(fn, e);
+  c->head += 1;
+  return ok();
+}
+
+int mw_kvcache_evict(mw_kvcache* c, int n_chunks) {
+  const char* fn = "mw_kvcache_evict";
+  int st = check_cache(fn, c);
+  if (st) return st;
+  if (n_chunks < 0) return fail(MW_EINVAL, "%s: n_chunks must be >= 0", fn);
+  if (n_chunks > c->head - c->tail)
+    return fail(MW_EEMPTY, "%s: cannot evict %d chunks, only %lld are live", fn, n_chunks,
+                (long long)(c->head - c->tail));
+  c->tail += n_chunks;
+  return ok();
+}
+
+int mw_kvcache_live(const mw_kvcache* c) {
+  int st = check_cache("mw_kvcache_live", c);
+  if (st) return st;
+  return (int)(c->head - c->tail);
+}
+
+int mw_kvcache_slot_of(const mw_kvcache* c, int64_t chunk) {
+  if (c == nullptr || c->S < 1) return -1;
+  if (chunk < c->tail || chunk >= c->head) return -1;
+  return (int)(chunk % c->S);
+}
+
+int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new, int n_queued, int q_len,
+                         const mw_kvcache* c, int window, int flags, void* o, float* lse, float scale,
+                         mw_stream_t stream) {
+  const char* fn = "mw_chunk_attn_cached";
+  int st = check_cache(fn, c);
+  if (st) return st;
+  st = check_ptrs(fn, {{"q", q}, {"k_new", k_new}, {"v_new", v_new}, {"o", o}});
+  if (st) return st;
+  if (lse != nullptr && !aligned16(lse)) return fail(MW_EALIGN, "%s: lse is not 16-byte aligned", fn);
+  if (n_queued < 1 || q_len < 1) return fail(MW_EINVAL, "%s: n_queued and q_len must be >= 1", fn);
+  if (flags != MW_QUEUED_CAUSAL && flags != MW_QUEUED_ISOLATED) return fail(MW_EINVAL, "%s: unknown flags %d", fn, flags);
+  if (!(scale > 0.f) || !std::isfinite(scale)) return fail(MW_EINVAL, "%s: scale must be finite and > 0", fn);
+  const long long live = c->head - c->tail;
+  if (window < -1) return fail(MW_EINVAL, "%s: window must be >= -1", fn);
+  const long long w = window == -1 ? live : window;
+  if (w > live) return fail(MW_EINVAL, "%s: window %d exceeds the %lld live chunks", fn, window, live);
+  if (w > MW_MAX_WINDOW) return fail(MW_EUNSUPPORTED, "%s: window %lld exceeds %d", fn, w, MW_MAX_WINDOW);
+  if (n_queued > MW_MAX_QUEUED) return fail(MW_EUNSUPPORTED, "%s: n_queued %d exceeds %d", fn, n_queued, MW_MAX_QUEUED);
+  const long long nq_tok = (long long)n_queued * q_len;
+  if (nq_tok + w * c->L > kMaxT) return fail(MW_EUNSUPPORTED, "%s: too many tokens", fn);
+  mw::FwdParams p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k_new);
+  p.v = static_cast<const uint16_t*>(v_new);
+  p.o = static_cast<uint16_t*>(o);
+  p.lse = lse;
+  p.BH = c->B * c->H;
+  p.Tq = (int)nq_tok;
+  p.n_qtiles = (p.Tq + mw::FWD_BM - 1) / mw::FWD_BM;
+  p.vis_mode = flags == MW_QUEUED_CAUSAL ? 1 : 2;
+  p.L = c->L;
+  p.wL = (int)(w * c->L);
+  p.Tk = p.wL + p.Tq;
+  p.qlen = q_len;
+  p.scale_log2 = scale * kLog2e;
+  p.scale_ln = scale;
+  p.k_slots = static_cast<const uint16_t*>(c->k_slots);
+  p.v_slots = static_cast<const uint16_t*>(c->v_slots);
+  p.slot_stride = (long long)c->B * c->H * c->L * c->D;
+  p.S = c->S;
+  p.first_slot = (int)((c->head - w) % c->S);
+  return hip_status(fn, mw::launch_fwd(p, c->D, true, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,152 @@
+// Device-side building blocks shared by the attention kernels (gfx950 / CDNA4).
+//
+// Register layouts used throughout (64-lane wavefront, lane l):
+//   v_mfma_f32_32x32x16_bf16  D[32x32] += A[32x16] * B[16x32]
+//     A: lane l holds A[m = l%32][k = 8*(l/32) + j], j = 0..7
+//     B: lane l holds B[k = 8*(l/32) + j][n = l%32]
+//     C/D: lane l, register i holds C[m = 8*(i/4) + 4*(l/32) + i%4][n = l%32]
+//   ds_read_b64_tr_b16 (transposing LDS read, groups of 16 lanes): element j
+//     of lane i is element i%4 of the 8 bytes addressed by lane 4*j + i/4.
+//
+// An accumulator tile whose row index runs over a contraction dimension (keys
+// for P, queries for dS) is fed back to the next MFMA as its B operand without
+// any data movement: the 16 k-slots of contraction step t are bound to
+//   row(t, s) = 16*t + 4*(s/8) + 8*((s%8)/4) + s%4,     s = 0..15,
+// which is exactly the set of rows held in registers 8t..8t+7 of each lane.
+// The matching A operand is read from a row-major LDS tile with two
+// transposing reads (tr_row/tr_col below).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mw {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef uint16_t bf16_t;  // storage type of bf16 in global memory
+
+#define MW_LDS __attribute__((address_space(3)))
+
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.f;
+  return z;
+}
+
+// fp32 -> bf16, round to nearest even (finite inputs; +-inf map to +-inf).
+__device__ __forceinline__ __bf16 to_bf16(float x) { return (__bf16)x; }
+
+// 8 fp32 accumulator values (registers 8t..8t+7) -> one bf16x8 B operand.
+__device__ __forceinline__ bf16x8 pack8(const f32x16& c, int t) {
+  bf16x8 r;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) r[j] = to_bf16(c[8 * t + j]);
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+// LDS tiles: [rows][D] bf16, row-major, with the 16-byte slots of each row
+// permuted by an XOR swizzle so that both access patterns used by the kernels
+// spread over all banks:
+//   - row reads: lane l reads 16 bytes of row l%32 (MFMA A/B operands);
+//   - transposing reads: 8 consecutive rows x 64 bytes per instruction.
+// ---------------------------------------------------------------------------
+template <int D>
+struct Tile {
+  static constexpr int SLOTS = D / 8;  // 16-byte slots per row
+  __device__ __forceinline__ static int swz(int row) {
+    if constexpr (D == 128) {
+      return 4 * (row & 3) + ((row >> 2) & 3);
+    } else {
+      const int u = row >> 1;
+      return 4 * (u & 1) + ((u >> 1) & 3);
+    }
+  }
+  // element offset of (row, col); col % 4 must be 0 for 8-byte and col % 8 for 16-byte access
+  __device__ __forceinline__ static int off(int row, int col) {
+    return row * D + ((((col >> 3) ^ swz(row)) << 3) | (col & 7));
+  }
+};
+
+// 16-byte load of the A/B operand "row r, columns c..c+7" from an LDS tile.
+template <int D>
+__device__ __forceinline__ bf16x8 lds_row8(const bf16_t* tile, int r, int c) {
+  return *reinterpret_cast<const bf16x8*>(tile + Tile<D>::off(r, c));
+}
+
+// A operand [m = column of the tile][k = slot] for contraction step t, taken
+// from an LDS tile whose rows are the contraction index:
+//   lane l gets tile[row(t, 8*(l/32) + j)][c0 + l%32], j = 0..7,
+// with row() the slot binding described at the top of this file.  `rbase` is
+// the tile row of slot row 0 (a multiple of 32 plus 16*t is added inside).
+template <int D>
+__device__ __forceinline__ bf16x8 lds_tr8(const bf16_t* tile, int rbase, int t, int c0, int lane) {
+  const int rr = rbase + 16 * t + 4 * (lane >> 5) + ((lane & 15) >> 2);
+  const int cc = c0 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const bf16_t* p0 = tile + Tile<D>::off(rr, cc);
+  const bf16_t* p1 = tile + Tile<D>::off(rr + 8, cc);
+  i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((MW_LDS i16x4*)(p0));
+  i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((MW_LDS i16x4*)(p1));
+  bf16x8 r;
+  bf16x4 lo4 = __builtin_bit_cast(bf16x4, lo);
+  bf16x4 hi4 = __builtin_bit_cast(bf16x4, hi);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    r[j] = lo4[j];
+    r[4 + j] = hi4[j];
+  }
+  return r;
+}
+
+// Row (within a 32-row accumulator block) of accumulator register i in lane l.
+__device__ __forceinline__ int acc_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
+
+// ---------------------------------------------------------------------------
+// Visibility of key j to query row i.  Three rules share one form: key j is
+// visible iff j < e1 or s2 <= j < e2.
+//   BLOCK_CAUSAL  : chunk c = i / L; e1 = min(T, (c+1) L); second range empty.
+//   QUEUED_CAUSAL : queued chunk q = i / qlen; e1 = wL + (q+1) qlen.
+//   QUEUED_ISOL   : e1 = wL; [s2, e2) = [wL + q qlen, wL + (q+1) qlen).
+// Keys are positions in the (virtual) key sequence.
+// ---------------------------------------------------------------------------
+enum VisMode { VIS_BLOCK_CAUSAL = 0, VIS_QUEUED_CAUSAL = 1, VIS_QUEUED_ISOLATED = 2 };
+
+struct Vis {
+  int mode;
+  int L;      // chunk length (training) / committed chunk length (cached)
+  int Tk;     // number of keys
+  int qlen;   // queued chunk length (cached)
+  int wL;     // window tokens (cached)
+  __device__ __forceinline__ void range(int i, int& e1, int& s2, int& e2) const {
+    if (mode == VIS_BLOCK_CAUSAL) {
+      const int c = i / L;
+      e1 = min(Tk, (c + 1) * L);
+      s2 = e1;
+      e2 = e1;
+    } else {
+      const int qc = i / qlen;
+      if (mode == VIS_QUEUED_CAUSAL) {
+        e1 = wL + (qc + 1) * qlen;
+        s2 = e1;
+        e2 = e1;
+      } else {
+        e1 = wL;
+        s2 = wL + qc * qlen;
+        e2 = s2 + qlen;
+      }
+    }
+  }
+};
+
+}  // namespace mw

@@ -1,0 +1,166 @@
+"""Host-side checks of the C ABI: the library loads, exports every declared symbol, validates
+arguments before touching the device, and keeps ring bookkeeping that agrees with the ring model.
+
+Only calls that return before any HIP call are made (no GPU is needed).  Pointers passed here are
+fake host addresses that are never dereferenced.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+import paper_2608_01127_amd as mw
+from paper_2608_01127_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+A = 0x10000   # aligned fake pointer
+U = 0x10008   # misaligned fake pointer
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "mw.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mw_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = mw.load()
+    names = declared_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+        assert n in _lib.SIGNATURES, f"binding lacks {n}"
+    assert lib.mw_version() == 100
+
+
+def test_struct_layout_matches_header():
+    assert ctypes.sizeof(_lib.mw_kvcache) == 56
+    assert _lib.mw_kvcache.head.offset == 40 and _lib.mw_kvcache.tail.offset == 48
+
+
+def err():
+    return mw.load().mw_last_error().decode()
+
+
+def test_fwd_validation():
+    lib = mw.load()
+    f = lib.mw_block_causal_attn_fwd
+    assert f(None, A, A, A, A, 1, 1, 64, 64, 16, 0.125, None) == mw.MW_EINVAL and "q is NULL" in err()
+    assert f(A, A, U, A, A, 1, 1, 64, 64, 16, 0.125, None) == mw.MW_EALIGN and "v" in err()
+    assert f(A, A, A, A, A, 1, 1, 64, 96, 16, 0.125, None) == mw.MW_EUNSUPPORTED
+    assert f(A, A, A, A, A, 1, 1, 64, 64, 0, 0.125, None) == mw.MW_EINVAL
+    assert f(A, A, A, A, A, 0, 1, 64, 64, 4, 0.125, None) == mw.MW_EINVAL
+    assert f(A, A, A, A, A, 1, 1, 0, 64, 4, 0.125, None) == mw.MW_EINVAL
+    assert f(A, A, A, A, A, 1, 1, 64, 64, 4, 0.0, None) == mw.MW_EINVAL
+    assert f(A, A, A, A, A, 1, 1, 64, 64, 4, float("nan"), None) == mw.MW_EINVAL
+
+
+def test_bwd_validation_and_workspace():
+    lib = mw.load()
+    ws = lib.mw_block_causal_attn_bwd_workspace_size(2, 3, 100, 64)
+    assert ws >= 2 * 3 * 100 * 4 and ws % 256 == 0
+    assert lib.mw_block_causal_attn_bwd_workspace_size(0, 3, 100, 64) == 0
+    b = lib.mw_block_causal_attn_bwd
+    args = [A] * 10
+    assert b(*args, ws - 1, 2, 3, 100, 64, 10, 0.125, None) == mw.MW_EINVAL and "workspace" in err()
+    bad = list(args)
+    bad[4] = None
+    assert b(*bad, ws, 2, 3, 100, 64, 10, 0.125, None) == mw.MW_EINVAL
+    bad[4] = U
+    assert b(*bad, ws, 2, 3, 100, 64, 10, 0.125, None) == mw.MW_EALIGN
+    assert b(*args, ws, 2, 3, 100, 32, 10, 0.125, None) == mw.MW_EUNSUPPORTED
+
+
+def new_cache(S=8, B=1, H=2, L=16, D=64):
+    c = _lib.mw_kvcache()
+    assert mw.load().mw_kvcache_init(ctypes.byref(c), A, A, S, B, H, L, D) == mw.MW_OK
+    return c
+
+
+def test_kvcache_init_validation():
+    lib = mw.load()
+    c = _lib.mw_kvcache()
+    assert lib.mw_kvcache_init(None, A, A, 8, 1, 1, 16, 64) == mw.MW_EINVAL
+    assert lib.mw_kvcache_init(ctypes.byref(c), A, U, 8, 1, 1, 16, 64) == mw.MW_EALIGN
+    assert lib.mw_kvcache_init(ctypes.byref(c), A, A, 0, 1, 1, 16, 64) == mw.MW_EINVAL
+    assert lib.mw_kvcache_init(ctypes.byref(c), A, A, 8, 1, 1, 16, 80) == mw.MW_EUNSUPPORTED
+    c = new_cache()
+    assert (c.head, c.tail, c.S, c.L, c.D) == (0, 0, 8, 16, 64)
+
+
+def test_ring_bookkeeping_matches_model_300_steps():
+    """Commits are simulated by advancing `head` (the device copy is not run without a GPU);
+    eviction, live counts and slot lookup go through the C ABI and must match the model."""
+    lib = mw.load()
+    S, W = 8, 6
+    c = new_cache(S=S)
+    ring = oracle.RingModel(S)
+    for t in range(300):
+        ring.append()
+        c.head += 1
+        if ring.live > W:
+            n = ring.live - W
+            ring.evict(n)
+            assert lib.mw_kvcache_evict(ctypes.byref(c), n) == mw.MW_OK
+        assert lib.mw_kvcache_live(ctypes.byref(c)) == ring.live
+        for chunk in range(max(0, t - 12), t + 3):
+            assert lib.mw_kvcache_slot_of(ctypes.byref(c), chunk) == ring.slot_of(chunk)
+    assert (c.head, c.tail) == (ring.head, ring.tail)
+
+
+def test_ring_full_empty_and_window_errors():
+    lib = mw.load()
+    c = new_cache(S=3)
+    c.head = 3  # three live chunks: the ring is full
+    assert lib.mw_kvcache_append(ctypes.byref(c), A, A, None) == mw.MW_EFULL and "evict" in err()
+    assert c.head == 3
+    assert lib.mw_kvcache_evict(ctypes.byref(c), 4) == mw.MW_EEMPTY
+    assert lib.mw_kvcache_evict(ctypes.byref(c), -1) == mw.MW_EINVAL
+    assert c.tail == 0
+    cached = lib.mw_chunk_attn_cached
+    assert cached(A, A, A, 2, 16, ctypes.byref(c), 4, 0, A, None, 0.125, None) == mw.MW_EINVAL and "window" in err()
+    assert cached(A, A, A, 2, 16, ctypes.byref(c), -2, 0, A, None, 0.125, None) == mw.MW_EINVAL
+    assert cached(A, A, A, 2, 16, ctypes.byref(c), 1, 7, A, None, 0.125, None) == mw.MW_EINVAL
+    assert cached(A, A, A, 0, 16, ctypes.byref(c), 1, 0, A, None, 0.125, None) == mw.MW_EINVAL
+    assert cached(A, A, A, 2, 16, ctypes.byref(c), 1, 0, A, U, 0.125, None) == mw.MW_EALIGN
+    assert cached(A, None, A, 2, 16, ctypes.byref(c), 1, 0, A, None, 0.125, None) == mw.MW_EINVAL
+    assert cached(A, A, A, 65, 16, ctypes.byref(c), 1, 0, A, None, 0.125, None) == mw.MW_EUNSUPPORTED
+    # a corrupt descriptor is rejected
+    c.tail = 5
+    assert lib.mw_kvcache_evict(ctypes.byref(c), 0) == mw.MW_EINVAL
+    assert lib.mw_kvcache_slot_of(None, 0) == -1
+
+
+def test_snapshot_restore_descriptor():
+    """The descriptor is plain data: copying it snapshots the ring, copying it back restores it."""
+    lib = mw.load()
+    c = new_cache(S=5)
+    c.head = 4
+    lib.mw_kvcache_evict(ctypes.byref(c), 2)
+    snap = _lib.mw_kvcache.from_buffer_copy(c)
+    c.head += 3
+    lib.mw_kvcache_evict(ctypes.byref(c), 3)
+    ctypes.memmove(ctypes.byref(c), ctypes.byref(snap), ctypes.sizeof(c))
+    assert (c.head, c.tail) == (4, 2)
+    assert [lib.mw_kvcache_slot_of(ctypes.byref(c), i) for i in range(6)] == [-1, -1, 2, 3, -1, -1]
+
+
+def test_last_error_is_cleared_on_success():
+    lib = mw.load()
+    c = new_cache()
+    lib.mw_kvcache_evict(ctypes.byref(c), 1)
+    assert err()
+    assert lib.mw_kvcache_evict(ctypes.byref(c), 0) == mw.MW_OK
+    assert err() == ""
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    saved = _lib._lib
+    try:
+        _lib._lib = None
+        with pytest.raises(RuntimeError, match="not found"):
+            _lib.load(str(tmp_path / "nope.so"))
+    finally:
+        _lib._lib = saved
