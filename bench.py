@@ -1,0 +1,264 @@
+#!/usr/bin/env python3
+"""Benchmark of the block-causal attention hot path on one MI355X.
+
+One step runs every row of the hot path once:
+  training   : block-causal attention forward + backward, B=2 H=12 T=10560 D=64,
+               8 chunks of 1320 tokens (3 latent frames x 440 tokens);
+  streaming  : commit one 2640-token chunk to the 8-slot KV ring, evict down to a
+               6-chunk window, and cached attention of 4 queued in-flight chunks
+               (2640 tokens each, B=1 H=16 D=128) over that window.
+Inputs are seeded synthetic N(0,1) bf16 tensors resident in HBM before timing.
+
+Prints one JSON line.  `value` is the training forward+backward throughput in
+useful TFLOP/s (4 P D forward + 10 P D backward, P = visible query-key pairs),
+timed with HIP events on the launch stream over the K timed steps.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def pairs_block_causal(B, H, T, L):
+    """Visible (query, key) pairs of block-causal attention."""
+    n = -(-T // L)
+    tot = 0
+    for c in range(n):
+        rows = min(T, (c + 1) * L) - c * L
+        tot += rows * min(T, (c + 1) * L)
+    return B * H * tot
+
+
+def pairs_cached(B, H, w, L, nq, qlen, causal=True):
+    per = 0
+    for j in range(nq):
+        per += qlen * (w * L + ((j + 1) if causal else 1) * qlen)
+    return B * H * per
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing leg")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle sample duration")
+    return ap.parse_args()
+
+
+def source_digest(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(kernel: str, digest: str):
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary, if it was
+    taken on the current kernel source; None otherwise."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_sha") != digest:
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(target_s: float):
+    """The fp64 oracle, as it stands, on a bounded sample of the training workload:
+    forward + backward of whole heads of the D=64 shape, as many heads as fit in
+    about target_s seconds (at least one)."""
+    import numpy as np
+    import oracle
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    s = synth.TRAIN_D64
+    bits = synth.training_inputs(s)
+    t = {n: synth.bf16_bits_to_f64(bits[n]) for n in bits}
+    heads_done = 0
+    t0 = time.perf_counter()
+    for b in range(s.B):
+        for h in range(s.H):
+            sl = (slice(b, b + 1), slice(h, h + 1))
+            q, k, v, do = (t[n][sl] for n in ("q", "k", "v", "do"))
+            oracle.block_causal_attn_fwd(q, k, v, s.chunk_len)
+            oracle.block_causal_attn_bwd(q, k, v, do, s.chunk_len)
+            heads_done += 1
+            if time.perf_counter() - t0 >= target_s:
+                break
+        if time.perf_counter() - t0 >= target_s:
+            break
+    dt = time.perf_counter() - t0
+    flops = 14.0 * pairs_block_causal(1, heads_done, s.T, s.chunk_len) * s.D
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"fp64 numpy oracle fwd+bwd of {heads_done} of {s.B * s.H} heads of {s.name} "
+                      f"({dt:.1f} s), useful-FLOP count as the GPU"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1"}))
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2608_01127_amd as mw
+    import synth
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    mw.load()
+
+    def up(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    # ------------------------------------------------------------------ inputs (resident in HBM)
+    tr = synth.TRAIN_D64
+    tb = synth.training_inputs(tr)
+    q, k, v, do = (up(tb[n]) for n in ("q", "k", "v", "do"))
+    B, H, T, D, L = tr.B, tr.H, tr.T, tr.D, tr.chunk_len
+    o = torch.empty_like(q)
+    lse = torch.empty((B, H, T), dtype=torch.float32, device=dev)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    ws = torch.empty(mw.mw_block_causal_attn_bwd_workspace_size(B, H, T, D), dtype=torch.uint8, device=dev)
+
+    st = synth.STREAM
+    cache = mw.KVCache(st.slots, st.B, st.H, st.chunk_len, st.D, device=dev)
+    n_src = 4  # distinct commit sources, rotated
+    commits = []
+    for i in range(n_src):
+        cb = synth.stream_step_inputs(st, i, which=("k_commit", "v_commit"))
+        commits.append((up(cb["k_commit"]), up(cb["v_commit"])))
+    sb = synth.stream_step_inputs(st, 0, which=("q", "k_new", "v_new"))
+    sq, skn, svn = (up(sb[n]) for n in ("q", "k_new", "v_new"))
+    so = torch.empty_like(sq)
+    for i in range(st.window):
+        mw.mw_kvcache_append(cache, *commits[i % n_src])
+    torch.cuda.synchronize()
+
+    P_train = pairs_block_causal(B, H, T, L)
+    F_fwd, F_bwd = 4.0 * P_train * D, 10.0 * P_train * D
+    P_st = pairs_cached(st.B, st.H, st.window, st.chunk_len, st.n_queued, st.q_len, causal=True)
+    F_st = 4.0 * P_st * st.D
+    chunk_bytes = st.B * st.H * st.chunk_len * st.D * 2
+    bytes_append = 4 * chunk_bytes                       # read K,V chunk + write K,V slot
+    bytes_cached = (4 * st.B * st.H * st.n_queued * st.q_len * st.D * 2   # Q, K_new, V_new, O
+                    + 2 * st.window * chunk_bytes)                         # window K, V
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    step_i = [0]
+
+    def step(rec=None):
+        e = [ev() for _ in range(5)] if rec is not None else None
+        if e: e[0].record()
+        mw.mw_block_causal_attn_fwd(q, k, v, L, out=o, lse=lse)
+        if e: e[1].record()
+        mw.mw_block_causal_attn_bwd(q, k, v, o, do, lse, L, workspace=ws, dq=dq, dk=dk, dv=dv)
+        if e: e[2].record()
+        mw.mw_kvcache_append(cache, *commits[step_i[0] % n_src])
+        step_i[0] += 1
+        if e: e[3].record()
+        mw.mw_kvcache_evict(cache, cache.live - st.window)
+        mw.mw_chunk_attn_cached(sq, skn, svn, st.n_queued, st.q_len, cache, window=st.window,
+                                flags=mw.MW_QUEUED_CAUSAL, out=so)
+        if e: e[4].record()
+        if rec is not None:
+            rec.append(e)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    recs = []
+    t_start, t_end = ev(), ev()
+    torch.cuda.synchronize()
+    t_start.record()
+    for _ in range(args.steps):
+        step(recs)
+    t_end.record()
+    torch.cuda.synchronize()
+    K = args.steps
+    total_ms = t_start.elapsed_time(t_end)
+    ph = {"fwd": 0.0, "bwd": 0.0, "append": 0.0, "cached": 0.0}
+    for e in recs:
+        ph["fwd"] += e[0].elapsed_time(e[1])
+        ph["bwd"] += e[1].elapsed_time(e[2])
+        ph["append"] += e[2].elapsed_time(e[3])
+        ph["cached"] += e[3].elapsed_time(e[4])
+    ph = {n: t / K for n, t in ph.items()}
+    ms_step = total_ms / K
+    train_ms = ph["fwd"] + ph["bwd"]
+    value = (F_fwd + F_bwd) / (train_ms * 1e-3) / 1e12
+
+    # dominant single-kernel launch of the step: the cached-attention kernel (one launch per call)
+    cached_tflops = F_st / (ph["cached"] * 1e-3) / 1e12
+    digest = source_digest(["paper_2608_01127_amd/csrc/attn_fwd.hip", "paper_2608_01127_amd/csrc/mw_device.h"])
+    traffic = read_traffic("attn_fwd_cached", digest)
+    roofline = {"kernel": "attn_fwd_kernel<128,true> (cached chunk attention)", "bound": "mfma",
+                "achieved": round(cached_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(cached_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
+                "algorithmic_flops_per_launch": F_st, "avg_launch_ms": round(ph["cached"], 4)}
+
+    res = {
+        "metric": "block-causal attn fwd+bwd TFLOP/s (% bf16 MFMA peak); cached-chunk attn GB/s",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{tr.name} fwd+bwd + {st.name} streaming step",
+                   "train": {"B": B, "H": H, "T": T, "D": D, "chunk_len": L},
+                   "stream": {"B": st.B, "H": st.H, "D": st.D, "chunk_len": st.chunk_len, "n_queued": st.n_queued,
+                              "q_len": st.q_len, "window": st.window, "slots": st.slots,
+                              "visibility": "queued-causal"}},
+        "frac_bf16_peak": round(value / PEAK_BF16_TFLOPS, 4),
+        "phases_ms": {n: round(t, 4) for n, t in ph.items()},
+        "train_fwd_tflops": round(F_fwd / (ph["fwd"] * 1e-3) / 1e12, 2),
+        "train_bwd_tflops": round(F_bwd / (ph["bwd"] * 1e-3) / 1e12, 2),
+        "cached_attn": {"tflops": round(cached_tflops, 2), "gbs": round(bytes_cached / (ph["cached"] * 1e-3) / 1e9, 1),
+                        "frac_bf16_peak": round(cached_tflops / PEAK_BF16_TFLOPS, 4)},
+        "append": {"gbs": round(bytes_append / (ph["append"] * 1e-3) / 1e9, 1),
+                   "frac_hbm_peak": round(bytes_append / (ph["append"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+    else:
+        res["cpu_baseline"] = None
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

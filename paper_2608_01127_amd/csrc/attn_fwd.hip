@@ -33,14 +33,77 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
   return (bid % 8) * (n / 8) + bid / 8;
 }
 
+// Staging of one K/V tile: each thread moves BN*D/(8*NT) 16-byte chunks of K and
+// of V.  Loads go to registers first so that the next tile's global traffic
+// overlaps the current tile's MFMA and softmax work.
+template <int D, bool CACHED>
+struct KVStage {
+  static constexpr int NT = 256;
+  static constexpr int CPR = D / 8;
+  static constexpr int PER = FWD_BN * CPR / NT;  // chunks per thread per tensor
+  u32x4 kr[PER], vr[PER];
+
+  __device__ __forceinline__ void load(const FwdParams& p, int bh, long long kvoff, int k0, int tid) {
+    const bool interior = k0 + FWD_BN <= p.Tk;
+#pragma unroll
+    for (int it = 0; it < PER; ++it) {
+      const int ci = tid + NT * it;
+      const int r = ci / CPR, cc = (ci % CPR) * 8;
+      const int key = k0 + r;
+      if (interior || key < p.Tk) {
+        const uint16_t *ksrc, *vsrc;
+        if constexpr (CACHED) {
+          if (key < p.wL) {
+            const int w = key / p.L, off = key - w * p.L;
+            int slot = p.first_slot + w;
+            slot = slot >= p.S ? slot - p.S : slot;
+            const long long base =
+                (long long)slot * p.slot_stride + (long long)bh * p.L * D + (long long)off * D + cc;
+            ksrc = p.k_slots + base;
+            vsrc = p.v_slots + base;
+          } else {
+            const long long base = kvoff + (long long)(key - p.wL) * D + cc;
+            ksrc = p.k + base;
+            vsrc = p.v + base;
+          }
+        } else {
+          const long long base = kvoff + (long long)key * D + cc;
+          ksrc = p.k + base;
+          vsrc = p.v + base;
+        }
+        kr[it] = *reinterpret_cast<const u32x4*>(ksrc);
+        vr[it] = *reinterpret_cast<const u32x4*>(vsrc);
+      } else {
+        kr[it] = u32x4{0, 0, 0, 0};
+        vr[it] = u32x4{0, 0, 0, 0};
+      }
+    }
+  }
+  __device__ __forceinline__ void store(bf16_t* Ks, bf16_t* Vs, int tid) const {
+#pragma unroll
+    for (int it = 0; it < PER; ++it) {
+      const int ci = tid + NT * it;
+      const int r = ci / CPR, cc = (ci % CPR) * 8;
+      *reinterpret_cast<u32x4*>(Ks + Tile<D>::off(r, cc)) = kr[it];
+      *reinterpret_cast<u32x4*>(Vs + Tile<D>::off(r, cc)) = vr[it];
+    }
+  }
+};
+
+// Rows of the running max only move when a tile raises it by more than this
+// many powers of two; until then probabilities are taken against the stale
+// max (they stay below 2^8, far from fp32/bf16 limits).  The normaliser uses
+// the same reference, so the result is unchanged up to rounding, and the
+// O rescale is skipped on almost every step.
+constexpr float kRescaleThreshold = 8.f;
+
 template <int D, bool CACHED>
 __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
-  constexpr int BM = FWD_BM, BN = FWD_BN, NT = 256;
+  constexpr int BM = FWD_BM, BN = FWD_BN;
   constexpr int KK = D / 16;  // contraction steps over D
   constexpr int DB = D / 32;  // 32-wide column blocks of D
-  constexpr int CPR = D / 8;  // 16-byte chunks per row
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[BN * D];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[BN * D];
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BN * D];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][BN * D];
 
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = logical / p.n_qtiles;
@@ -70,6 +133,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   vis.range(q0, e1f, s2f, e2f);
   vis.range(min(q0 + BM, p.Tq) - 1, e1l, s2l, e2l);
   const int kend = max(e1l, e2l);
+  // next visited key tile after k: tiles no row of this workgroup can see are skipped
+  auto advance = [&](int k) {
+    int n = k + BN;
+    if (n >= e1l && n + BN <= s2f) n = (s2f / BN) * BN;
+    return n;
+  };
 
   f32x16 o[DB];
 #pragma unroll
@@ -79,92 +148,80 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
 
   const long long kvoff = (long long)bh * (CACHED ? (long long)p.Tq * D : (long long)p.Tk * D);
 
-  for (int k0 = 0; k0 < kend; k0 += BN) {
-    const bool skip = (k0 >= e1l) && (k0 + BN <= s2f || k0 >= e2l);
-    if (skip) continue;
+  KVStage<D, CACHED> stage;
+  int k0 = advance(-BN);
+  int buf = 0;
+  if (k0 < kend) {
+    stage.load(p, bh, kvoff, k0, tid);
+    stage.store(Ks[0], Vs[0], tid);
+  }
+  __syncthreads();
+
+  while (k0 < kend) {
+    const int kn = advance(k0);
+    if (kn < kend) stage.load(p, bh, kvoff, kn, tid);  // in flight during this step's math
+    const bf16_t* Kt = Ks[buf];
+    const bf16_t* Vt = Vs[buf];
     const bool full = (k0 + BN <= e1f) || (s2l <= k0 && k0 + BN <= e2f);
 
-    __syncthreads();  // previous tile fully consumed
-#pragma unroll
-    for (int it = 0; it < BN * CPR / NT; ++it) {
-      const int ci = tid + NT * it;
-      const int r = ci / CPR, cc = (ci % CPR) * 8;
-      const int key = k0 + r;
-      u32x4 kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
-      if (key < p.Tk) {
-        const uint16_t *ksrc, *vsrc;
-        if constexpr (CACHED) {
-          if (key < p.wL) {
-            const int w = key / p.L, off = key - w * p.L;
-            int slot = p.first_slot + w;
-            slot = slot >= p.S ? slot - p.S : slot;
-            const long long base = (long long)slot * p.slot_stride + (long long)bh * p.L * D + (long long)off * D + cc;
-            ksrc = p.k_slots + base;
-            vsrc = p.v_slots + base;
-          } else {
-            const long long base = kvoff + (long long)(key - p.wL) * D + cc;
-            ksrc = p.k + base;
-            vsrc = p.v + base;
-          }
-        } else {
-          const long long base = kvoff + (long long)key * D + cc;
-          ksrc = p.k + base;
-          vsrc = p.v + base;
-        }
-        kv = *reinterpret_cast<const u32x4*>(ksrc);
-        vv = *reinterpret_cast<const u32x4*>(vsrc);
-      }
-      *reinterpret_cast<u32x4*>(Ks + Tile<D>::off(r, cc)) = kv;
-      *reinterpret_cast<u32x4*>(Vs + Tile<D>::off(r, cc)) = vv;
-    }
-    __syncthreads();
-
-    // S^T for two 32-key blocks
+    // S^T for two 32-key blocks (independent accumulation chains interleaved)
     f32x16 s[2];
+    s[0] = zero16();
+    s[1] = zero16();
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      s[kb] = zero16();
+    for (int kk = 0; kk < KK; ++kk) {
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk)
-        s[kb] = mfma32(lds_row8<D>(Ks, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), qf[kk], s[kb]);
+      for (int kb = 0; kb < 2; ++kb)
+        s[kb] = mfma32(lds_row8<D>(Kt, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), qf[kk], s[kb]);
     }
 
+    if (!full) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = k0 + kb * 32 + acc_row(i, lane);
+          // non-short-circuit form: evaluated as compares and one select, without
+          // branches (a branchy lowering of the short-circuit form clobbered the
+          // accumulator element before the second range was tested)
+          const bool ok = (key < e1) | ((key >= s2) & (key < e2));
+          s[kb][i] = ok ? s[kb][i] : -INFINITY;
+        }
+      }
+    }
     float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float x = s[kb][i] * c;
-        if (!full) {
-          const int key = k0 + kb * 32 + acc_row(i, lane);
-          const bool ok = key < e1 || (key >= s2 && key < e2);
-          x = ok ? x : -INFINITY;
-        }
-        s[kb][i] = x;
-        mx = fmaxf(mx, x);
-      }
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mnew = fmaxf(m, mx);
-    const float msafe = (mnew == -INFINITY) ? 0.f : mnew;
-    const float alpha = exp2f(m - msafe);
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c;  // scaled row max of this tile (log2 units)
+    const bool need = mx > m + kRescaleThreshold;
+    if (wave_any(need)) {
+      // lanes that move their max rescale by 2^(m - mx) (0 while m is still -inf);
+      // the others keep alpha = 1 (their m may still be -inf: no -inf - -inf)
+      const float alpha = need ? fast_exp2(m - mx) : 1.f;
+      const float mnew = need ? mx : m;
+      lsum *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
+      }
+      m = mnew;
+    }
+    const float nm = (m == -INFINITY) ? 0.f : -m;
     float ls = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float pv = exp2f(s[kb][i] - msafe);
+        const float pv = fast_exp2(fmaf(s[kb][i], c, nm));
         s[kb][i] = pv;
         ls += pv;
       }
     }
-    lsum = lsum * alpha + ls;
-    m = mnew;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
-    }
+    lsum += ls;
 
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -173,9 +230,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
         const bf16x8 pb = pack8(s[kb], t);
 #pragma unroll
         for (int db = 0; db < DB; ++db)
-          o[db] = mfma32(lds_tr8<D>(Vs, kb * 32, t, db * 32, lane), pb, o[db]);
+          o[db] = mfma32(lds_tr8<D>(Vt, kb * 32, t, db * 32, lane), pb, o[db]);
       }
     }
+
+    if (kn < kend) stage.store(Ks[buf ^ 1], Vs[buf ^ 1], tid);
+    __syncthreads();
+    buf ^= 1;
+    k0 = kn;
   }
 
   lsum += __shfl_xor(lsum, 32);

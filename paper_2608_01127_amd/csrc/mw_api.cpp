@@ -8,7 +8,7 @@
 #include <cstdio>
 #include <string>
 
-#include "../../include/mw.h"
+#include "mw.h"
 #include "mw_kernels.h"
 
 namespace {

@@ -14,7 +14,7 @@
 //   row(t, s) = 16*t + 4*(s/8) + 8*((s%8)/4) + s%4,     s = 0..15,
 // which is exactly the set of rows held in registers 8t..8t+7 of each lane.
 // The matching A operand is read from a row-major LDS tile with two
-// transposing reads (tr_row/tr_col below).
+// transposing reads (lds_tr8 below).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -43,6 +43,13 @@ __device__ __forceinline__ f32x16 zero16() {
   for (int i = 0; i < 16; ++i) z[i] = 0.f;
   return z;
 }
+
+// 2^x with the hardware instruction (v_exp_f32): results below the normal range
+// flush to 0, which is harmless for softmax weights.  2^-inf = 0.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// True if `pred` holds in any lane of the wavefront (a wave-uniform value).
+__device__ __forceinline__ bool wave_any(bool pred) { return __builtin_amdgcn_ballot_w64(pred) != 0; }
 
 // fp32 -> bf16, round to nearest even (finite inputs; +-inf map to +-inf).
 __device__ __forceinline__ __bf16 to_bf16(float x) { return (__bf16)x; }
