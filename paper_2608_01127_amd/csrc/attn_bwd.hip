@@ -26,10 +26,12 @@ __device__ __forceinline__ int xcd_remap_b(int bid, int n) {
   return (bid % 8) * (n / 8) + bid / 8;
 }
 
-// Delta = rowsum(dO * O): one 16-byte chunk per thread, reduced over the row's lanes.
+// Row terms of the backward pass: Delta = rowsum(dO * O) and LSE scaled to
+// base 2 (LSE * log2 e), one 16-byte chunk per thread, reduced over the row's lanes.
 template <int D>
-__global__ __launch_bounds__(256) void bwd_delta_kernel(const uint16_t* __restrict__ o, const uint16_t* __restrict__ d_o,
-                                                        float* __restrict__ delta, long long n_rows) {
+__global__ __launch_bounds__(256) void bwd_rowterms_kernel(const uint16_t* __restrict__ o, const uint16_t* __restrict__ d_o,
+                                                           const float* __restrict__ lse, float* __restrict__ delta,
+                                                           float* __restrict__ lse2, long long n_rows) {
   constexpr int CPR = D / 8;  // lanes per row (8 or 16)
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long row = gid / CPR;
@@ -48,17 +50,23 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(const uint16_t* __restri
   }
 #pragma unroll
   for (int w = CPR / 2; w >= 1; w >>= 1) acc += __shfl_xor(acc, w);
-  if (row < n_rows && c == 0) delta[row] = acc;
+  if (row < n_rows && c == 0) {
+    delta[row] = acc;
+    lse2[row] = lse[row] * 1.4426950408889634f;
+  }
 }
 
+// D = 128 keeps 192 registers of per-wave state (K and V fragments, dK and dV
+// accumulators) and runs one wave per SIMD with the full register file; D = 64
+// fits two waves per SIMD.
 template <int D>
-__global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams p, int n_ktiles) {
-  constexpr int BN = DKV_BN, BM = DKV_BM, NT = 256;
-  constexpr int KK = D / 16, DB = D / 32, CPR = D / 8;
-  __shared__ __attribute__((aligned(16))) bf16_t Qs[BM * D];
-  __shared__ __attribute__((aligned(16))) bf16_t dOs[BM * D];
-  __shared__ __attribute__((aligned(16))) float lse_s[BM];
-  __shared__ __attribute__((aligned(16))) float dlt_s[BM];
+__global__ __launch_bounds__(256, D == 64 ? 2 : 1) void bwd_dkdv_kernel(BwdParams p, int n_ktiles) {
+  constexpr int BN = DKV_BN, BM = DKV_BM;
+  constexpr int KK = D / 16, DB = D / 32;
+  __shared__ __attribute__((aligned(16))) bf16_t Qs[2][BM * D];
+  __shared__ __attribute__((aligned(16))) bf16_t dOs[2][BM * D];
+  __shared__ __attribute__((aligned(16))) float lse_s[2][BM];
+  __shared__ __attribute__((aligned(16))) float dlt_s[2][BM];
 
   const int logical = xcd_remap_b(blockIdx.x, gridDim.x);
   const int bh = logical / n_ktiles;
@@ -68,21 +76,18 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams p, int n_kti
   const int k0 = kt * BN;
   const int mykey = k0 + wave * 32 + (lane & 31);
   const long long off = (long long)bh * T * D;
+  const float* lse2_bh = p.lse2 + (long long)bh * T;
+  const float* dlt_bh = p.delta + (long long)bh * T;
 
-  // K and V fragments: B operands of S = Q K^T and dP = dO V^T.
+  // K and V fragments: B operands of S = Q K^T and dP = dO V^T.  Keys past T
+  // read the last key; their dK/dV are never stored.
   bf16x8 kf[KK], vf[KK];
+  {
+    const long long a0 = off + (long long)min(mykey, T - 1) * D + 8 * (lane >> 5);
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) {
-    if (mykey < T) {
-      const long long a = off + (long long)mykey * D + 16 * kk + 8 * (lane >> 5);
-      kf[kk] = *reinterpret_cast<const bf16x8*>(p.k + a);
-      vf[kk] = *reinterpret_cast<const bf16x8*>(p.v + a);
-    } else {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        kf[kk][j] = (__bf16)0.f;
-        vf[kk][j] = (__bf16)0.f;
-      }
+    for (int kk = 0; kk < KK; ++kk) {
+      kf[kk] = *reinterpret_cast<const bf16x8*>(p.k + a0 + 16 * kk);
+      vf[kk] = *reinterpret_cast<const bf16x8*>(p.v + a0 + 16 * kk);
     }
   }
   f32x16 dv[DB], dk[DB];
@@ -96,52 +101,46 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams p, int n_kti
   const int qstart = ((k0 / L) * L / BM) * BM;  // first query tile with a query of chunk >= chunk(k0)
   const float c = p.scale_log2;
 
+  auto stage = [&](int q0, int b) {
+    stage_rows_direct<D, BM>(Qs[b], [&](int r) { return p.q + off + (long long)min(q0 + r, T - 1) * D; }, tid);
+    stage_rows_direct<D, BM>(dOs[b], [&](int r) { return p.d_o + off + (long long)min(q0 + r, T - 1) * D; }, tid);
+    if (wave == 0) stage_f32x64_direct(lse_s[b], lse2_bh, q0, T, lane);
+    if (wave == 1) stage_f32x64_direct(dlt_s[b], dlt_bh, q0, T, lane);
+  };
+
+  int buf = 0;
+  if (qstart < T) stage(qstart, 0);
+  wait_vmem();
+  __syncthreads();
+
   for (int q0 = qstart; q0 < T; q0 += BM) {
-    const bool full = (q0 / L) >= (klast / L);
-    __syncthreads();
-#pragma unroll
-    for (int it = 0; it < BM * CPR / NT; ++it) {
-      const int ci = tid + NT * it;
-      const int r = ci / CPR, cc = (ci % CPR) * 8;
-      const int q = q0 + r;
-      u32x4 qv = {0, 0, 0, 0}, dov = {0, 0, 0, 0};
-      if (q < T) {
-        const long long a = off + (long long)q * D + cc;
-        qv = *reinterpret_cast<const u32x4*>(p.q + a);
-        dov = *reinterpret_cast<const u32x4*>(p.d_o + a);
-      }
-      *reinterpret_cast<u32x4*>(Qs + Tile<D>::off(r, cc)) = qv;
-      *reinterpret_cast<u32x4*>(dOs + Tile<D>::off(r, cc)) = dov;
-    }
-    if (tid < BM) {
-      const int q = q0 + tid;
-      // padding rows get LSE = +inf, so their probabilities are exactly 0
-      lse_s[tid] = q < T ? p.lse[(long long)bh * T + q] * 1.4426950408889634f : INFINITY;
-      dlt_s[tid] = q < T ? p.delta[(long long)bh * T + q] : 0.f;
-    }
-    __syncthreads();
+    if (q0 + BM < T) stage(q0 + BM, buf ^ 1);  // next query tile streams in during this one
+    const bf16_t* Qt = Qs[buf];
+    const bf16_t* dOt = dOs[buf];
+    // every (query, key) pair of this step visible and every query row real?
+    const bool full = ((q0 / L) >= (klast / L)) & (q0 + BM <= T);
 
 #pragma unroll
     for (int qb = 0; qb < BM / 32; ++qb) {
       f32x16 s = zero16(), dp = zero16();
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        s = mfma32(lds_row8<D>(Qs, qb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), kf[kk], s);
-        dp = mfma32(lds_row8<D>(dOs, qb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), vf[kk], dp);
+        s = mfma32(lds_row8<D>(Qt, qb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), kf[kk], s);
+        dp = mfma32(lds_row8<D>(dOt, qb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), vf[kk], dp);
       }
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int rr = qb * 32 + 8 * g + 4 * (lane >> 5);
-        const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse_s + rr);
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(dlt_s + rr);
+        const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse_s[buf][rr]);
+        const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dlt_s[buf][rr]);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int i = 4 * g + j;
-          float pv = exp2f(fmaf(s[i], c, -l4[j]));
+          float pv = fast_exp2(fmaf(s[i], c, -l4[j]));
           if (!full) {
             const int q = q0 + rr + j;
-            const int e1 = min(T, (q / L + 1) * L);
-            pv = mykey < e1 ? pv : 0.f;
+            const bool ok = (q < T) & (mykey < min(T, (q / L + 1) * L));
+            pv = ok ? pv : 0.f;
           }
           s[i] = pv;
           dp[i] = pv * (dp[i] - d4[j]);
@@ -153,11 +152,14 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams p, int n_kti
         const bf16x8 dsb = pack8(dp, t);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          dv[db] = mfma32(lds_tr8<D>(dOs, qb * 32, t, db * 32, lane), pb, dv[db]);
-          dk[db] = mfma32(lds_tr8<D>(Qs, qb * 32, t, db * 32, lane), dsb, dk[db]);
+          dv[db] = mfma32(lds_tr8<D>(dOt, qb * 32, t, db * 32, lane), pb, dv[db]);
+          dk[db] = mfma32(lds_tr8<D>(Qt, qb * 32, t, db * 32, lane), dsb, dk[db]);
         }
       }
     }
+    wait_vmem();
+    __syncthreads();
+    buf ^= 1;
   }
 
   if (mykey < T) {
@@ -183,10 +185,10 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams p, int n_kti
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p, int n_qtiles) {
-  constexpr int BM = DQ_BM, BN = DQ_BN, NT = 256;
-  constexpr int KK = D / 16, DB = D / 32, CPR = D / 8;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[BN * D];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[BN * D];
+  constexpr int BM = DQ_BM, BN = DQ_BN;
+  constexpr int KK = D / 16, DB = D / 32;
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BN * D];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][BN * D];
 
   const int logical = xcd_remap_b(blockIdx.x, gridDim.x);
   const int bh = logical / n_qtiles;
@@ -198,22 +200,16 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p, int n_qtile
   const long long off = (long long)bh * T * D;
 
   bf16x8 qf[KK], df[KK];
+  {
+    const long long a0 = off + (long long)min(qrow, T - 1) * D + 8 * (lane >> 5);
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) {
-    if (qrow < T) {
-      const long long a = off + (long long)qrow * D + 16 * kk + 8 * (lane >> 5);
-      qf[kk] = *reinterpret_cast<const bf16x8*>(p.q + a);
-      df[kk] = *reinterpret_cast<const bf16x8*>(p.d_o + a);
-    } else {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        qf[kk][j] = (__bf16)0.f;
-        df[kk][j] = (__bf16)0.f;
-      }
+    for (int kk = 0; kk < KK; ++kk) {
+      qf[kk] = *reinterpret_cast<const bf16x8*>(p.q + a0 + 16 * kk);
+      df[kk] = *reinterpret_cast<const bf16x8*>(p.d_o + a0 + 16 * kk);
     }
   }
-  const float lse2 = qrow < T ? p.lse[(long long)bh * T + qrow] * 1.4426950408889634f : INFINITY;
-  const float dlt = qrow < T ? p.delta[(long long)bh * T + qrow] : 0.f;
+  const float lse2 = p.lse2[(long long)bh * T + min(qrow, T - 1)];
+  const float dlt = p.delta[(long long)bh * T + min(qrow, T - 1)];
   const int e1 = min(T, (min(qrow, T - 1) / L + 1) * L);
   const int e1f = min(T, (q0 / L + 1) * L);
   const int kend = min(T, ((min(q0 + BM, T) - 1) / L + 1) * L);
@@ -223,36 +219,32 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p, int n_qtile
 #pragma unroll
   for (int db = 0; db < DB; ++db) dq[db] = zero16();
 
+  auto stage = [&](int k0, int b) {
+    stage_rows_direct<D, BN>(Ks[b], [&](int r) { return p.k + off + (long long)min(k0 + r, T - 1) * D; }, tid);
+    stage_rows_direct<D, BN>(Vs[b], [&](int r) { return p.v + off + (long long)min(k0 + r, T - 1) * D; }, tid);
+  };
+  int buf = 0;
+  stage(0, 0);
+  wait_vmem();
+  __syncthreads();
+
   for (int k0 = 0; k0 < kend; k0 += BN) {
+    if (k0 + BN < kend) stage(k0 + BN, buf ^ 1);
+    const bf16_t* Kt = Ks[buf];
+    const bf16_t* Vt = Vs[buf];
     const bool full = k0 + BN <= e1f;
-    __syncthreads();
-#pragma unroll
-    for (int it = 0; it < BN * CPR / NT; ++it) {
-      const int ci = tid + NT * it;
-      const int r = ci / CPR, cc = (ci % CPR) * 8;
-      const int key = k0 + r;
-      u32x4 kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
-      if (key < T) {
-        const long long a = off + (long long)key * D + cc;
-        kv = *reinterpret_cast<const u32x4*>(p.k + a);
-        vv = *reinterpret_cast<const u32x4*>(p.v + a);
-      }
-      *reinterpret_cast<u32x4*>(Ks + Tile<D>::off(r, cc)) = kv;
-      *reinterpret_cast<u32x4*>(Vs + Tile<D>::off(r, cc)) = vv;
-    }
-    __syncthreads();
 
 #pragma unroll
     for (int kb = 0; kb < BN / 32; ++kb) {
       f32x16 s = zero16(), dp = zero16();
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        s = mfma32(lds_row8<D>(Ks, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), qf[kk], s);
-        dp = mfma32(lds_row8<D>(Vs, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), df[kk], dp);
+        s = mfma32(lds_row8<D>(Kt, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), qf[kk], s);
+        dp = mfma32(lds_row8<D>(Vt, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), df[kk], dp);
       }
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        float pv = exp2f(fmaf(s[i], c, -lse2));
+        float pv = fast_exp2(fmaf(s[i], c, -lse2));
         if (!full) {
           const int key = k0 + kb * 32 + acc_row(i, lane);
           pv = key < e1 ? pv : 0.f;
@@ -263,9 +255,12 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p, int n_qtile
       for (int t = 0; t < 2; ++t) {
         const bf16x8 dsb = pack8(dp, t);
 #pragma unroll
-        for (int db = 0; db < DB; ++db) dq[db] = mfma32(lds_tr8<D>(Ks, kb * 32, t, db * 32, lane), dsb, dq[db]);
+        for (int db = 0; db < DB; ++db) dq[db] = mfma32(lds_tr8<D>(Kt, kb * 32, t, db * 32, lane), dsb, dq[db]);
       }
     }
+    wait_vmem();
+    __syncthreads();
+    buf ^= 1;
   }
 
   if (qrow < T) {
@@ -287,8 +282,8 @@ template <int D>
 static hipError_t launch_bwd_d(const BwdParams& p, hipStream_t stream) {
   const long long rows = (long long)p.BH * p.T;
   const long long threads = rows * (D / 8);
-  hipLaunchKernelGGL(bwd_delta_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p.o, p.d_o,
-                     p.delta, rows);
+  hipLaunchKernelGGL(bwd_rowterms_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p.o,
+                     p.d_o, p.lse, p.delta, p.lse2, rows);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int nkt = (p.T + DKV_BN - 1) / DKV_BN;

@@ -33,62 +33,29 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
   return (bid % 8) * (n / 8) + bid / 8;
 }
 
-// Staging of one K/V tile: each thread moves BN*D/(8*NT) 16-byte chunks of K and
-// of V.  Loads go to registers first so that the next tile's global traffic
-// overlaps the current tile's MFMA and softmax work.
+// Staging of one K/V tile straight into LDS.  Key rows past the end of the
+// (virtual) key sequence read the last key instead; the mask hides them.
 template <int D, bool CACHED>
-struct KVStage {
-  static constexpr int NT = 256;
-  static constexpr int CPR = D / 8;
-  static constexpr int PER = FWD_BN * CPR / NT;  // chunks per thread per tensor
-  u32x4 kr[PER], vr[PER];
-
-  __device__ __forceinline__ void load(const FwdParams& p, int bh, long long kvoff, int k0, int tid) {
-    const bool interior = k0 + FWD_BN <= p.Tk;
-#pragma unroll
-    for (int it = 0; it < PER; ++it) {
-      const int ci = tid + NT * it;
-      const int r = ci / CPR, cc = (ci % CPR) * 8;
-      const int key = k0 + r;
-      if (interior || key < p.Tk) {
-        const uint16_t *ksrc, *vsrc;
-        if constexpr (CACHED) {
-          if (key < p.wL) {
-            const int w = key / p.L, off = key - w * p.L;
-            int slot = p.first_slot + w;
-            slot = slot >= p.S ? slot - p.S : slot;
-            const long long base =
-                (long long)slot * p.slot_stride + (long long)bh * p.L * D + (long long)off * D + cc;
-            ksrc = p.k_slots + base;
-            vsrc = p.v_slots + base;
-          } else {
-            const long long base = kvoff + (long long)(key - p.wL) * D + cc;
-            ksrc = p.k + base;
-            vsrc = p.v + base;
-          }
-        } else {
-          const long long base = kvoff + (long long)key * D + cc;
-          ksrc = p.k + base;
-          vsrc = p.v + base;
-        }
-        kr[it] = *reinterpret_cast<const u32x4*>(ksrc);
-        vr[it] = *reinterpret_cast<const u32x4*>(vsrc);
-      } else {
-        kr[it] = u32x4{0, 0, 0, 0};
-        vr[it] = u32x4{0, 0, 0, 0};
+__device__ __forceinline__ void stage_kv(const FwdParams& p, int bh, long long kvoff, int k0, bf16_t* Kt,
+                                         bf16_t* Vt, int tid) {
+  auto src = [&](const uint16_t* win_base, const uint16_t* base, int r) -> const bf16_t* {
+    const int key = min(k0 + r, p.Tk - 1);
+    if constexpr (CACHED) {
+      if (key < p.wL) {
+        const int w = key / p.L, off = key - w * p.L;
+        int slot = p.first_slot + w;
+        slot = slot >= p.S ? slot - p.S : slot;
+        return win_base + (long long)slot * p.slot_stride + (long long)bh * p.L * D + (long long)off * D;
       }
+      return base + kvoff + (long long)(key - p.wL) * D;
+    } else {
+      (void)win_base;
+      return base + kvoff + (long long)key * D;
     }
-  }
-  __device__ __forceinline__ void store(bf16_t* Ks, bf16_t* Vs, int tid) const {
-#pragma unroll
-    for (int it = 0; it < PER; ++it) {
-      const int ci = tid + NT * it;
-      const int r = ci / CPR, cc = (ci % CPR) * 8;
-      *reinterpret_cast<u32x4*>(Ks + Tile<D>::off(r, cc)) = kr[it];
-      *reinterpret_cast<u32x4*>(Vs + Tile<D>::off(r, cc)) = vr[it];
-    }
-  }
-};
+  };
+  stage_rows_direct<D, FWD_BN>(Kt, [&](int r) { return src(p.k_slots, p.k, r); }, tid);
+  stage_rows_direct<D, FWD_BN>(Vt, [&](int r) { return src(p.v_slots, p.v, r); }, tid);
+}
 
 // Rows of the running max only move when a tile raises it by more than this
 // many powers of two; until then probabilities are taken against the stale
@@ -148,18 +115,16 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
 
   const long long kvoff = (long long)bh * (CACHED ? (long long)p.Tq * D : (long long)p.Tk * D);
 
-  KVStage<D, CACHED> stage;
   int k0 = advance(-BN);
   int buf = 0;
-  if (k0 < kend) {
-    stage.load(p, bh, kvoff, k0, tid);
-    stage.store(Ks[0], Vs[0], tid);
-  }
+  if (k0 < kend) stage_kv<D, CACHED>(p, bh, kvoff, k0, Ks[0], Vs[0], tid);
+  wait_vmem();
   __syncthreads();
 
   while (k0 < kend) {
     const int kn = advance(k0);
-    if (kn < kend) stage.load(p, bh, kvoff, kn, tid);  // in flight during this step's math
+    // next tile streams into the other buffer during this step's math
+    if (kn < kend) stage_kv<D, CACHED>(p, bh, kvoff, kn, Ks[buf ^ 1], Vs[buf ^ 1], tid);
     const bf16_t* Kt = Ks[buf];
     const bf16_t* Vt = Vs[buf];
     const bool full = (k0 + BN <= e1f) || (s2l <= k0 && k0 + BN <= e2f);
@@ -234,7 +199,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
       }
     }
 
-    if (kn < kend) stage.store(Ks[buf ^ 1], Vs[buf ^ 1], tid);
+    wait_vmem();
     __syncthreads();
     buf ^= 1;
     k0 = kn;

@@ -97,7 +97,7 @@ size_t mw_block_causal_attn_bwd_workspace_size(int B, int H, int T, int D) {
   (void)D;
   if (B < 1 || H < 1 || T < 1) return 0;
   const size_t bytes = (size_t)B * H * T * sizeof(float);
-  return (bytes + 255) & ~(size_t)255;
+  return 2 * ((bytes + 255) & ~(size_t)255);  // Delta and base-2 LSE, one fp32 per row each
 }
 
 int mw_block_causal_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* d_o,
@@ -121,6 +121,7 @@ int mw_block_causal_attn_bwd(const void* q, const void* k, const void* v, const 
   p.d_o = static_cast<const uint16_t*>(d_o);
   p.lse = lse;
   p.delta = static_cast<float*>(workspace);
+  p.lse2 = reinterpret_cast<float*>(static_cast<char*>(workspace) + need / 2);
   p.dq = static_cast<uint16_t*>(dq);
   p.dk = static_cast<uint16_t*>(dk);
   p.dv = static_cast<uint16_t*>(dv);

@@ -116,6 +116,44 @@ __device__ __forceinline__ bf16x8 lds_tr8(const bf16_t* tile, int rbase, int t, 
   return r;
 }
 
+// ---------------------------------------------------------------------------
+// Direct global -> LDS staging (global_load_lds_dwordx4): each lane's 16 bytes
+// land at wave_base + 16 * lane, so the tile swizzle is applied on the source
+// side: LDS chunk ci (16 bytes, row ci / SLOTS, physical slot ci % SLOTS) is
+// fetched from logical slot (physical ^ swz(row)) of the source row.  No
+// registers are used and nothing has to be written back to LDS; the data is
+// complete once vmcnt reaches zero (wait_vmem() below) and a barrier follows.
+// `row_ptr(r)` returns the global address of tile row r; it must always be a
+// valid address (callers clamp rows past the end of the data).
+// ---------------------------------------------------------------------------
+template <int D, int ROWS, typename RowPtr>
+__device__ __forceinline__ void stage_rows_direct(bf16_t* lds_tile, RowPtr row_ptr, int tid) {
+  constexpr int SLOTS = D / 8;
+  constexpr int ROUNDS = ROWS * SLOTS / 256;
+  static_assert(ROWS * SLOTS % 256 == 0, "tile must be a whole number of 256-chunk rounds");
+#pragma unroll
+  for (int it = 0; it < ROUNDS; ++it) {
+    const int ci = it * 256 + tid;
+    const int row = ci / SLOTS, ps = ci % SLOTS;
+    const int ls = ps ^ Tile<D>::swz(row);
+    const bf16_t* src = row_ptr(row) + ls * 8;
+    bf16_t* dst = lds_tile + (it * 256 + (tid & ~63)) * 8;  // wave-uniform base
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                     (MW_LDS void*)dst, 16, 0, 0);
+  }
+}
+
+// 64 consecutive fp32 values (rows r0..r0+63, clamped to n-1) into LDS by one wave.
+__device__ __forceinline__ void stage_f32x64_direct(float* lds, const float* g, int r0, int n, int lane) {
+  const float* src = g + min(r0 + lane, n - 1);
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src, (MW_LDS void*)lds, 4, 0, 0);
+}
+
+// Wait until this wave's outstanding memory operations (global loads, including
+// direct-to-LDS loads, and LDS accesses) have completed: s_waitcnt with every
+// counter at zero.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0); }
+
 // Row (within a 32-row accumulator block) of accumulator register i in lane l.
 __device__ __forceinline__ int acc_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
 
