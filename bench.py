@@ -220,7 +220,7 @@ def main():
     cached_tflops = F_st / (ph["cached"] * 1e-3) / 1e12
     digest = source_digest(["paper_2608_01127_amd/csrc/attn_fwd.hip", "paper_2608_01127_amd/csrc/mw_device.h"])
     traffic = read_traffic("attn_fwd_cached", digest)
-    roofline = {"kernel": "attn_fwd_kernel<128,true> (cached chunk attention)", "bound": "mfma",
+    roofline = {"kernel": "attn_fwd_kernel<128, true, 8, 64> (cached chunk attention)", "bound": "mfma",
                 "achieved": round(cached_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(cached_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
                 "algorithmic_flops_per_launch": F_st, "avg_launch_ms": round(ph["cached"], 4)}

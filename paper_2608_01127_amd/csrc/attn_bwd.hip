@@ -16,6 +16,8 @@
 // Recomputing S and dP in the dQ kernel costs 1.4x the MFMA work of a fused
 // kernel with atomic dQ updates, but needs no fp32 dQ buffer and gives a
 // deterministic result.
+#include <type_traits>
+
 #include "mw_device.h"
 #include "mw_kernels.h"
 
@@ -98,28 +100,20 @@ __global__ __launch_bounds__(256, D == 64 ? 2 : 1) void bwd_dkdv_kernel(BwdParam
   }
 
   const int klast = min(k0 + BN, T) - 1;
+  const int qvis = (min(mykey, T - 1) / L) * L;  // first query that sees mykey
   const int qstart = ((k0 / L) * L / BM) * BM;  // first query tile with a query of chunk >= chunk(k0)
   const float c = p.scale_log2;
 
   auto stage = [&](int q0, int b) {
-    stage_rows_direct<D, BM>(Qs[b], [&](int r) { return p.q + off + (long long)min(q0 + r, T - 1) * D; }, tid);
-    stage_rows_direct<D, BM>(dOs[b], [&](int r) { return p.d_o + off + (long long)min(q0 + r, T - 1) * D; }, tid);
+    stage_rows_direct<D, BM, 256>(Qs[b], [&](int r) { return p.q + off + (long long)min(q0 + r, T - 1) * D; }, tid);
+    stage_rows_direct<D, BM, 256>(dOs[b], [&](int r) { return p.d_o + off + (long long)min(q0 + r, T - 1) * D; }, tid);
     if (wave == 0) stage_f32x64_direct(lse_s[b], lse2_bh, q0, T, lane);
     if (wave == 1) stage_f32x64_direct(dlt_s[b], dlt_bh, q0, T, lane);
   };
 
-  int buf = 0;
-  if (qstart < T) stage(qstart, 0);
-  wait_vmem();
-  __syncthreads();
-
-  for (int q0 = qstart; q0 < T; q0 += BM) {
-    if (q0 + BM < T) stage(q0 + BM, buf ^ 1);  // next query tile streams in during this one
+  auto step = [&](auto masked, const int q0, const int buf) {
     const bf16_t* Qt = Qs[buf];
     const bf16_t* dOt = dOs[buf];
-    // every (query, key) pair of this step visible and every query row real?
-    const bool full = ((q0 / L) >= (klast / L)) & (q0 + BM <= T);
-
 #pragma unroll
     for (int qb = 0; qb < BM / 32; ++qb) {
       f32x16 s = zero16(), dp = zero16();
@@ -137,9 +131,9 @@ __global__ __launch_bounds__(256, D == 64 ? 2 : 1) void bwd_dkdv_kernel(BwdParam
         for (int j = 0; j < 4; ++j) {
           const int i = 4 * g + j;
           float pv = fast_exp2(fmaf(s[i], c, -l4[j]));
-          if (!full) {
+          if constexpr (decltype(masked)::value) {
             const int q = q0 + rr + j;
-            const bool ok = (q < T) & (mykey < min(T, (q / L + 1) * L));
+            const bool ok = (q < T) & (q >= qvis);  // q in mykey's chunk or a later one
             pv = ok ? pv : 0.f;
           }
           s[i] = pv;
@@ -157,10 +151,29 @@ __global__ __launch_bounds__(256, D == 64 ? 2 : 1) void bwd_dkdv_kernel(BwdParam
         }
       }
     }
-    wait_vmem();
-    __syncthreads();
-    buf ^= 1;
-  }
+  };
+
+  // Query tiles [qfb, qfe) see every key of this workgroup and are whole; the
+  // ones before (same chunk as the keys) and the ragged last tile run masked.
+  const int qfb = max(qstart, ((L * (klast / L) + BM - 1) / BM) * BM);
+  const int qfe = max(qfb, (T / BM) * BM);
+  int buf = 0;
+  int q0 = qstart;
+  if (q0 < T) stage(q0, 0);
+  wait_vmem();
+  __syncthreads();
+  auto run = [&](auto masked, const int qstop) {
+    for (; q0 < qstop; q0 += BM) {
+      if (q0 + BM < T) stage(q0 + BM, buf ^ 1);  // next query tile streams in during this one
+      step(masked, q0, buf);
+      wait_vmem();
+      __syncthreads();
+      buf ^= 1;
+    }
+  };
+  run(std::true_type{}, min(qfb, T));
+  run(std::false_type{}, min(qfe, T));
+  run(std::true_type{}, T);
 
   if (mykey < T) {
     bf16_t* dkrow = p.dk + off + (long long)mykey * D;
@@ -220,20 +233,12 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p, int n_qtile
   for (int db = 0; db < DB; ++db) dq[db] = zero16();
 
   auto stage = [&](int k0, int b) {
-    stage_rows_direct<D, BN>(Ks[b], [&](int r) { return p.k + off + (long long)min(k0 + r, T - 1) * D; }, tid);
-    stage_rows_direct<D, BN>(Vs[b], [&](int r) { return p.v + off + (long long)min(k0 + r, T - 1) * D; }, tid);
+    stage_rows_direct<D, BN, 256>(Ks[b], [&](int r) { return p.k + off + (long long)min(k0 + r, T - 1) * D; }, tid);
+    stage_rows_direct<D, BN, 256>(Vs[b], [&](int r) { return p.v + off + (long long)min(k0 + r, T - 1) * D; }, tid);
   };
-  int buf = 0;
-  stage(0, 0);
-  wait_vmem();
-  __syncthreads();
-
-  for (int k0 = 0; k0 < kend; k0 += BN) {
-    if (k0 + BN < kend) stage(k0 + BN, buf ^ 1);
+  auto step = [&](auto masked, const int k0, const int buf) {
     const bf16_t* Kt = Ks[buf];
     const bf16_t* Vt = Vs[buf];
-    const bool full = k0 + BN <= e1f;
-
 #pragma unroll
     for (int kb = 0; kb < BN / 32; ++kb) {
       f32x16 s = zero16(), dp = zero16();
@@ -245,7 +250,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p, int n_qtile
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         float pv = fast_exp2(fmaf(s[i], c, -lse2));
-        if (!full) {
+        if constexpr (decltype(masked)::value) {
           const int key = k0 + kb * 32 + acc_row(i, lane);
           pv = key < e1 ? pv : 0.f;
         }
@@ -258,10 +263,26 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p, int n_qtile
         for (int db = 0; db < DB; ++db) dq[db] = mfma32(lds_tr8<D>(Kt, kb * 32, t, db * 32, lane), dsb, dq[db]);
       }
     }
-    wait_vmem();
-    __syncthreads();
-    buf ^= 1;
-  }
+  };
+
+  // key tiles [0, kfull) are visible to every query of the workgroup
+  const int kfull = (e1f / BN) * BN;
+  int buf = 0;
+  int k0 = 0;
+  stage(0, 0);
+  wait_vmem();
+  __syncthreads();
+  auto run = [&](auto masked, const int kstop) {
+    for (; k0 < kstop; k0 += BN) {
+      if (k0 + BN < kend) stage(k0 + BN, buf ^ 1);
+      step(masked, k0, buf);
+      wait_vmem();
+      __syncthreads();
+      buf ^= 1;
+    }
+  };
+  run(std::false_type{}, min(kfull, kend));
+  run(std::true_type{}, kend);
 
   if (qrow < T) {
     bf16_t* row = p.dq + off + (long long)qrow * D;

@@ -19,6 +19,8 @@
 // Visibility rule: paper Sec. 3.2 (block-causal chunks) for training and
 // Sec. 3.5 (queued in-flight chunks over committed history) for the cached
 // variant; see Vis in mw_device.h.
+#include <type_traits>
+
 #include "mw_device.h"
 #include "mw_kernels.h"
 
@@ -35,7 +37,7 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
 
 // Staging of one K/V tile straight into LDS.  Key rows past the end of the
 // (virtual) key sequence read the last key instead; the mask hides them.
-template <int D, bool CACHED>
+template <int D, bool CACHED, int BN, int NT>
 __device__ __forceinline__ void stage_kv(const FwdParams& p, int bh, long long kvoff, int k0, bf16_t* Kt,
                                          bf16_t* Vt, int tid) {
   auto src = [&](const uint16_t* win_base, const uint16_t* base, int r) -> const bf16_t* {
@@ -53,8 +55,8 @@ __device__ __forceinline__ void stage_kv(const FwdParams& p, int bh, long long k
       return base + kvoff + (long long)key * D;
     }
   };
-  stage_rows_direct<D, FWD_BN>(Kt, [&](int r) { return src(p.k_slots, p.k, r); }, tid);
-  stage_rows_direct<D, FWD_BN>(Vt, [&](int r) { return src(p.v_slots, p.v, r); }, tid);
+  stage_rows_direct<D, BN, NT>(Kt, [&](int r) { return src(p.k_slots, p.k, r); }, tid);
+  stage_rows_direct<D, BN, NT>(Vt, [&](int r) { return src(p.v_slots, p.v, r); }, tid);
 }
 
 // Rows of the running max only move when a tile raises it by more than this
@@ -64,9 +66,10 @@ __device__ __forceinline__ void stage_kv(const FwdParams& p, int bh, long long k
 // O rescale is skipped on almost every step.
 constexpr float kRescaleThreshold = 8.f;
 
-template <int D, bool CACHED>
-__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
-  constexpr int BM = FWD_BM, BN = FWD_BN;
+// NW waves per workgroup, each owning 32 query rows; BN keys per main-loop step.
+template <int D, bool CACHED, int NW, int BN>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) {
+  constexpr int BM = 32 * NW, NT = 64 * NW, KB = BN / 32;
   constexpr int KK = D / 16;  // contraction steps over D
   constexpr int DB = D / 32;  // 32-wide column blocks of D
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BN * D];
@@ -115,34 +118,27 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
 
   const long long kvoff = (long long)bh * (CACHED ? (long long)p.Tq * D : (long long)p.Tk * D);
 
-  int k0 = advance(-BN);
-  int buf = 0;
-  if (k0 < kend) stage_kv<D, CACHED>(p, bh, kvoff, k0, Ks[0], Vs[0], tid);
-  wait_vmem();
-  __syncthreads();
+  // Tiles [0, kfull) are visible to every row of the workgroup and run without
+  // any mask code; the remaining tiles (chunk edges, the ragged end, the gap of
+  // the isolated rule) run the masked instantiation.  Separate loops keep the
+  // fast loop free of the mask and of register copies between the two bodies.
+  const int kfull = max(0, (e1f / BN) * BN);
 
-  while (k0 < kend) {
-    const int kn = advance(k0);
-    // next tile streams into the other buffer during this step's math
-    if (kn < kend) stage_kv<D, CACHED>(p, bh, kvoff, kn, Ks[buf ^ 1], Vs[buf ^ 1], tid);
-    const bf16_t* Kt = Ks[buf];
-    const bf16_t* Vt = Vs[buf];
-    const bool full = (k0 + BN <= e1f) || (s2l <= k0 && k0 + BN <= e2f);
-
-    // S^T for two 32-key blocks (independent accumulation chains interleaved)
-    f32x16 s[2];
-    s[0] = zero16();
-    s[1] = zero16();
+  auto step = [&](auto masked, const int k0, const bf16_t* Kt, const bf16_t* Vt) {
+    // S^T for KB 32-key blocks (independent accumulation chains interleaved)
+    f32x16 s[KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) s[kb] = zero16();
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < KB; ++kb)
         s[kb] = mfma32(lds_row8<D>(Kt, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), qf[kk], s[kb]);
     }
 
-    if (!full) {
+    if constexpr (decltype(masked)::value) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < KB; ++kb) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int key = k0 + kb * 32 + acc_row(i, lane);
@@ -156,7 +152,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     }
     float mx = -INFINITY;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < KB; ++kb) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
     }
@@ -178,7 +174,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     const float nm = (m == -INFINITY) ? 0.f : -m;
     float ls = 0.f;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < KB; ++kb) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const float pv = fast_exp2(fmaf(s[kb][i], c, nm));
@@ -189,7 +185,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     lsum += ls;
 
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < KB; ++kb) {
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         const bf16x8 pb = pack8(s[kb], t);
@@ -198,12 +194,28 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
           o[db] = mfma32(lds_tr8<D>(Vt, kb * 32, t, db * 32, lane), pb, o[db]);
       }
     }
+  };
 
-    wait_vmem();
-    __syncthreads();
-    buf ^= 1;
-    k0 = kn;
-  }
+  int k0 = advance(-BN);
+  int buf = 0;
+  if (k0 < kend) stage_kv<D, CACHED, BN, NT>(p, bh, kvoff, k0, Ks[0], Vs[0], tid);
+  wait_vmem();
+  __syncthreads();
+
+  auto run = [&](auto masked, const int kstop) {
+    while (k0 < kstop) {
+      const int kn = advance(k0);
+      // next tile streams into the other buffer during this step's math
+      if (kn < kend) stage_kv<D, CACHED, BN, NT>(p, bh, kvoff, kn, Ks[buf ^ 1], Vs[buf ^ 1], tid);
+      step(masked, k0, Ks[buf], Vs[buf]);
+      wait_vmem();
+      __syncthreads();
+      buf ^= 1;
+      k0 = kn;
+    }
+  };
+  run(std::false_type{}, min(kfull, kend));
+  run(std::true_type{}, kend);
 
   lsum += __shfl_xor(lsum, 32);
   if (qrow < p.Tq) {
@@ -225,16 +237,27 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   }
 }
 
-hipError_t launch_fwd(const FwdParams& p, int D, bool cached, hipStream_t stream) {
-  const dim3 grid(p.n_qtiles * p.BH), block(256);
-  if (D == 64) {
-    if (cached) hipLaunchKernelGGL((attn_fwd_kernel<64, true>), grid, block, 0, stream, p);
-    else hipLaunchKernelGGL((attn_fwd_kernel<64, false>), grid, block, 0, stream, p);
-  } else {
-    if (cached) hipLaunchKernelGGL((attn_fwd_kernel<128, true>), grid, block, 0, stream, p);
-    else hipLaunchKernelGGL((attn_fwd_kernel<128, false>), grid, block, 0, stream, p);
-  }
+// Tile configuration per head dimension: waves per workgroup (32 query rows
+// each) and keys per step.  With D = 128 a workgroup of 8 waves shares each
+// staged K/V tile among 256 queries, halving L2 -> LDS traffic per MFMA; with
+// D = 64 four waves and a third workgroup per CU measured faster.
+template <int D>
+struct FwdCfg {
+  static constexpr int NW = D == 64 ? 4 : 8;
+  static constexpr int BN = 64;
+};
+
+template <int D, bool CACHED>
+static hipError_t launch_fwd_cfg(FwdParams p, hipStream_t stream) {
+  constexpr int NW = FwdCfg<D>::NW, BN = FwdCfg<D>::BN;
+  p.n_qtiles = (p.Tq + 32 * NW - 1) / (32 * NW);
+  hipLaunchKernelGGL((attn_fwd_kernel<D, CACHED, NW, BN>), dim3(p.n_qtiles * p.BH), dim3(64 * NW), 0, stream, p);
   return hipGetLastError();
+}
+
+hipError_t launch_fwd(const FwdParams& p, int D, bool cached, hipStream_t stream) {
+  if (D == 64) return cached ? launch_fwd_cfg<64, true>(p, stream) : launch_fwd_cfg<64, false>(p, stream);
+  return cached ? launch_fwd_cfg<128, true>(p, stream) : launch_fwd_cfg<128, false>(p, stream);
 }
 
 }  // namespace mw

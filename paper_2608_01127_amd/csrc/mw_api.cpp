@@ -82,7 +82,6 @@ int mw_block_causal_attn_fwd(const void* q, const void* k, const void* v, void* 
   p.lse = lse;
   p.BH = B * H;
   p.Tq = T;
-  p.n_qtiles = (T + mw::FWD_BM - 1) / mw::FWD_BM;
   p.vis_mode = 0;
   p.L = chunk_len > T ? T : chunk_len;
   p.Tk = T;
@@ -232,7 +231,6 @@ int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new, in
   p.lse = lse;
   p.BH = c->B * c->H;
   p.Tq = (int)nq_tok;
-  p.n_qtiles = (p.Tq + mw::FWD_BM - 1) / mw::FWD_BM;
   p.vis_mode = flags == MW_QUEUED_CAUSAL ? 1 : 2;
   p.L = c->L;
   p.wL = (int)(w * c->L);

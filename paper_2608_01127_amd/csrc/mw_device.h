@@ -126,18 +126,18 @@ __device__ __forceinline__ bf16x8 lds_tr8(const bf16_t* tile, int rbase, int t, 
 // `row_ptr(r)` returns the global address of tile row r; it must always be a
 // valid address (callers clamp rows past the end of the data).
 // ---------------------------------------------------------------------------
-template <int D, int ROWS, typename RowPtr>
+template <int D, int ROWS, int NT, typename RowPtr>
 __device__ __forceinline__ void stage_rows_direct(bf16_t* lds_tile, RowPtr row_ptr, int tid) {
   constexpr int SLOTS = D / 8;
-  constexpr int ROUNDS = ROWS * SLOTS / 256;
-  static_assert(ROWS * SLOTS % 256 == 0, "tile must be a whole number of 256-chunk rounds");
+  constexpr int ROUNDS = ROWS * SLOTS / NT;
+  static_assert(ROWS * SLOTS % NT == 0, "tile must be a whole number of NT-chunk rounds");
 #pragma unroll
   for (int it = 0; it < ROUNDS; ++it) {
-    const int ci = it * 256 + tid;
+    const int ci = it * NT + tid;
     const int row = ci / SLOTS, ps = ci % SLOTS;
     const int ls = ps ^ Tile<D>::swz(row);
     const bf16_t* src = row_ptr(row) + ls * 8;
-    bf16_t* dst = lds_tile + (it * 256 + (tid & ~63)) * 8;  // wave-uniform base
+    bf16_t* dst = lds_tile + (it * NT + (tid & ~63)) * 8;  // wave-uniform base
     __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
                                      (MW_LDS void*)dst, 16, 0, 0);
   }

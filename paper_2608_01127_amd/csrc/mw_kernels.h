@@ -16,7 +16,7 @@ struct FwdParams {
   float* lse;  // may be null (cached attention)
   int BH;
   int Tq;
-  int n_qtiles;
+  int n_qtiles;   // set by the launcher from its tile configuration
   int vis_mode;  // VisMode
   int L;         // chunk length (training) / committed chunk length (cached)
   int Tk;        // keys in the (virtual) sequence
@@ -52,8 +52,6 @@ struct BwdParams {
 };
 
 // Tile sizes (shared with the host for grid computation).
-constexpr int FWD_BM = 128;   // queries per workgroup (4 waves x 32)
-constexpr int FWD_BN = 64;    // keys per main-loop step
 constexpr int DKV_BN = 128;   // keys per workgroup in the dK/dV kernel
 constexpr int DKV_BM = 64;    // queries per step in the dK/dV kernel
 constexpr int DQ_BM = 128;    // queries per workgroup in the dQ kernel
