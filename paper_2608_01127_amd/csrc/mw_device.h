@@ -118,14 +118,32 @@ __device__ __forceinline__ bf16x8 lds_tr8(const bf16_t* tile, int rbase, int t, 
 
 // ---------------------------------------------------------------------------
 // Direct global -> LDS staging (global_load_lds_dwordx4): each lane's 16 bytes
-// land at wave_base + 16 * lane, so the tile swizzle is applied on the source
-// side: LDS chunk ci (16 bytes, row ci / SLOTS, physical slot ci % SLOTS) is
-// fetched from logical slot (physical ^ swz(row)) of the source row.  No
-// registers are used and nothing has to be written back to LDS; the data is
-// complete once vmcnt reaches zero (wait_vmem() below) and a barrier follows.
+// land at wave_base + 16 * lane (wave_base in M0), so the tile swizzle is
+// applied on the source side: LDS chunk ci (16 bytes, row ci / SLOTS, physical
+// slot ci % SLOTS) is fetched from logical slot (physical ^ swz(row)) of the
+// source row.  No registers are used and nothing is written back to LDS.
+//
+// The instruction is issued through inline assembly on purpose: the compiler
+// treats the builtin form as an LDS write that may alias every later LDS read,
+// and so inserted a full vmcnt(0) wait before the current tile's reads, which
+// serialised the next tile's load latency with this tile's math.  Here the
+// kernels synchronise explicitly instead: wait_vmem() (all counters zero)
+// followed by a workgroup barrier before any wave reads a staged buffer, and
+// no wave issues a load into a buffer before the barrier that ends the reads
+// of that buffer.  Compiler-inserted vmcnt waits stay correct: loads it does
+// not know of can only make such waits longer.
 // `row_ptr(r)` returns the global address of tile row r; it must always be a
 // valid address (callers clamp rows past the end of the data).
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ void dma_lds_16(const void* src, MW_LDS void* wave_dst) {
+  const unsigned base = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)wave_dst);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(base) : "m0", "memory");
+}
+__device__ __forceinline__ void dma_lds_4(const void* src, MW_LDS void* wave_dst) {
+  const unsigned base = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)wave_dst);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(base) : "m0", "memory");
+}
+
 template <int D, int ROWS, int NT, typename RowPtr>
 __device__ __forceinline__ void stage_rows_direct(bf16_t* lds_tile, RowPtr row_ptr, int tid) {
   constexpr int SLOTS = D / 8;
@@ -138,15 +156,14 @@ __device__ __forceinline__ void stage_rows_direct(bf16_t* lds_tile, RowPtr row_p
     const int ls = ps ^ Tile<D>::swz(row);
     const bf16_t* src = row_ptr(row) + ls * 8;
     bf16_t* dst = lds_tile + (it * NT + (tid & ~63)) * 8;  // wave-uniform base
-    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                     (MW_LDS void*)dst, 16, 0, 0);
+    dma_lds_16(src, (MW_LDS void*)dst);
   }
 }
 
 // 64 consecutive fp32 values (rows r0..r0+63, clamped to n-1) into LDS by one wave.
 __device__ __forceinline__ void stage_f32x64_direct(float* lds, const float* g, int r0, int n, int lane) {
   const float* src = g + min(r0 + lane, n - 1);
-  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src, (MW_LDS void*)lds, 4, 0, 0);
+  dma_lds_4(src, (MW_LDS void*)lds);
 }
 
 // Wait until this wave's outstanding memory operations (global loads, including
