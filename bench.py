@@ -119,6 +119,40 @@ def cpu_baseline(target_s: float):
                       f"({dt:.1f} s), useful-FLOP count as the GPU"}
 
 
+def decode_shapes(mw, torch, cache, st, dev, reps=20):
+    """Cache-bound shapes: one queued chunk of q_len tokens over the full window
+    (6 committed chunks of 2640 tokens, B1 H16 D128).  Each timed call is
+    preceded by a 512 MB write that evicts the 256 MB Infinity Cache, so the
+    window's K/V come from HBM.  Algorithmic bytes = window K and V + Q, K_new,
+    V_new and O of the queued chunk."""
+    out = []
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    g = torch.Generator(device=dev).manual_seed(1234)
+    for ql in (64, 128, 256):
+        q, kn, vn = (torch.randn(st.B, st.H, ql, st.D, device=dev, generator=g).to(torch.bfloat16) for _ in range(3))
+        o = torch.empty_like(q)
+        ws = torch.empty(max(16, mw.mw_chunk_attn_cached_workspace_size(cache, 1, ql, st.window)), dtype=torch.uint8,
+                         device=dev)
+        run = lambda: mw.mw_chunk_attn_cached(q, kn, vn, 1, ql, cache, window=st.window, out=o, workspace=ws)
+        for _ in range(3):
+            run()
+        tot = 0.0
+        for _ in range(reps):
+            flush.fill_(1)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            run()
+            e1.record()
+            torch.cuda.synchronize()
+            tot += e0.elapsed_time(e1)
+        ms = tot / reps
+        nbytes = 2 * st.window * st.B * st.H * st.chunk_len * st.D * 2 + 4 * st.B * st.H * ql * st.D * 2
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        out.append({"q_len": ql, "us": round(ms * 1e3, 2), "gbs": round(gbs, 1),
+                    "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4), "bytes": nbytes})
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -159,6 +193,8 @@ def main():
     sb = synth.stream_step_inputs(st, 0, which=("q", "k_new", "v_new"))
     sq, skn, svn = (up(sb[n]) for n in ("q", "k_new", "v_new"))
     so = torch.empty_like(sq)
+    ws_c = torch.empty(max(16, mw.mw_chunk_attn_cached_workspace_size(cache, st.n_queued, st.q_len, st.window)),
+                       dtype=torch.uint8, device=dev)
     for i in range(st.window):
         mw.mw_kvcache_append(cache, *commits[i % n_src])
     torch.cuda.synchronize()
@@ -187,7 +223,7 @@ def main():
         if e: e[3].record()
         mw.mw_kvcache_evict(cache, cache.live - st.window)
         mw.mw_chunk_attn_cached(sq, skn, svn, st.n_queued, st.q_len, cache, window=st.window,
-                                flags=mw.MW_QUEUED_CAUSAL, out=so)
+                                flags=mw.MW_QUEUED_CAUSAL, out=so, workspace=ws_c)
         if e: e[4].record()
         if rec is not None:
             rec.append(e)
@@ -253,6 +289,7 @@ def main():
                    "frac_hbm_peak": round(bytes_append / (ph["append"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
         "roofline": roofline,
     }
+    res["decode"] = decode_shapes(mw, torch, cache, st, dev)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     else:

@@ -159,6 +159,15 @@ int mw_kvcache_slot_of(const mw_kvcache* c, int64_t chunk);
  *
  * q, k_new, v_new, o : bf16 [B, H, n_queued*q_len, D] with B, H, D those of the cache
  * lse                : fp32 [B, H, n_queued*q_len] or NULL
+ * workspace          : optional device buffer.  With at least
+ *                      mw_chunk_attn_cached_workspace_size(...) bytes the key
+ *                      range of each query tile is split over several
+ *                      workgroups (fp32 partial results in the workspace, then a
+ *                      merge), which keeps the GPU busy when there are few query
+ *                      tiles (few or short queued chunks).  NULL or a smaller
+ *                      buffer: as many splits as fit (possibly none).  The
+ *                      result does not depend on the split count beyond fp32
+ *                      rounding.
  * Keys are visited in logical order whatever the ring offset, so the result
  * for a given window content does not depend on where the ring wrapped.
  * Errors: MW_EINVAL (null pointers, n_queued/q_len < 1, window > live,
@@ -167,9 +176,14 @@ int mw_kvcache_slot_of(const mw_kvcache* c, int64_t chunk);
  * ---------------------------------------------------------------------- */
 enum { MW_QUEUED_CAUSAL = 0, MW_QUEUED_ISOLATED = 1 };
 
+/* Workspace bytes that let mw_chunk_attn_cached use its preferred split count
+ * for this shape (0 when it would not split).  Negative window: all live. */
+size_t mw_chunk_attn_cached_workspace_size(const mw_kvcache* c, int n_queued, int q_len, int window);
+
 int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new,
                          int n_queued, int q_len, const mw_kvcache* c, int window, int flags,
-                         void* o, float* lse, float scale, mw_stream_t stream);
+                         void* o, float* lse, float scale, void* workspace, size_t workspace_bytes,
+                         mw_stream_t stream);
 
 #ifdef __cplusplus
 }

@@ -56,7 +56,8 @@ SIGNATURES = {
     "mw_kvcache_evict": ([_cache_p, _i], _i),
     "mw_kvcache_live": ([_cache_p], _i),
     "mw_kvcache_slot_of": ([_cache_p, ctypes.c_int64], _i),
-    "mw_chunk_attn_cached": ([_vp, _vp, _vp, _i, _i, _cache_p, _i, _i, _vp, _vp, _f, _vp], _i),
+    "mw_chunk_attn_cached_workspace_size": ([_cache_p, _i, _i, _i], _sz),
+    "mw_chunk_attn_cached": ([_vp, _vp, _vp, _i, _i, _cache_p, _i, _i, _vp, _vp, _f, _vp, _sz, _vp], _i),
 }
 
 _lib = None
@@ -237,9 +238,19 @@ def mw_kvcache_slot_of(cache: KVCache, chunk: int) -> int:
     return cache.slot_of(chunk)
 
 
+def mw_chunk_attn_cached_workspace_size(cache: KVCache, n_queued: int, q_len: int, window: int = -1) -> int:
+    return int(load().mw_chunk_attn_cached_workspace_size(ctypes.byref(cache.desc), int(n_queued), int(q_len),
+                                                          int(window)))
+
+
 def mw_chunk_attn_cached(q, k_new, v_new, n_queued: int, q_len: int, cache: KVCache, window: int = -1,
-                         flags: int = MW_QUEUED_CAUSAL, scale=None, out=None, lse=None, want_lse: bool = False):
-    """Cached chunk attention of n_queued in-flight chunks.  Returns (o, lse or None)."""
+                         flags: int = MW_QUEUED_CAUSAL, scale=None, out=None, lse=None, want_lse: bool = False,
+                         workspace=None, split: bool = True):
+    """Cached chunk attention of n_queued in-flight chunks.  Returns (o, lse or None).
+
+    With split=True and no workspace given, a workspace of the size the library
+    asks for is allocated here (torch); split=False runs the single-pass kernel.
+    """
     torch = _torch()
     d = cache.desc
     for n, t in (("q", q), ("k_new", k_new), ("v_new", v_new)):
@@ -252,7 +263,13 @@ def mw_chunk_attn_cached(q, k_new, v_new, n_queued: int, q_len: int, cache: KVCa
     _bf16_4d("out", o)
     if want_lse and lse is None:
         lse = torch.empty((d.B, d.H, n_queued * q_len), dtype=torch.float32, device=dev)
+    if split and workspace is None:
+        need = mw_chunk_attn_cached_workspace_size(cache, n_queued, q_len, window)
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev) if need > 0 else None
+    if not split:
+        workspace = None
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(load().mw_chunk_attn_cached(_ptr(q), _ptr(k_new), _ptr(v_new), int(n_queued), int(q_len),
                                        ctypes.byref(d), int(window), int(flags), _ptr(o), _ptr(lse), scale,
-                                       _stream_handle(dev)))
+                                       _ptr(workspace), nbytes, _stream_handle(dev)))
     return o, lse

@@ -61,9 +61,9 @@ __global__ __launch_bounds__(256) void bwd_rowterms_kernel(const uint16_t* __res
 // D = 128 keeps 192 registers of per-wave state (K and V fragments, dK and dV
 // accumulators) and runs one wave per SIMD with the full register file; D = 64
 // fits two waves per SIMD.
-template <int D>
-__global__ __launch_bounds__(256, D == 64 ? 2 : 1) void bwd_dkdv_kernel(BwdParams p, int n_ktiles) {
-  constexpr int BN = DKV_BN, BM = DKV_BM;
+template <int D, int NW>
+__global__ __launch_bounds__(64 * NW, (D == 64 ? 8 : 4) / NW) void bwd_dkdv_kernel(BwdParams p, int n_ktiles) {
+  constexpr int BN = 32 * NW, BM = DKV_BM, NT = 64 * NW;
   constexpr int KK = D / 16, DB = D / 32;
   __shared__ __attribute__((aligned(16))) bf16_t Qs[2][BM * D];
   __shared__ __attribute__((aligned(16))) bf16_t dOs[2][BM * D];
@@ -105,8 +105,8 @@ __global__ __launch_bounds__(256, D == 64 ? 2 : 1) void bwd_dkdv_kernel(BwdParam
   const float c = p.scale_log2;
 
   auto stage = [&](int q0, int b) {
-    stage_rows_direct<D, BM, 256>(Qs[b], [&](int r) { return p.q + off + (long long)min(q0 + r, T - 1) * D; }, tid);
-    stage_rows_direct<D, BM, 256>(dOs[b], [&](int r) { return p.d_o + off + (long long)min(q0 + r, T - 1) * D; }, tid);
+    stage_rows_direct<D, BM, NT>(Qs[b], [&](int r) { return p.q + off + (long long)min(q0 + r, T - 1) * D; }, tid);
+    stage_rows_direct<D, BM, NT>(dOs[b], [&](int r) { return p.d_o + off + (long long)min(q0 + r, T - 1) * D; }, tid);
     if (wave == 0) stage_f32x64_direct(lse_s[b], lse2_bh, q0, T, lane);
     if (wave == 1) stage_f32x64_direct(dlt_s[b], dlt_bh, q0, T, lane);
   };
@@ -196,9 +196,9 @@ __global__ __launch_bounds__(256, D == 64 ? 2 : 1) void bwd_dkdv_kernel(BwdParam
   }
 }
 
-template <int D>
-__global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p, int n_qtiles) {
-  constexpr int BM = DQ_BM, BN = DQ_BN;
+template <int D, int NW>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, int n_qtiles) {
+  constexpr int BM = 32 * NW, BN = DQ_BN, NT = 64 * NW;
   constexpr int KK = D / 16, DB = D / 32;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BN * D];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[2][BN * D];
@@ -233,8 +233,8 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p, int n_qtile
   for (int db = 0; db < DB; ++db) dq[db] = zero16();
 
   auto stage = [&](int k0, int b) {
-    stage_rows_direct<D, BN, 256>(Ks[b], [&](int r) { return p.k + off + (long long)min(k0 + r, T - 1) * D; }, tid);
-    stage_rows_direct<D, BN, 256>(Vs[b], [&](int r) { return p.v + off + (long long)min(k0 + r, T - 1) * D; }, tid);
+    stage_rows_direct<D, BN, NT>(Ks[b], [&](int r) { return p.k + off + (long long)min(k0 + r, T - 1) * D; }, tid);
+    stage_rows_direct<D, BN, NT>(Vs[b], [&](int r) { return p.v + off + (long long)min(k0 + r, T - 1) * D; }, tid);
   };
   auto step = [&](auto masked, const int k0, const int buf) {
     const bf16_t* Kt = Ks[buf];
@@ -299,25 +299,41 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams p, int n_qtile
   }
 }
 
+// Waves per workgroup of the dK/dV kernel (32 keys each) and of the dQ kernel
+// (32 queries each).
+template <int D>
+struct BwdCfg {
+  static constexpr int NW_DKV = 4;
+  static constexpr int NW_DQ = 4;
+};
+
 template <int D>
 static hipError_t launch_bwd_d(const BwdParams& p, hipStream_t stream) {
+  constexpr int NK = BwdCfg<D>::NW_DKV, NQ = BwdCfg<D>::NW_DQ;
   const long long rows = (long long)p.BH * p.T;
   const long long threads = rows * (D / 8);
   hipLaunchKernelGGL(bwd_rowterms_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p.o,
                      p.d_o, p.lse, p.delta, p.lse2, rows);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int nkt = (p.T + DKV_BN - 1) / DKV_BN;
-  hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(nkt * p.BH), dim3(256), 0, stream, p, nkt);
+  const int nkt = (p.T + 32 * NK - 1) / (32 * NK);
+  hipLaunchKernelGGL((bwd_dkdv_kernel<D, NK>), dim3(nkt * p.BH), dim3(64 * NK), 0, stream, p, nkt);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int nqt = (p.T + DQ_BM - 1) / DQ_BM;
-  hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(nqt * p.BH), dim3(256), 0, stream, p, nqt);
+  const int nqt = (p.T + 32 * NQ - 1) / (32 * NQ);
+  hipLaunchKernelGGL((bwd_dq_kernel<D, NQ>), dim3(nqt * p.BH), dim3(64 * NQ), 0, stream, p, nqt);
   return hipGetLastError();
 }
 
-hipError_t launch_bwd(const BwdParams& p, int D, hipStream_t stream) {
-  return D == 64 ? launch_bwd_d<64>(p, stream) : launch_bwd_d<128>(p, stream);
-}
+// This file is compiled once per head dimension (MW_BWD_HEAD_DIM = 64 or 128):
+// the two instantiations get different instruction-scheduling options in the
+// build (each measured the faster one for its size).
+#if MW_BWD_HEAD_DIM == 64
+hipError_t launch_bwd_64(const BwdParams& p, hipStream_t stream) { return launch_bwd_d<64>(p, stream); }
+#elif MW_BWD_HEAD_DIM == 128
+hipError_t launch_bwd_128(const BwdParams& p, hipStream_t stream) { return launch_bwd_d<128>(p, stream); }
+#else
+#error "compile with -DMW_BWD_HEAD_DIM=64 or -DMW_BWD_HEAD_DIM=128"
+#endif
 
 }  // namespace mw

@@ -19,6 +19,8 @@
 // Visibility rule: paper Sec. 3.2 (block-causal chunks) for training and
 // Sec. 3.5 (queued in-flight chunks over committed history) for the cached
 // variant; see Vis in mw_device.h.
+#include <algorithm>
+#include <cmath>
 #include <type_traits>
 
 #include "mw_device.h"
@@ -76,8 +78,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
   __shared__ __attribute__((aligned(16))) bf16_t Vs[2][BN * D];
 
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
-  const int bh = logical / p.n_qtiles;
-  const int qt = p.n_qtiles - 1 - logical % p.n_qtiles;  // heaviest (last) query tile first
+  const int NS = p.n_splits;
+  const int split = logical % NS;
+  const int bh = (logical / NS) / p.n_qtiles;
+  const int qt = p.n_qtiles - 1 - (logical / NS) % p.n_qtiles;  // heaviest (last) query tile first
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q0 = qt * BM;
   const int qrow = q0 + wave * 32 + (lane & 31);
@@ -102,7 +106,11 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
   int e1f, s2f, e2f, e1l, s2l, e2l;
   vis.range(q0, e1f, s2f, e2f);
   vis.range(min(q0 + BM, p.Tq) - 1, e1l, s2l, e2l);
-  const int kend = max(e1l, e2l);
+  const int kend_all = max(e1l, e2l);
+  // this workgroup's share of the key tiles [0, kend_all): split `split` of NS
+  const int ntiles = (kend_all + BN - 1) / BN;
+  const int kbeg = (int)((long long)ntiles * split / NS) * BN;
+  const int kend = min(kend_all, (int)((long long)ntiles * (split + 1) / NS) * BN);
   // next visited key tile after k: tiles no row of this workgroup can see are skipped
   auto advance = [&](int k) {
     int n = k + BN;
@@ -196,7 +204,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
     }
   };
 
-  int k0 = advance(-BN);
+  int k0 = advance(kbeg - BN);
   int buf = 0;
   if (k0 < kend) stage_kv<D, CACHED, BN, NT>(p, bh, kvoff, k0, Ks[0], Vs[0], tid);
   wait_vmem();
@@ -216,6 +224,33 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
   };
   run(std::false_type{}, min(kfull, kend));
   run(std::true_type{}, kend);
+
+  if (NS > 1) {
+    // partial result of this key range: unnormalised O, the reference max m
+    // (log2 units, possibly stale by up to the rescale threshold) and the sum
+    // l of 2^(s - m); rows past Tq are not written
+    lsum += __shfl_xor(lsum, 32);
+    if (qrow < p.Tq) {
+      const long long row = ((long long)split * p.BH + bh) * p.Tq + qrow;
+      float* po = p.part + row * D;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          f32x4 w;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) w[j] = o[db][4 * g + j];
+          *reinterpret_cast<f32x4*>(po + db * 32 + 8 * g + 4 * (lane >> 5)) = w;
+        }
+      }
+      if (lane < 32) {
+        float* ml = p.part + (long long)NS * p.BH * p.Tq * D + 2 * row;
+        ml[0] = m;
+        ml[1] = lsum;
+      }
+    }
+    return;
+  }
 
   lsum += __shfl_xor(lsum, 32);
   if (qrow < p.Tq) {
@@ -237,6 +272,39 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
   }
 }
 
+// Merge of the per-split partials: with M = max_s m_s and w_s = 2^(m_s - M),
+//   O = sum_s w_s O_s / sum_s w_s l_s,   LSE = (M + log2 sum_s w_s l_s) ln 2.
+// One thread per 4 output columns of a row.
+template <int D>
+__global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part, uint16_t* __restrict__ o,
+                                                           float* __restrict__ lse, int NS, long long rows) {
+  constexpr int TPR = D / 4;  // threads per row
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long row = gid / TPR;
+  if (row >= rows) return;
+  const int c = (int)(gid % TPR) * 4;
+  const float* ml = part + (long long)NS * rows * D;
+  float M = -INFINITY;
+  for (int s = 0; s < NS; ++s) M = fmaxf(M, ml[2 * ((long long)s * rows + row)]);
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float L = 0.f;
+  for (int s = 0; s < NS; ++s) {
+    const long long r = (long long)s * rows + row;
+    const float ms = ml[2 * r], ls = ml[2 * r + 1];
+    const float w = (ms == -INFINITY) ? 0.f : fast_exp2(ms - M);  // empty split: no keys
+    L = fmaf(w, ls, L);
+    const f32x4 v = *reinterpret_cast<const f32x4*>(part + r * D + c);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = fmaf(w, v[j], acc[j]);
+  }
+  const float inv = 1.f / L;
+  bf16x4 out;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) out[j] = to_bf16(acc[j] * inv);
+  *reinterpret_cast<bf16x4*>(o + row * D + c) = out;
+  if (lse != nullptr && c == 0) lse[row] = (M + __log2f(L)) * 0.69314718055994530942f;
+}
+
 // Tile configuration per head dimension: waves per workgroup (32 query rows
 // each) and keys per step.  With D = 128 a workgroup of 8 waves shares each
 // staged K/V tile among 256 queries, halving L2 -> LDS traffic per MFMA; with
@@ -251,13 +319,56 @@ template <int D, bool CACHED>
 static hipError_t launch_fwd_cfg(FwdParams p, hipStream_t stream) {
   constexpr int NW = FwdCfg<D>::NW, BN = FwdCfg<D>::BN;
   p.n_qtiles = (p.Tq + 32 * NW - 1) / (32 * NW);
-  hipLaunchKernelGGL((attn_fwd_kernel<D, CACHED, NW, BN>), dim3(p.n_qtiles * p.BH), dim3(64 * NW), 0, stream, p);
+  if (p.n_splits < 1) p.n_splits = 1;
+  hipLaunchKernelGGL((attn_fwd_kernel<D, CACHED, NW, BN>), dim3(p.n_qtiles * p.BH * p.n_splits), dim3(64 * NW), 0,
+                     stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.n_splits == 1) return e;
+  const long long rows = (long long)p.BH * p.Tq;
+  const long long threads = rows * (D / 4);
+  hipLaunchKernelGGL(attn_combine_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p.part,
+                     p.o, p.lse, p.n_splits, rows);
   return hipGetLastError();
 }
 
 hipError_t launch_fwd(const FwdParams& p, int D, bool cached, hipStream_t stream) {
   if (D == 64) return cached ? launch_fwd_cfg<64, true>(p, stream) : launch_fwd_cfg<64, false>(p, stream);
   return cached ? launch_fwd_cfg<128, true>(p, stream) : launch_fwd_cfg<128, false>(p, stream);
+}
+
+size_t fwd_split_bytes(int D, int BH, int Tq, int n_splits) {
+  if (n_splits <= 1) return 0;
+  return (size_t)n_splits * BH * Tq * (D + 2) * sizeof(float);
+}
+
+// Split count from a small cost model: the unsplit work runs in
+// max(MFMA time, K/V streaming time); a grid of `base * ns` workgroups fills
+// its last round of the GPU's workgroup slots only partly (efficiency =
+// grid / (rounds * slots)); each split adds fp32 partials written and read
+// back.  The count with the lowest estimate wins (each split keeps at least
+// two key tiles; at most 64 splits; bounded by the workspace).
+int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes) {
+  const int NW = D == 64 ? FwdCfg<64>::NW : FwdCfg<128>::NW;
+  const int BN = D == 64 ? FwdCfg<64>::BN : FwdCfg<128>::BN;
+  const int wg_per_cu = D == 64 ? 3 : 2;  // resident workgroups per CU (registers / LDS)
+  const double slots = 256.0 * wg_per_cu;
+  const double base = (double)((Tq + 32 * NW - 1) / (32 * NW)) * BH;
+  const double pairs = (double)BH * Tq * std::max(1.0, (double)Tk - 0.5 * Tq);
+  const double t_work = std::max(4.0 * pairs * D / 0.8e15, 2.0 * BH * (double)Tk * D * 2 / 4.0e12);
+  const int ns_max = (int)std::min<long long>(64, std::max(1, (Tk / BN) / 2));
+  int best = 1;
+  double best_t = 1e30;
+  for (int ns = 1; ns <= ns_max; ++ns) {
+    if (ns > 1 && fwd_split_bytes(D, BH, Tq, ns) > ws_bytes) break;
+    const double grid = base * ns;
+    const double eff = grid / (std::ceil(grid / slots) * slots);
+    const double t = t_work / eff + (ns > 1 ? 2.0 * fwd_split_bytes(D, BH, Tq, ns) / 4.0e12 : 0.0);
+    if (t < best_t * 0.98) {  // prefer fewer splits unless clearly better
+      best_t = t;
+      best = ns;
+    }
+  }
+  return best;
 }
 
 }  // namespace mw

@@ -129,7 +129,8 @@ int mw_block_causal_attn_bwd(const void* q, const void* k, const void* v, const 
   p.L = chunk_len > T ? T : chunk_len;
   p.scale = scale;
   p.scale_log2 = scale * kLog2e;
-  return hip_status(fn, mw::launch_bwd(p, D, static_cast<hipStream_t>(stream)));
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  return hip_status(fn, D == 64 ? mw::launch_bwd_64(p, hs) : mw::launch_bwd_128(p, hs));
 }
 
 int mw_kvcache_init(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, int H, int L, int D) {
@@ -203,21 +204,38 @@ int mw_kvcache_slot_of(const mw_kvcache* c, int64_t chunk) {
   return (int)(chunk % c->S);
 }
 
+static long long window_chunks(const mw_kvcache* c, int window) {
+  const long long live = c->head - c->tail;
+  return window < 0 ? live : window;
+}
+
+size_t mw_chunk_attn_cached_workspace_size(const mw_kvcache* c, int n_queued, int q_len, int window) {
+  if (c == nullptr || n_queued < 1 || q_len < 1 || c->L < 1 || (c->D != 64 && c->D != 128)) return 0;
+  const long long w = window_chunks(c, window);
+  const long long tq = (long long)n_queued * q_len;
+  const long long tk = w * c->L + tq;
+  if (tq > kMaxT || tk > kMaxT) return 0;
+  const int bh = c->B * c->H;
+  const int ns = mw::fwd_choose_splits(c->D, bh, (int)tq, (int)tk, (size_t)-1);
+  return mw::fwd_split_bytes(c->D, bh, (int)tq, ns);
+}
+
 int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new, int n_queued, int q_len,
                          const mw_kvcache* c, int window, int flags, void* o, float* lse, float scale,
-                         mw_stream_t stream) {
+                         void* workspace, size_t workspace_bytes, mw_stream_t stream) {
   const char* fn = "mw_chunk_attn_cached";
   int st = check_cache(fn, c);
   if (st) return st;
   st = check_ptrs(fn, {{"q", q}, {"k_new", k_new}, {"v_new", v_new}, {"o", o}});
   if (st) return st;
   if (lse != nullptr && !aligned16(lse)) return fail(MW_EALIGN, "%s: lse is not 16-byte aligned", fn);
+  if (workspace != nullptr && !aligned16(workspace)) return fail(MW_EALIGN, "%s: workspace is not 16-byte aligned", fn);
   if (n_queued < 1 || q_len < 1) return fail(MW_EINVAL, "%s: n_queued and q_len must be >= 1", fn);
   if (flags != MW_QUEUED_CAUSAL && flags != MW_QUEUED_ISOLATED) return fail(MW_EINVAL, "%s: unknown flags %d", fn, flags);
   if (!(scale > 0.f) || !std::isfinite(scale)) return fail(MW_EINVAL, "%s: scale must be finite and > 0", fn);
   const long long live = c->head - c->tail;
   if (window < -1) return fail(MW_EINVAL, "%s: window must be >= -1", fn);
-  const long long w = window == -1 ? live : window;
+  const long long w = window_chunks(c, window);
   if (w > live) return fail(MW_EINVAL, "%s: window %d exceeds the %lld live chunks", fn, window, live);
   if (w > MW_MAX_WINDOW) return fail(MW_EUNSUPPORTED, "%s: window %lld exceeds %d", fn, w, MW_MAX_WINDOW);
   if (n_queued > MW_MAX_QUEUED) return fail(MW_EUNSUPPORTED, "%s: n_queued %d exceeds %d", fn, n_queued, MW_MAX_QUEUED);
@@ -243,6 +261,8 @@ int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new, in
   p.slot_stride = (long long)c->B * c->H * c->L * c->D;
   p.S = c->S;
   p.first_slot = (int)((c->head - w) % c->S);
+  p.n_splits = mw::fwd_choose_splits(c->D, p.BH, p.Tq, p.Tk, workspace != nullptr ? workspace_bytes : 0);
+  p.part = static_cast<float*>(workspace);
   return hip_status(fn, mw::launch_fwd(p, c->D, true, static_cast<hipStream_t>(stream)));
 }
 

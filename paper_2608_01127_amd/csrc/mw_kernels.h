@@ -30,6 +30,10 @@ struct FwdParams {
   long long slot_stride;  // elements per slot (B*H*L*D)
   int S;                  // ring capacity in slots
   int first_slot;         // slot of the oldest window chunk; chunk i of the window is in slot (first_slot+i)%S
+  // key-range splitting (n_splits > 1): each workgroup covers 1/n_splits of its
+  // query tile's key tiles and writes fp32 partials (see attn_fwd.hip)
+  int n_splits;
+  float* part;  // [n_splits][BH][Tq][D] unnormalised O, then [n_splits][BH][Tq][2] (m, l)
 };
 
 struct BwdParams {
@@ -52,13 +56,16 @@ struct BwdParams {
 };
 
 // Tile sizes (shared with the host for grid computation).
-constexpr int DKV_BN = 128;   // keys per workgroup in the dK/dV kernel
 constexpr int DKV_BM = 64;    // queries per step in the dK/dV kernel
-constexpr int DQ_BM = 128;    // queries per workgroup in the dQ kernel
 constexpr int DQ_BN = 64;     // keys per step in the dQ kernel
 
 hipError_t launch_fwd(const FwdParams& p, int D, bool cached, hipStream_t stream);
-hipError_t launch_bwd(const BwdParams& p, int D, hipStream_t stream);
+// Split count the cached launcher uses for this shape given `ws_bytes` of
+// workspace (1 = no split), and the workspace bytes a split count needs.
+int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes);
+size_t fwd_split_bytes(int D, int BH, int Tq, int n_splits);
+hipError_t launch_bwd_64(const BwdParams& p, hipStream_t stream);
+hipError_t launch_bwd_128(const BwdParams& p, hipStream_t stream);
 hipError_t launch_kv_copy(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_dst,
                           uint16_t* v_dst, long long n_elems, hipStream_t stream);
 

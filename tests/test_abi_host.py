@@ -119,18 +119,34 @@ def test_ring_full_empty_and_window_errors():
     assert lib.mw_kvcache_evict(ctypes.byref(c), 4) == mw.MW_EEMPTY
     assert lib.mw_kvcache_evict(ctypes.byref(c), -1) == mw.MW_EINVAL
     assert c.tail == 0
-    cached = lib.mw_chunk_attn_cached
-    assert cached(A, A, A, 2, 16, ctypes.byref(c), 4, 0, A, None, 0.125, None) == mw.MW_EINVAL and "window" in err()
-    assert cached(A, A, A, 2, 16, ctypes.byref(c), -2, 0, A, None, 0.125, None) == mw.MW_EINVAL
-    assert cached(A, A, A, 2, 16, ctypes.byref(c), 1, 7, A, None, 0.125, None) == mw.MW_EINVAL
-    assert cached(A, A, A, 0, 16, ctypes.byref(c), 1, 0, A, None, 0.125, None) == mw.MW_EINVAL
-    assert cached(A, A, A, 2, 16, ctypes.byref(c), 1, 0, A, U, 0.125, None) == mw.MW_EALIGN
-    assert cached(A, None, A, 2, 16, ctypes.byref(c), 1, 0, A, None, 0.125, None) == mw.MW_EINVAL
-    assert cached(A, A, A, 65, 16, ctypes.byref(c), 1, 0, A, None, 0.125, None) == mw.MW_EUNSUPPORTED
+    cached = lambda *a: lib.mw_chunk_attn_cached(*a[:11], None, 0, None)
+    assert cached(A, A, A, 2, 16, ctypes.byref(c), 4, 0, A, None, 0.125) == mw.MW_EINVAL and "window" in err()
+    assert cached(A, A, A, 2, 16, ctypes.byref(c), -2, 0, A, None, 0.125) == mw.MW_EINVAL
+    assert cached(A, A, A, 2, 16, ctypes.byref(c), 1, 7, A, None, 0.125) == mw.MW_EINVAL
+    assert cached(A, A, A, 0, 16, ctypes.byref(c), 1, 0, A, None, 0.125) == mw.MW_EINVAL
+    assert cached(A, A, A, 2, 16, ctypes.byref(c), 1, 0, A, U, 0.125) == mw.MW_EALIGN
+    assert cached(A, None, A, 2, 16, ctypes.byref(c), 1, 0, A, None, 0.125) == mw.MW_EINVAL
+    assert cached(A, A, A, 65, 16, ctypes.byref(c), 1, 0, A, None, 0.125) == mw.MW_EUNSUPPORTED
+    assert lib.mw_chunk_attn_cached(A, A, A, 2, 16, ctypes.byref(c), 1, 0, A, None, 0.125, U, 1 << 20,
+                                    None) == mw.MW_EALIGN
     # a corrupt descriptor is rejected
     c.tail = 5
     assert lib.mw_kvcache_evict(ctypes.byref(c), 0) == mw.MW_EINVAL
     assert lib.mw_kvcache_slot_of(None, 0) == -1
+
+
+def test_cached_workspace_size_policy():
+    """The split heuristic asks for workspace only when there are few query tiles."""
+    lib = mw.load()
+    c = new_cache(S=8, B=1, H=16, L=2640, D=128)
+    c.head = 6
+    assert lib.mw_chunk_attn_cached_workspace_size(None, 1, 64, -1) == 0
+    big = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 4, 2640, 6)   # 42 tiles x 16 heads
+    small = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 1, 128, 6)  # one tile per head
+    # per split: fp32 O (D floats) plus (m, l) per query row
+    assert big % (16 * 4 * 2640 * 130 * 4) == 0
+    assert small % (16 * 128 * 130 * 4) == 0 and small // (16 * 128 * 130 * 4) >= 8
+    assert lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 0, 128, 6) == 0
 
 
 def test_snapshot_restore_descriptor():

@@ -23,6 +23,7 @@ def queued(B, H, nq, qlen, D, seed):
     return {n: synth.normal_bf16((B, H, nq * qlen, D), seed + i) for i, n in enumerate(("q", "k_new", "v_new"))}
 
 
+@pytest.mark.parametrize("split", [True, False])
 @pytest.mark.parametrize("mode", [0, 1])
 @pytest.mark.parametrize("B,H,D,L,S,n_commit,window,nq,qlen", [
     (1, 2, 64, 96, 4, 6, 3, 2, 96),      # wrapped ring, chunk edges inside tiles
@@ -30,9 +31,9 @@ def queued(B, H, nq, qlen, D, seed):
     (1, 2, 64, 100, 3, 2, 0, 2, 70),     # empty window, queued chunks of another length
     (1, 1, 128, 64, 8, 9, 7, 4, 33),     # short queued chunks
 ])
-def test_cached_attention_vs_oracle(mw, mode, B, H, D, L, S, n_commit, window, nq, qlen):
-    print(f"[case] cached mode={mode} B={B} H={H} D={D} L={L} S={S} commits={n_commit} w={window} nq={nq} qlen={qlen}",
-          flush=True)
+def test_cached_attention_vs_oracle(mw, split, mode, B, H, D, L, S, n_commit, window, nq, qlen):
+    print(f"[case] cached split={split} mode={mode} B={B} H={H} D={D} L={L} S={S} commits={n_commit} w={window} "
+          f"nq={nq} qlen={qlen}", flush=True)
     cache = mw.KVCache(S, B, H, L, D)
     chunks = make_chunks(n_commit, B, H, L, D, seed=300 + L)
     ring = oracle.RingModel(S)
@@ -45,7 +46,7 @@ def test_cached_attention_vs_oracle(mw, mode, B, H, D, L, S, n_commit, window, n
     win = ring.window(None if window == -1 else window)
     inp = queued(B, H, nq, qlen, D, seed=400 + qlen)
     o, lse = mw.mw_chunk_attn_cached(to_gpu(inp["q"]), to_gpu(inp["k_new"]), to_gpu(inp["v_new"]), nq, qlen, cache,
-                                     window=window, flags=mode, want_lse=True)
+                                     window=window, flags=mode, want_lse=True, split=split)
     sync()
     ro, rl = oracle.cached_chunk_attn(f64(inp["q"]), f64(inp["k_new"]), f64(inp["v_new"]),
                                       [f64(chunks[c][0]) for c in win], [f64(chunks[c][1]) for c in win],
@@ -64,8 +65,9 @@ def test_cached_full_history_equals_training_rows(mw):
     for kc, vc in hist:
         mw.mw_kvcache_append(cache, to_gpu(kc), to_gpu(vc))
     inp = queued(B, H, nq, L, D, seed=600)
+    # single pass: the split path sums partial results in another order
     o, lse = mw.mw_chunk_attn_cached(to_gpu(inp["q"]), to_gpu(inp["k_new"]), to_gpu(inp["v_new"]), nq, L, cache,
-                                     want_lse=True)
+                                     want_lse=True, split=False)
     K = np.concatenate([c[0] for c in hist] + [inp["k_new"]], axis=2)
     V = np.concatenate([c[1] for c in hist] + [inp["v_new"]], axis=2)
     Q = np.concatenate([np.zeros_like(c[0]) for c in hist] + [inp["q"]], axis=2)
@@ -76,8 +78,10 @@ def test_cached_full_history_equals_training_rows(mw):
     assert torch.equal(lse, lf[:, :, n0:].contiguous())
 
 
-def test_wraparound_invariance(mw):
-    """The same logical window at different ring offsets gives bit-identical outputs."""
+@pytest.mark.parametrize("split", [True, False])
+def test_wraparound_invariance(mw, split):
+    """The same logical window at different ring offsets gives bit-identical outputs
+    (split boundaries depend only on the shape, so this holds with splitting too)."""
     B, H, D, L, S, w, nq = 1, 2, 64, 128, 5, 3, 2
     chunks = make_chunks(w, B, H, L, D, seed=700)
     inp = queued(B, H, nq, L, D, seed=800)
@@ -91,7 +95,8 @@ def test_wraparound_invariance(mw):
         for kc, vc in chunks:
             mw.mw_kvcache_append(cache, to_gpu(kc), to_gpu(vc))
         assert cache.slot_of(cache.head - w) == offset % S
-        o, _ = mw.mw_chunk_attn_cached(to_gpu(inp["q"]), to_gpu(inp["k_new"]), to_gpu(inp["v_new"]), nq, L, cache)
+        o, _ = mw.mw_chunk_attn_cached(to_gpu(inp["q"]), to_gpu(inp["k_new"]), to_gpu(inp["v_new"]), nq, L, cache,
+                                       split=split)
         sync()
         outs.append(o)
     for o in outs[1:]:
@@ -157,6 +162,30 @@ def test_ring_errors_and_slots(mw):
         assert bits_equal(cache.k_slots[slot], to_gpu(chunks[c][0]))
         assert bits_equal(cache.v_slots[slot], to_gpu(chunks[c][1]))
     assert cache.slot_of(0) == -1
+
+
+@pytest.mark.parametrize("q_len", [64, 256])
+def test_decode_shape_split_vs_oracle(mw, q_len):
+    """One short queued chunk over a full 6-chunk window (B1 H16 D128, 2640-token chunks):
+    few query tiles, so the key range is split over many workgroups."""
+    s = synth.STREAM
+    print(f"[case] decode q_len={q_len}", flush=True)
+    cache = mw.KVCache(s.slots, s.B, s.H, s.chunk_len, s.D)
+    hist = make_chunks(s.window, s.B, s.H, s.chunk_len, s.D, seed=s.seed_base + 70)
+    for kc, vc in hist:
+        mw.mw_kvcache_append(cache, to_gpu(kc), to_gpu(vc))
+    assert mw.mw_chunk_attn_cached_workspace_size(cache, 1, q_len) > 0
+    inp = queued(s.B, s.H, 1, q_len, s.D, seed=s.seed_base + 80 + q_len)
+    o, lse = mw.mw_chunk_attn_cached(to_gpu(inp["q"]), to_gpu(inp["k_new"]), to_gpu(inp["v_new"]), 1, q_len, cache,
+                                     want_lse=True)
+    o1, _ = mw.mw_chunk_attn_cached(to_gpu(inp["q"]), to_gpu(inp["k_new"]), to_gpu(inp["v_new"]), 1, q_len, cache,
+                                    split=False)
+    sync()
+    ro, rl = oracle.cached_chunk_attn(f64(inp["q"]), f64(inp["k_new"]), f64(inp["v_new"]),
+                                      [f64(c[0]) for c in hist], [f64(c[1]) for c in hist], 1, q_len)
+    assert_close("o split", to_f64(o), ro)
+    assert_close("lse split", to_f64(lse), rl, max_abs=2e-3, mean_abs=2e-4)
+    assert_close("o single pass", to_f64(o1), ro)
 
 
 @pytest.fixture(scope="module")
