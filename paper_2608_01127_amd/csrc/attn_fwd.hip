@@ -68,10 +68,14 @@ __device__ __forceinline__ void stage_kv(const FwdParams& p, int bh, long long k
 // O rescale is skipped on almost every step.
 constexpr float kRescaleThreshold = 8.f;
 
-// NW waves per workgroup, each owning 32 query rows; BN keys per main-loop step.
-template <int D, bool CACHED, int NW, int BN>
+// NW waves per workgroup, each owning RB blocks of 32 query rows; BN keys per
+// main-loop step.  With RB = 2 every K and V fragment read from LDS feeds two
+// MFMAs (one per row block), halving LDS traffic per MFMA: with one 32-row
+// block per wave the LDS bandwidth (128 B/clk/CU) equals what four waves
+// consume at the full MFMA rate.
+template <int D, bool CACHED, int NW, int BN, int RB>
 __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) {
-  constexpr int BM = 32 * NW, NT = 64 * NW, KB = BN / 32;
+  constexpr int BM = 32 * RB * NW, NT = 64 * NW, KB = BN / 32;
   constexpr int KK = D / 16;  // contraction steps over D
   constexpr int DB = D / 32;  // 32-wide column blocks of D
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BN * D];
@@ -84,25 +88,28 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
   const int qt = p.n_qtiles - 1 - (logical / NS) % p.n_qtiles;  // heaviest (last) query tile first
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q0 = qt * BM;
-  const int qrow = q0 + wave * 32 + (lane & 31);
   const long long qoff = (long long)bh * p.Tq * D;
 
   Vis vis{p.vis_mode, p.L, p.Tk, p.qlen, p.wL};
 
-  // Q fragments: B operand of S^T = K Q^T (lane holds Q[qrow][16kk + 8(l/32) + 0..7]).
-  bf16x8 qf[KK];
+  // Per row block: this lane's query row, its Q fragments (B operand of
+  // S^T = K Q^T: Q[qrow][16kk + 8(l/32) + 0..7]) and its visible key ranges.
+  int qrow[RB], e1[RB], s2[RB], e2[RB];
+  bf16x8 qf[RB][KK];
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) {
-    if (qrow < p.Tq) {
-      qf[kk] = *reinterpret_cast<const bf16x8*>(p.q + qoff + (long long)qrow * D + 16 * kk + 8 * (lane >> 5));
-    } else {
+  for (int rb = 0; rb < RB; ++rb) {
+    qrow[rb] = q0 + (wave * RB + rb) * 32 + (lane & 31);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) qf[kk][j] = (__bf16)0.f;
+    for (int kk = 0; kk < KK; ++kk) {
+      if (qrow[rb] < p.Tq) {
+        qf[rb][kk] = *reinterpret_cast<const bf16x8*>(p.q + qoff + (long long)qrow[rb] * D + 16 * kk + 8 * (lane >> 5));
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) qf[rb][kk][j] = (__bf16)0.f;
+      }
     }
+    vis.range(min(qrow[rb], p.Tq - 1), e1[rb], s2[rb], e2[rb]);
   }
-
-  int e1, s2, e2;
-  vis.range(min(qrow, p.Tq - 1), e1, s2, e2);
   int e1f, s2f, e2f, e1l, s2l, e2l;
   vis.range(q0, e1f, s2f, e2f);
   vis.range(min(q0 + BM, p.Tq) - 1, e1l, s2l, e2l);
@@ -118,10 +125,15 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
     return n;
   };
 
-  f32x16 o[DB];
+  f32x16 o[RB][DB];
+  float m[RB], lsum[RB];
 #pragma unroll
-  for (int db = 0; db < DB; ++db) o[db] = zero16();
-  float m = -INFINITY, lsum = 0.f;
+  for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[rb][db] = zero16();
+    m[rb] = -INFINITY;
+    lsum[rb] = 0.f;
+  }
   const float c = p.scale_log2;
 
   const long long kvoff = (long long)bh * (CACHED ? (long long)p.Tq * D : (long long)p.Tk * D);
@@ -133,73 +145,99 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
   const int kfull = max(0, (e1f / BN) * BN);
 
   auto step = [&](auto masked, const int k0, const bf16_t* Kt, const bf16_t* Vt) {
-    // S^T for KB 32-key blocks (independent accumulation chains interleaved)
-    f32x16 s[KB];
+    // S^T for KB 32-key blocks x RB row blocks; each K fragment is read once
+    f32x16 s[RB][KB];
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) s[kb] = zero16();
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) s[rb][kb] = zero16();
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-        s[kb] = mfma32(lds_row8<D>(Kt, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), qf[kk], s[kb]);
+      for (int kb = 0; kb < KB; ++kb) {
+        const bf16x8 kfrag = lds_row8<D>(Kt, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5));
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) s[rb][kb] = mfma32(kfrag, qf[rb][kk], s[rb][kb]);
+      }
     }
 
     if constexpr (decltype(masked)::value) {
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) {
+      for (int rb = 0; rb < RB; ++rb) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = k0 + kb * 32 + acc_row(i, lane);
-          // non-short-circuit form: evaluated as compares and one select, without
-          // branches (a branchy lowering of the short-circuit form clobbered the
-          // accumulator element before the second range was tested)
-          const bool ok = (key < e1) | ((key >= s2) & (key < e2));
-          s[kb][i] = ok ? s[kb][i] : -INFINITY;
+        for (int kb = 0; kb < KB; ++kb) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int key = k0 + kb * 32 + acc_row(i, lane);
+            // non-short-circuit form: evaluated as compares and one select, without
+            // branches (a branchy lowering of the short-circuit form clobbered the
+            // accumulator element before the second range was tested)
+            const bool ok = (key < e1[rb]) | ((key >= s2[rb]) & (key < e2[rb]));
+            s[rb][kb][i] = ok ? s[rb][kb][i] : -INFINITY;
+          }
         }
       }
     }
-    float mx = -INFINITY;
+    float mx[RB];
+    bool need_any = false;
+    bool need[RB];
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
+    for (int rb = 0; rb < RB; ++rb) {
+      mx[rb] = -INFINITY;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c;  // scaled row max of this tile (log2 units)
-    const bool need = mx > m + kRescaleThreshold;
-    if (wave_any(need)) {
-      // lanes that move their max rescale by 2^(m - mx) (0 while m is still -inf);
-      // the others keep alpha = 1 (their m may still be -inf: no -inf - -inf)
-      const float alpha = need ? fast_exp2(m - mx) : 1.f;
-      const float mnew = need ? mx : m;
-      lsum *= alpha;
+      for (int kb = 0; kb < KB; ++kb) {
 #pragma unroll
-      for (int db = 0; db < DB; ++db) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
+        for (int i = 0; i < 16; ++i) mx[rb] = fmaxf(mx[rb], s[rb][kb][i]);
       }
-      m = mnew;
+      mx[rb] = fmaxf(mx[rb], __shfl_xor(mx[rb], 32)) * c;  // scaled row max of this tile (log2 units)
+      need[rb] = mx[rb] > m[rb] + kRescaleThreshold;
+      need_any |= need[rb];
     }
-    const float nm = (m == -INFINITY) ? 0.f : -m;
-    float ls = 0.f;
+    if (wave_any(need_any)) {
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
+      for (int rb = 0; rb < RB; ++rb) {
+        // lanes that move their max rescale by 2^(m - mx) (0 while m is still -inf);
+        // the others keep alpha = 1 (their m may still be -inf: no -inf - -inf)
+        const float alpha = need[rb] ? fast_exp2(m[rb] - mx[rb]) : 1.f;
+        lsum[rb] *= alpha;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float pv = fast_exp2(fmaf(s[kb][i], c, nm));
-        s[kb][i] = pv;
-        ls += pv;
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i) o[rb][db][i] *= alpha;
+        }
+        m[rb] = need[rb] ? mx[rb] : m[rb];
       }
     }
-    lsum += ls;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const float nm = (m[rb] == -INFINITY) ? 0.f : -m[rb];
+      float ls = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float pv = fast_exp2(fmaf(s[rb][kb][i], c, nm));
+          s[rb][kb][i] = pv;
+          ls += pv;
+        }
+      }
+      lsum[rb] += ls;
+    }
 
+    // O^T += V^T P^T; each V fragment is read once for all row blocks
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        const bf16x8 pb = pack8(s[kb], t);
+        bf16x8 pb[RB];
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
-          o[db] = mfma32(lds_tr8<D>(Vt, kb * 32, t, db * 32, lane), pb, o[db]);
+        for (int rb = 0; rb < RB; ++rb) pb[rb] = pack8(s[rb][kb], t);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const bf16x8 vfrag = lds_tr8<D>(Vt, kb * 32, t, db * 32, lane);
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) o[rb][db] = mfma32(vfrag, pb[rb], o[rb][db]);
+        }
       }
     }
   };
@@ -225,13 +263,15 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
   run(std::false_type{}, min(kfull, kend));
   run(std::true_type{}, kend);
 
-  if (NS > 1) {
-    // partial result of this key range: unnormalised O, the reference max m
-    // (log2 units, possibly stale by up to the rescale threshold) and the sum
-    // l of 2^(s - m); rows past Tq are not written
-    lsum += __shfl_xor(lsum, 32);
-    if (qrow < p.Tq) {
-      const long long row = ((long long)split * p.BH + bh) * p.Tq + qrow;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    lsum[rb] += __shfl_xor(lsum[rb], 32);
+    if (qrow[rb] >= p.Tq) continue;
+    if (NS > 1) {
+      // partial result of this key range: unnormalised O, the reference max m
+      // (log2 units, possibly stale by up to the rescale threshold) and the sum
+      // l of 2^(s - m); rows past Tq are not written
+      const long long row = ((long long)split * p.BH + bh) * p.Tq + qrow[rb];
       float* po = p.part + row * D;
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
@@ -239,38 +279,45 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
         for (int g = 0; g < 4; ++g) {
           f32x4 w;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) w[j] = o[db][4 * g + j];
+          for (int j = 0; j < 4; ++j) w[j] = o[rb][db][4 * g + j];
           *reinterpret_cast<f32x4*>(po + db * 32 + 8 * g + 4 * (lane >> 5)) = w;
         }
       }
       if (lane < 32) {
         float* ml = p.part + (long long)NS * p.BH * p.Tq * D + 2 * row;
-        ml[0] = m;
-        ml[1] = lsum;
+        ml[0] = m[rb];
+        ml[1] = lsum[rb];
       }
-    }
-    return;
-  }
-
-  lsum += __shfl_xor(lsum, 32);
-  if (qrow < p.Tq) {
-    const float inv = 1.f / lsum;
-    bf16_t* orow = p.o + qoff + (long long)qrow * D;
+    } else {
+      const float inv = 1.f / lsum[rb];
+      bf16_t* orow = p.o + qoff + (long long)qrow[rb] * D;
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
+      for (int db = 0; db < DB; ++db) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        bf16x4 w;
+        for (int g = 0; g < 4; ++g) {
+          bf16x4 w;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) w[j] = to_bf16(o[db][4 * g + j] * inv);
-        *reinterpret_cast<bf16x4*>(orow + db * 32 + 8 * g + 4 * (lane >> 5)) = w;
+          for (int j = 0; j < 4; ++j) w[j] = to_bf16(o[rb][db][4 * g + j] * inv);
+          *reinterpret_cast<bf16x4*>(orow + db * 32 + 8 * g + 4 * (lane >> 5)) = w;
+        }
       }
-    }
-    if (p.lse != nullptr && lane < 32) {
-      p.lse[(long long)bh * p.Tq + qrow] = (m + __log2f(lsum)) * 0.69314718055994530942f;
+      if (p.lse != nullptr && lane < 32) {
+        p.lse[(long long)bh * p.Tq + qrow[rb]] = (m[rb] + __log2f(lsum[rb])) * 0.69314718055994530942f;
+      }
     }
   }
 }
+
+// Tile configuration per head dimension: waves per workgroup (32 query rows
+// each) and keys per step.  With D = 128 a workgroup of 8 waves shares each
+// staged K/V tile among 256 queries, halving L2 -> LDS traffic per MFMA; with
+// D = 64 four waves and a third workgroup per CU measured faster.
+template <int D>
+struct FwdCfg {
+  static constexpr int NW = D == 64 ? 4 : 8;
+  static constexpr int BN = 64;
+  static constexpr int RB = D == 64 ? 2 : 1;  // 32-row query blocks per wave
+};
 
 // Merge of the per-split partials: with M = max_s m_s and w_s = 2^(m_s - M),
 //   O = sum_s w_s O_s / sum_s w_s l_s,   LSE = (M + log2 sum_s w_s l_s) ln 2.
@@ -305,23 +352,13 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   if (lse != nullptr && c == 0) lse[row] = (M + __log2f(L)) * 0.69314718055994530942f;
 }
 
-// Tile configuration per head dimension: waves per workgroup (32 query rows
-// each) and keys per step.  With D = 128 a workgroup of 8 waves shares each
-// staged K/V tile among 256 queries, halving L2 -> LDS traffic per MFMA; with
-// D = 64 four waves and a third workgroup per CU measured faster.
-template <int D>
-struct FwdCfg {
-  static constexpr int NW = D == 64 ? 4 : 8;
-  static constexpr int BN = 64;
-};
-
 template <int D, bool CACHED>
 static hipError_t launch_fwd_cfg(FwdParams p, hipStream_t stream) {
-  constexpr int NW = FwdCfg<D>::NW, BN = FwdCfg<D>::BN;
-  p.n_qtiles = (p.Tq + 32 * NW - 1) / (32 * NW);
+  constexpr int NW = FwdCfg<D>::NW, BN = FwdCfg<D>::BN, RB = FwdCfg<D>::RB;
+  p.n_qtiles = (p.Tq + 32 * RB * NW - 1) / (32 * RB * NW);
   if (p.n_splits < 1) p.n_splits = 1;
-  hipLaunchKernelGGL((attn_fwd_kernel<D, CACHED, NW, BN>), dim3(p.n_qtiles * p.BH * p.n_splits), dim3(64 * NW), 0,
-                     stream, p);
+  hipLaunchKernelGGL((attn_fwd_kernel<D, CACHED, NW, BN, RB>), dim3(p.n_qtiles * p.BH * p.n_splits), dim3(64 * NW),
+                     0, stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_splits == 1) return e;
   const long long rows = (long long)p.BH * p.Tq;
@@ -331,11 +368,22 @@ static hipError_t launch_fwd_cfg(FwdParams p, hipStream_t stream) {
   return hipGetLastError();
 }
 
-hipError_t launch_fwd(const FwdParams& p, int D, bool cached, hipStream_t stream) {
-  if (D == 64) return cached ? launch_fwd_cfg<64, true>(p, stream) : launch_fwd_cfg<64, false>(p, stream);
+// This file is compiled once per head dimension (MW_FWD_HEAD_DIM = 64 or 128),
+// with the instruction-scheduling option measured faster for each; the merge
+// kernel and the split heuristic live in the D = 128 unit.
+#if MW_FWD_HEAD_DIM == 64
+hipError_t launch_fwd_64(const FwdParams& p, bool cached, hipStream_t stream) {
+  return cached ? launch_fwd_cfg<64, true>(p, stream) : launch_fwd_cfg<64, false>(p, stream);
+}
+#elif MW_FWD_HEAD_DIM == 128
+hipError_t launch_fwd_128(const FwdParams& p, bool cached, hipStream_t stream) {
   return cached ? launch_fwd_cfg<128, true>(p, stream) : launch_fwd_cfg<128, false>(p, stream);
 }
+#else
+#error "compile with -DMW_FWD_HEAD_DIM=64 or -DMW_FWD_HEAD_DIM=128"
+#endif
 
+#if MW_FWD_HEAD_DIM == 128
 size_t fwd_split_bytes(int D, int BH, int Tq, int n_splits) {
   if (n_splits <= 1) return 0;
   return (size_t)n_splits * BH * Tq * (D + 2) * sizeof(float);
@@ -350,9 +398,10 @@ size_t fwd_split_bytes(int D, int BH, int Tq, int n_splits) {
 int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes) {
   const int NW = D == 64 ? FwdCfg<64>::NW : FwdCfg<128>::NW;
   const int BN = D == 64 ? FwdCfg<64>::BN : FwdCfg<128>::BN;
+  const int RB = D == 64 ? FwdCfg<64>::RB : FwdCfg<128>::RB;
   const int wg_per_cu = D == 64 ? 3 : 2;  // resident workgroups per CU (registers / LDS)
   const double slots = 256.0 * wg_per_cu;
-  const double base = (double)((Tq + 32 * NW - 1) / (32 * NW)) * BH;
+  const double base = (double)((Tq + 32 * RB * NW - 1) / (32 * RB * NW)) * BH;
   const double pairs = (double)BH * Tq * std::max(1.0, (double)Tk - 0.5 * Tq);
   const double t_work = std::max(4.0 * pairs * D / 0.8e15, 2.0 * BH * (double)Tk * D * 2 / 4.0e12);
   const int ns_max = (int)std::min<long long>(64, std::max(1, (Tk / BN) / 2));
@@ -370,5 +419,6 @@ int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes) {
   }
   return best;
 }
+#endif  // MW_FWD_HEAD_DIM == 128
 
 }  // namespace mw

@@ -59,7 +59,11 @@ struct BwdParams {
 constexpr int DKV_BM = 64;    // queries per step in the dK/dV kernel
 constexpr int DQ_BN = 64;     // keys per step in the dQ kernel
 
-hipError_t launch_fwd(const FwdParams& p, int D, bool cached, hipStream_t stream);
+hipError_t launch_fwd_64(const FwdParams& p, bool cached, hipStream_t stream);
+hipError_t launch_fwd_128(const FwdParams& p, bool cached, hipStream_t stream);
+inline hipError_t launch_fwd(const FwdParams& p, int D, bool cached, hipStream_t stream) {
+  return D == 64 ? launch_fwd_64(p, cached, stream) : launch_fwd_128(p, cached, stream);
+}
 // Split count the cached launcher uses for this shape given `ws_bytes` of
 // workspace (1 = no split), and the workspace bytes a split count needs.
 int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes);
