@@ -13,6 +13,8 @@ Contents
   (paper Sec. 3.5).
 - ring.py: the integer model of the ring-buffered FIFO KV cache
   (paper Sec. 3.5, "Structured Rolling KV Cache").
+- rope_rotate (attention.py): rotary position embedding on a band of head
+  dimensions, used for the re-shifting of cached keys (paper Sec. 3.5).
 
 Parity status: every function here is pinned by the not-gpu tests in
 tests/test_oracle.py (library special cases, closed forms, invariants,
@@ -28,6 +30,7 @@ from .attention import (  # noqa: F401
     block_causal_attn_fwd_rows,
     cached_visible,
     cached_chunk_attn,
+    rope_rotate,
     QUEUED_CAUSAL,
     QUEUED_ISOLATED,
 )

@@ -158,17 +158,21 @@ def block_causal_attn_bwd(q, k, v, do, chunk_len: int, scale=None, row_block: in
     return dq, dk, dv
 
 
-def cached_visible(n_window: int, chunk_len: int, n_queued: int, q_len: int, mode: int) -> np.ndarray:
+def cached_visible(n_window: int, chunk_len, n_queued: int, q_len: int, mode: int) -> np.ndarray:
     """Visibility of the streaming step (Sec. 3.5) over the virtual key sequence.
 
-    Keys are [window chunks, oldest first (n_window x chunk_len tokens)] followed
-    by [queued chunks 0..n_queued-1 (q_len tokens each)]; queries are the queued
-    chunks.  Virtual chunk ids: window chunk i -> i, queued chunk j -> n_window + j.
+    Keys are [committed history segments, oldest first] followed by [queued
+    chunks 0..n_queued-1 (q_len tokens each)]; queries are the queued chunks.
+    ``chunk_len`` is the length of every history segment (int) or a list of
+    per-segment lengths (a sink segment first, then the window chunks).
+    Virtual chunk ids: history segment i -> i, queued chunk j -> n_window + j.
     QUEUED_CAUSAL: key id <= query id (history plus preceding in-flight chunks).
     QUEUED_ISOLATED: key id < n_window or key id == query id.
-    Returns bool [n_queued*q_len, n_window*chunk_len + n_queued*q_len].
+    Returns bool [n_queued*q_len, sum(history lengths) + n_queued*q_len].
     """
-    key_ids = np.concatenate([np.repeat(np.arange(n_window), chunk_len),
+    lens = [chunk_len] * n_window if np.isscalar(chunk_len) else list(chunk_len)
+    assert len(lens) == n_window
+    key_ids = np.concatenate([np.repeat(np.arange(n_window), lens).astype(int),
                               n_window + np.repeat(np.arange(n_queued), q_len)])
     q_ids = n_window + np.repeat(np.arange(n_queued), q_len)
     if mode == QUEUED_CAUSAL:
@@ -179,21 +183,24 @@ def cached_visible(n_window: int, chunk_len: int, n_queued: int, q_len: int, mod
 
 
 def cached_chunk_attn(q, k_new, v_new, window_k, window_v, n_queued: int, q_len: int,
-                      mode: int = QUEUED_CAUSAL, scale=None, heads=None):
-    """Attention of queued in-flight chunks over [committed window || queued chunks] (Sec. 3.5).
+                      mode: int = QUEUED_CAUSAL, scale=None, heads=None, sink_k=None, sink_v=None):
+    """Attention of queued in-flight chunks over [sink || committed window || queued] (Sec. 3.5).
 
     q, k_new, v_new: [B,H,n_queued*q_len,D]; window_k/window_v: sequences of
-    [B,H,chunk_len,D] arrays in logical order, oldest first (may be empty).
+    [B,H,chunk_len,D] arrays in logical order, oldest first (may be empty);
+    sink_k/sink_v: optional [B,H,sink_len,D], the permanent sink anchor, placed
+    first and visible to every queued chunk like the rest of the history.
     Returns (O [B,H,n_queued*q_len,D], LSE [B,H,n_queued*q_len]).
     """
     q = np.asarray(q, dtype=np.float64)
     B, H, NQ, D = q.shape
     assert NQ == n_queued * q_len
-    w = len(window_k)
-    chunk_len = window_k[0].shape[2] if w else 1
-    xk = np.concatenate([np.asarray(c, np.float64) for c in window_k] + [np.asarray(k_new, np.float64)], axis=2)
-    xv = np.concatenate([np.asarray(c, np.float64) for c in window_v] + [np.asarray(v_new, np.float64)], axis=2)
-    vis = cached_visible(w, chunk_len, n_queued, q_len, mode)
+    hist_k = ([] if sink_k is None else [sink_k]) + list(window_k)
+    hist_v = ([] if sink_v is None else [sink_v]) + list(window_v)
+    lens = [np.asarray(c).shape[2] for c in hist_k]
+    xk = np.concatenate([np.asarray(c, np.float64) for c in hist_k] + [np.asarray(k_new, np.float64)], axis=2)
+    xv = np.concatenate([np.asarray(c, np.float64) for c in hist_v] + [np.asarray(v_new, np.float64)], axis=2)
+    vis = cached_visible(len(hist_k), lens, n_queued, q_len, mode)
     sc = _default_scale(D, scale)
     o = np.zeros((B, H, NQ, xv.shape[-1]))
     lse = np.zeros((B, H, NQ))
@@ -201,3 +208,27 @@ def cached_chunk_attn(q, k_new, v_new, window_k, window_v, n_queued: int, q_len:
     for b, h in pairs:
         o[b, h], lse[b, h] = attention_fwd(q[b, h], xk[b, h], xv[b, h], vis, sc)
     return o, lse
+
+
+def rope_rotate(x, positions, dim_offset: int, dim_count: int, theta: float = 10000.0):
+    """Rotary position embedding on one band of head dimensions (Sec. 3.5, RoPE re-shifting).
+
+    Dimensions [dim_offset, dim_offset + dim_count) form dim_count/2 interleaved
+    pairs (2i, 2i+1); pair i at position p is rotated by the angle
+    p * theta^(-2i/dim_count).  Other dimensions are returned unchanged.
+    x: [..., T, D]; positions: broadcastable to [..., T] (any real numbers).
+    Re-shifting keys by -delta positions is rope_rotate(k, -delta, ...), since
+    rotations by a and b compose to a rotation by a + b.
+    """
+    x = np.array(x, dtype=np.float64, copy=True)
+    assert dim_count % 2 == 0 and dim_offset % 2 == 0 and dim_offset + dim_count <= x.shape[-1]
+    npair = dim_count // 2
+    freq = theta ** (-2.0 * np.arange(npair) / dim_count)
+    ang = np.asarray(positions, dtype=np.float64)[..., None] * freq  # [..., T, npair]
+    band = x[..., dim_offset:dim_offset + dim_count]
+    a, b = band[..., 0::2].copy(), band[..., 1::2].copy()
+    c, s = np.cos(ang), np.sin(ang)
+    band[..., 0::2] = a * c - b * s
+    band[..., 1::2] = a * s + b * c
+    x[..., dim_offset:dim_offset + dim_count] = band
+    return x

@@ -378,3 +378,55 @@ def test_ring_rollout_schedule_and_errors():
         r.window(5)
     with pytest.raises(RingError):
         RingModel(0)
+
+
+# ---------------------------------------------------------------- sink anchor and RoPE re-shift
+
+def test_sink_is_history_visible_to_every_queued_chunk():
+    """A sink segment behaves like one more (shorter) committed chunk placed first."""
+    L, q_len, n_q = 6, 4, 3
+    hk, hv, q, kn, vn = _stream_case(L=L, q_len=q_len, n_q=n_q)
+    sk, sv = rand(1, 2, 3, 8, seed=300), rand(1, 2, 3, 8, seed=301)
+    for mode in (QUEUED_CAUSAL, QUEUED_ISOLATED):
+        o, _ = cached_chunk_attn(q, kn, vn, hk[-2:], hv[-2:], n_q, q_len, mode=mode, sink_k=sk, sink_v=sv)
+        # reference: the isolated/causal rule over [sink, window] with an explicit boolean mask and SDPA
+        K = np.concatenate([sk] + hk[-2:] + [kn], axis=2)
+        V = np.concatenate([sv] + hv[-2:] + [vn], axis=2)
+        nh = 3 + 2 * L
+        mask = np.zeros((n_q * q_len, K.shape[2]), bool)
+        for j in range(n_q):
+            rows = slice(j * q_len, (j + 1) * q_len)
+            mask[rows, :nh] = True
+            lo = nh + (0 if mode == QUEUED_CAUSAL else j * q_len)
+            mask[rows, lo:nh + (j + 1) * q_len] = True
+        ro, _ = sdpa(q, K, V, mask=mask)
+        assert np.max(np.abs(o - ro.detach().numpy())) < 1e-12
+
+
+def test_rope_matches_complex_rotation():
+    """Band rotation equals multiplying each interleaved pair, read as a complex number,
+    by exp(i * p * theta^(-2k/n))."""
+    x = rand(2, 5, 16, seed=310)
+    pos = np.arange(5) * 1.5 - 2
+    off, cnt, th = 4, 8, 500.0
+    y = oracle.rope_rotate(x, pos, off, cnt, th)
+    z = x[..., off:off + cnt:2] + 1j * x[..., off + 1:off + cnt:2]
+    w = z * np.exp(1j * pos[:, None] * th ** (-np.arange(cnt // 2) * 2.0 / cnt))
+    assert np.max(np.abs(y[..., off:off + cnt:2] - w.real)) < 1e-13
+    assert np.max(np.abs(y[..., off + 1:off + cnt:2] - w.imag)) < 1e-13
+    assert np.array_equal(y[..., :off], x[..., :off]) and np.array_equal(y[..., off + cnt:], x[..., off + cnt:])
+
+
+def test_rope_group_properties_and_relative_positions():
+    x = rand(3, 7, 12, seed=320)
+    pa, pb = rand(3, 7, seed=321) * 5, rand(3, 7, seed=322) * 5
+    r = lambda v, p: oracle.rope_rotate(v, p, 2, 8)
+    assert np.max(np.abs(r(x, 0.0) - x)) < 1e-15
+    assert np.max(np.abs(r(r(x, pa), pb) - r(x, pa + pb))) < 1e-12           # R(a) R(b) = R(a+b)
+    assert np.max(np.abs(r(r(x, pa), -pa) - x)) < 1e-12                      # re-shift undoes a shift
+    assert np.max(np.abs(np.linalg.norm(r(x, pa), axis=-1) - np.linalg.norm(x, axis=-1))) < 1e-12
+    # q.k after rotation depends only on the position difference (what re-shifting preserves)
+    q, k = rand(12, seed=323), rand(12, seed=324)
+    d1 = r(q[None], np.array([9.0]))[0] @ r(k[None], np.array([4.0]))[0]
+    d2 = r(q[None], np.array([5.0]))[0] @ r(k[None], np.array([0.0]))[0]
+    assert abs(d1 - d2) < 1e-12
