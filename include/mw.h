@@ -121,13 +121,46 @@ typedef struct {
   void* k_slots;
   void* v_slots;
   int S, B, H, L, D;
-  int64_t head; /* chunks committed so far */
-  int64_t tail; /* chunks evicted so far  */
+  int64_t head;        /* chunks committed so far */
+  int64_t tail;        /* chunks evicted so far  */
+  const void* k_sink;  /* sink anchor (see mw_kvcache_set_sink), or NULL */
+  const void* v_sink;
+  int sink_len;        /* sink tokens (0: no sink) */
 } mw_kvcache;
 
-/* Initialise an empty ring over k_slots/v_slots (bf16 [S,B,H,L,D]); no device work.
+/* Initialise an empty ring over k_slots/v_slots (bf16 [S,B,H,L,D]), without a
+ * sink; no device work.
  * Errors: MW_EINVAL (null, sizes < 1), MW_EALIGN, MW_EUNSUPPORTED (D not 64/128). */
 int mw_kvcache_init(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, int H, int L, int D);
+
+/* Sink anchor (Sec. 3.5): the initial clean context kept permanently, outside
+ * the FIFO.  k_sink, v_sink: caller-owned bf16 [B, H, sink_len, D] (the cache
+ * keeps the pointers, not a copy; the caller keeps them alive and unchanged).
+ * The sink comes first in the key sequence of mw_chunk_attn_cached, is visible
+ * to every queued chunk, is never evicted and is not re-shifted.  sink_len = 0
+ * (pointers ignored) removes it.  Host only.
+ * Errors: MW_EINVAL (null cache, sink_len < 0, null pointers with sink_len > 0),
+ * MW_EALIGN, MW_EUNSUPPORTED (sink_len too large). */
+int mw_kvcache_set_sink(mw_kvcache* c, const void* k_sink, const void* v_sink, int sink_len);
+
+/* Rotary position embedding on one band of the head dimension: dimensions
+ * [dim_offset, dim_offset + dim_count) form dim_count/2 interleaved pairs
+ * (2i, 2i+1); pair i at position p is rotated by p * theta^(-2i/dim_count). */
+typedef struct {
+  int dim_offset; /* even, >= 0 */
+  int dim_count;  /* even, 2..128, dim_offset + dim_count <= D */
+  float theta;    /* > 0, e.g. 10000 */
+} mw_rope;
+
+/* RoPE re-shifting (Sec. 3.5): rotate the keys of every live committed chunk
+ * (not the sink) by -shift positions on the rope band, in place, so the
+ * retained window is re-indexed from the start after `shift` positions of
+ * history were evicted (shift = evicted chunks x positions per chunk).
+ * Relative positions inside the window are unchanged; values are untouched.
+ * Arithmetic: bf16 in, fp32 rotation (cos/sin computed on the host in double),
+ * bf16 out (nearest even).  shift = 0 or no live chunk: no device work.
+ * Errors: MW_EINVAL (null cache or rope, invalid band, theta <= 0), MW_EHIP. */
+int mw_kvcache_rope_shift(mw_kvcache* c, int shift, const mw_rope* rope, mw_stream_t stream);
 
 /* Commit one chunk: enqueue a copy of k_chunk and v_chunk (bf16 [B,H,L,D]) into
  * slot head mod S, then head += 1 (host state changes at call time).
@@ -147,15 +180,16 @@ int mw_kvcache_slot_of(const mw_kvcache* c, int64_t chunk);
 /* ------------------------------------------------------------------------
  * Cached chunk attention for the pipelined denoiser (Sec. 3.5).
  *
- * n_queued in-flight chunks of q_len tokens each attend to the `window`
- * newest live committed chunks (window = -1: all live chunks) and to the
- * in-flight chunks' own keys.  The keys form the virtual sequence
- *   [window chunks, oldest first (window * L tokens)] ++ [queued chunks 0..n_queued-1]
+ * n_queued in-flight chunks of q_len tokens each attend to the sink anchor
+ * (if set), the `window` newest live committed chunks (window = -1: all live
+ * chunks) and the in-flight chunks' own keys.  The keys form the virtual sequence
+ *   [sink (sink_len tokens)] ++ [window chunks, oldest first (window * L tokens)]
+ *   ++ [queued chunks 0..n_queued-1]
  * and queued chunk j sees
- *   MW_QUEUED_CAUSAL  : the window and queued chunks 0..j (the committed history
- *                       plus the preceding chunks of the active window; the
- *                       chunk-wise causal rule of Sec. 3.5);
- *   MW_QUEUED_ISOLATED: the window and itself only.
+ *   MW_QUEUED_CAUSAL  : the sink, the window and queued chunks 0..j (the
+ *                       committed history plus the preceding chunks of the
+ *                       active window; the chunk-wise causal rule of Sec. 3.5);
+ *   MW_QUEUED_ISOLATED: the sink, the window and itself only.
  *
  * q, k_new, v_new, o : bf16 [B, H, n_queued*q_len, D] with B, H, D those of the cache
  * lse                : fp32 [B, H, n_queued*q_len] or NULL

@@ -29,5 +29,8 @@ from ._lib import (  # noqa: F401
     mw_kvcache,
     mw_kvcache_append,
     mw_kvcache_evict,
+    mw_kvcache_rope_shift,
+    mw_kvcache_set_sink,
+    mw_rope,
     mw_kvcache_slot_of,
 )

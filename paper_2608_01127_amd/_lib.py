@@ -39,7 +39,12 @@ class MWError(RuntimeError):
 class mw_kvcache(ctypes.Structure):
     _fields_ = [("k_slots", ctypes.c_void_p), ("v_slots", ctypes.c_void_p),
                 ("S", ctypes.c_int), ("B", ctypes.c_int), ("H", ctypes.c_int), ("L", ctypes.c_int),
-                ("D", ctypes.c_int), ("head", ctypes.c_int64), ("tail", ctypes.c_int64)]
+                ("D", ctypes.c_int), ("head", ctypes.c_int64), ("tail", ctypes.c_int64),
+                ("k_sink", ctypes.c_void_p), ("v_sink", ctypes.c_void_p), ("sink_len", ctypes.c_int)]
+
+
+class mw_rope(ctypes.Structure):
+    _fields_ = [("dim_offset", ctypes.c_int), ("dim_count", ctypes.c_int), ("theta", ctypes.c_float)]
 
 
 # Exported symbols and their signatures (mirrors include/mw.h).
@@ -54,6 +59,8 @@ SIGNATURES = {
     "mw_kvcache_init": ([_cache_p, _vp, _vp, _i, _i, _i, _i, _i], _i),
     "mw_kvcache_append": ([_cache_p, _vp, _vp, _vp], _i),
     "mw_kvcache_evict": ([_cache_p, _i], _i),
+    "mw_kvcache_set_sink": ([_cache_p, _vp, _vp, _i], _i),
+    "mw_kvcache_rope_shift": ([_cache_p, _i, ctypes.POINTER(mw_rope), _vp], _i),
     "mw_kvcache_live": ([_cache_p], _i),
     "mw_kvcache_slot_of": ([_cache_p, ctypes.c_int64], _i),
     "mw_chunk_attn_cached_workspace_size": ([_cache_p, _i, _i, _i], _sz),
@@ -210,6 +217,20 @@ class KVCache:
     def slot_of(self, chunk: int) -> int:
         return int(load().mw_kvcache_slot_of(ctypes.byref(self.desc), int(chunk)))
 
+    def set_sink(self, k_sink, v_sink) -> None:
+        """Keep k_sink/v_sink (bf16 [B,H,sink_len,D]) as the sink anchor; None removes it."""
+        d = self.desc
+        if k_sink is None:
+            _check(load().mw_kvcache_set_sink(ctypes.byref(d), None, None, 0))
+            self._sink = None
+            return
+        for n, t in (("k_sink", k_sink), ("v_sink", v_sink)):
+            _bf16_4d(n, t)
+            if tuple(t.shape[:2]) != (d.B, d.H) or t.shape[3] != d.D or t.shape != k_sink.shape:
+                raise ValueError(f"{n} must be [B,H,sink_len,D] with B,H,D of the cache")
+        _check(load().mw_kvcache_set_sink(ctypes.byref(d), _ptr(k_sink), _ptr(v_sink), int(k_sink.shape[2])))
+        self._sink = (k_sink, v_sink)  # keep the tensors alive while the cache points at them
+
     def snapshot(self) -> tuple:
         return (int(self.desc.head), int(self.desc.tail))
 
@@ -232,6 +253,17 @@ def mw_kvcache_append(cache: KVCache, k_chunk, v_chunk) -> int:
 
 def mw_kvcache_evict(cache: KVCache, n_chunks: int) -> None:
     _check(load().mw_kvcache_evict(ctypes.byref(cache.desc), int(n_chunks)))
+
+
+def mw_kvcache_set_sink(cache: KVCache, k_sink, v_sink) -> None:
+    cache.set_sink(k_sink, v_sink)
+
+
+def mw_kvcache_rope_shift(cache: KVCache, shift: int, dim_offset: int, dim_count: int, theta: float = 10000.0) -> None:
+    """Rotate the keys of all live chunks by -shift positions on the rope band (in place)."""
+    rope = mw_rope(int(dim_offset), int(dim_count), float(theta))
+    _check(load().mw_kvcache_rope_shift(ctypes.byref(cache.desc), int(shift), ctypes.byref(rope),
+                                        _stream_handle(cache.k_slots.device)))
 
 
 def mw_kvcache_slot_of(cache: KVCache, chunk: int) -> int:

@@ -42,11 +42,13 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
 template <int D, bool CACHED, int BN, int NT>
 __device__ __forceinline__ void stage_kv(const FwdParams& p, int bh, long long kvoff, int k0, bf16_t* Kt,
                                          bf16_t* Vt, int tid) {
-  auto src = [&](const uint16_t* win_base, const uint16_t* base, int r) -> const bf16_t* {
+  auto src = [&](const uint16_t* sink_base, const uint16_t* win_base, const uint16_t* base, int r) -> const bf16_t* {
     const int key = min(k0 + r, p.Tk - 1);
     if constexpr (CACHED) {
+      if (key < p.sink_len) return sink_base + ((long long)bh * p.sink_len + key) * D;
       if (key < p.wL) {
-        const int w = key / p.L, off = key - w * p.L;
+        const int kw = key - p.sink_len;
+        const int w = kw / p.L, off = kw - w * p.L;
         int slot = p.first_slot + w;
         slot = slot >= p.S ? slot - p.S : slot;
         return win_base + (long long)slot * p.slot_stride + (long long)bh * p.L * D + (long long)off * D;
@@ -54,11 +56,12 @@ __device__ __forceinline__ void stage_kv(const FwdParams& p, int bh, long long k
       return base + kvoff + (long long)(key - p.wL) * D;
     } else {
       (void)win_base;
+      (void)sink_base;
       return base + kvoff + (long long)key * D;
     }
   };
-  stage_rows_direct<D, BN, NT>(Kt, [&](int r) { return src(p.k_slots, p.k, r); }, tid);
-  stage_rows_direct<D, BN, NT>(Vt, [&](int r) { return src(p.v_slots, p.v, r); }, tid);
+  stage_rows_direct<D, BN, NT>(Kt, [&](int r) { return src(p.k_sink, p.k_slots, p.k, r); }, tid);
+  stage_rows_direct<D, BN, NT>(Vt, [&](int r) { return src(p.v_sink, p.v_slots, p.v, r); }, tid);
 }
 
 // Rows of the running max only move when a tile raises it by more than this

@@ -151,13 +151,17 @@ int mw_kvcache_init(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, i
   c->D = D;
   c->head = 0;
   c->tail = 0;
+  c->k_sink = nullptr;
+  c->v_sink = nullptr;
+  c->sink_len = 0;
   return ok();
 }
 
 static int check_cache(const char* fn, const mw_kvcache* c) {
   if (c == nullptr) return fail(MW_EINVAL, "%s: cache is NULL", fn);
   if (c->k_slots == nullptr || c->v_slots == nullptr || c->S < 1 || c->B < 1 || c->H < 1 || c->L < 1 ||
-      (c->D != 64 && c->D != 128) || c->tail < 0 || c->head < c->tail || c->head - c->tail > c->S)
+      (c->D != 64 && c->D != 128) || c->tail < 0 || c->head < c->tail || c->head - c->tail > c->S ||
+      c->sink_len < 0 || (c->sink_len > 0 && (c->k_sink == nullptr || c->v_sink == nullptr)))
     return fail(MW_EINVAL, "%s: cache descriptor is not initialised or is corrupt", fn);
   return MW_OK;
 }
@@ -178,6 +182,53 @@ int mw_kvcache_append(mw_kvcache* c, const void* k_chunk, const void* v_chunk, m
   if (e != hipSuccess) return hip_status(fn, e);
   c->head += 1;
   return ok();
+}
+
+int mw_kvcache_set_sink(mw_kvcache* c, const void* k_sink, const void* v_sink, int sink_len) {
+  const char* fn = "mw_kvcache_set_sink";
+  int st = check_cache(fn, c);
+  if (st) return st;
+  if (sink_len < 0) return fail(MW_EINVAL, "%s: sink_len must be >= 0", fn);
+  if (sink_len == 0) {
+    c->k_sink = nullptr;
+    c->v_sink = nullptr;
+    c->sink_len = 0;
+    return ok();
+  }
+  st = check_ptrs(fn, {{"k_sink", k_sink}, {"v_sink", v_sink}});
+  if (st) return st;
+  if (sink_len > kMaxT / 2) return fail(MW_EUNSUPPORTED, "%s: sink_len %d too large", fn, sink_len);
+  c->k_sink = k_sink;
+  c->v_sink = v_sink;
+  c->sink_len = sink_len;
+  return ok();
+}
+
+int mw_kvcache_rope_shift(mw_kvcache* c, int shift, const mw_rope* rope, mw_stream_t stream) {
+  const char* fn = "mw_kvcache_rope_shift";
+  int st = check_cache(fn, c);
+  if (st) return st;
+  if (rope == nullptr) return fail(MW_EINVAL, "%s: rope is NULL", fn);
+  if (rope->dim_offset < 0 || rope->dim_offset % 2 || rope->dim_count < 2 || rope->dim_count % 2 ||
+      rope->dim_count > 128 || rope->dim_offset + rope->dim_count > c->D)
+    return fail(MW_EINVAL, "%s: rope band [%d, %d) is not a valid even band of the %d head dims", fn, rope->dim_offset,
+                rope->dim_offset + rope->dim_count, c->D);
+  if (!(rope->theta > 0.f) || !std::isfinite(rope->theta)) return fail(MW_EINVAL, "%s: theta must be > 0", fn);
+  const long long live = c->head - c->tail;
+  if (shift == 0 || live == 0) return ok();
+  mw::RopeTable tab{};
+  const int np = rope->dim_count / 2;
+  for (int i = 0; i < np; ++i) {
+    const double freq = std::pow((double)rope->theta, -2.0 * i / rope->dim_count);
+    const double ang = -(double)shift * freq;
+    tab.c[i] = (float)std::cos(ang);
+    tab.s[i] = (float)std::sin(ang);
+  }
+  const long long rows = (long long)c->B * c->H * c->L;
+  hipError_t e = mw::launch_rope_shift(static_cast<uint16_t*>(c->k_slots), rows * c->D, c->S, (int)(c->tail % c->S),
+                                       (int)live, rows, c->D, rope->dim_offset, np, tab,
+                                       static_cast<hipStream_t>(stream));
+  return hip_status(fn, e);
 }
 
 int mw_kvcache_evict(mw_kvcache* c, int n_chunks) {
@@ -213,7 +264,7 @@ size_t mw_chunk_attn_cached_workspace_size(const mw_kvcache* c, int n_queued, in
   if (c == nullptr || n_queued < 1 || q_len < 1 || c->L < 1 || (c->D != 64 && c->D != 128)) return 0;
   const long long w = window_chunks(c, window);
   const long long tq = (long long)n_queued * q_len;
-  const long long tk = w * c->L + tq;
+  const long long tk = c->sink_len + w * c->L + tq;
   if (tq > kMaxT || tk > kMaxT) return 0;
   const int bh = c->B * c->H;
   const int ns = mw::fwd_choose_splits(c->D, bh, (int)tq, (int)tk, (size_t)-1);
@@ -240,7 +291,7 @@ int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new, in
   if (w > MW_MAX_WINDOW) return fail(MW_EUNSUPPORTED, "%s: window %lld exceeds %d", fn, w, MW_MAX_WINDOW);
   if (n_queued > MW_MAX_QUEUED) return fail(MW_EUNSUPPORTED, "%s: n_queued %d exceeds %d", fn, n_queued, MW_MAX_QUEUED);
   const long long nq_tok = (long long)n_queued * q_len;
-  if (nq_tok + w * c->L > kMaxT) return fail(MW_EUNSUPPORTED, "%s: too many tokens", fn);
+  if (nq_tok + w * c->L + c->sink_len > kMaxT) return fail(MW_EUNSUPPORTED, "%s: too many tokens", fn);
   mw::FwdParams p{};
   p.q = static_cast<const uint16_t*>(q);
   p.k = static_cast<const uint16_t*>(k_new);
@@ -251,7 +302,10 @@ int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new, in
   p.Tq = (int)nq_tok;
   p.vis_mode = flags == MW_QUEUED_CAUSAL ? 1 : 2;
   p.L = c->L;
-  p.wL = (int)(w * c->L);
+  p.sink_len = c->sink_len;
+  p.k_sink = static_cast<const uint16_t*>(c->k_sink);
+  p.v_sink = static_cast<const uint16_t*>(c->v_sink);
+  p.wL = (int)(c->sink_len + w * c->L);
   p.Tk = p.wL + p.Tq;
   p.qlen = q_len;
   p.scale_log2 = scale * kLog2e;

@@ -21,12 +21,15 @@ struct FwdParams {
   int L;         // chunk length (training) / committed chunk length (cached)
   int Tk;        // keys in the (virtual) sequence
   int qlen;      // queued chunk length (cached)
-  int wL;        // window tokens = n_window * L (cached; 0 in training)
+  int wL;        // history tokens = sink_len + n_window * L (cached; 0 in training)
   float scale_log2;  // softmax scale * log2(e)
   float scale_ln;    // unused by the kernels; kept for the host's records
   // cached attention only: the window lives in ring slots
   const uint16_t* k_slots;
   const uint16_t* v_slots;
+  const uint16_t* k_sink;  // [BH, sink_len, D], first in the key sequence
+  const uint16_t* v_sink;
+  int sink_len;
   long long slot_stride;  // elements per slot (B*H*L*D)
   int S;                  // ring capacity in slots
   int first_slot;         // slot of the oldest window chunk; chunk i of the window is in slot (first_slot+i)%S
@@ -70,6 +73,14 @@ int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes);
 size_t fwd_split_bytes(int D, int BH, int Tq, int n_splits);
 hipError_t launch_bwd_64(const BwdParams& p, hipStream_t stream);
 hipError_t launch_bwd_128(const BwdParams& p, hipStream_t stream);
+// cos/sin of the re-shift angle of each rope pair
+struct RopeTable {
+  float c[64];
+  float s[64];
+};
+hipError_t launch_rope_shift(uint16_t* k_slots, long long slot_stride, int S, int first_slot, int n_live,
+                             long long rows_per_slot, int D, int dim_offset, int n_pairs, const RopeTable& tab,
+                             hipStream_t stream);
 hipError_t launch_kv_copy(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_dst,
                           uint16_t* v_dst, long long n_elems, hipStream_t stream);
 

@@ -36,8 +36,10 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_struct_layout_matches_header():
-    assert ctypes.sizeof(_lib.mw_kvcache) == 56
+    assert ctypes.sizeof(_lib.mw_kvcache) == 80
     assert _lib.mw_kvcache.head.offset == 40 and _lib.mw_kvcache.tail.offset == 48
+    assert _lib.mw_kvcache.k_sink.offset == 56 and _lib.mw_kvcache.sink_len.offset == 72
+    assert ctypes.sizeof(_lib.mw_rope) == 12
 
 
 def err():
@@ -147,6 +149,29 @@ def test_cached_workspace_size_policy():
     assert big % (16 * 4 * 2640 * 130 * 4) == 0
     assert small % (16 * 128 * 130 * 4) == 0 and small // (16 * 128 * 130 * 4) >= 8
     assert lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 0, 128, 6) == 0
+
+
+def test_sink_and_rope_validation():
+    lib = mw.load()
+    c = new_cache(S=4, D=128)
+    assert (c.sink_len, c.k_sink) == (0, None)
+    assert lib.mw_kvcache_set_sink(ctypes.byref(c), None, A, 5) == mw.MW_EINVAL
+    assert lib.mw_kvcache_set_sink(ctypes.byref(c), A, U, 5) == mw.MW_EALIGN
+    assert lib.mw_kvcache_set_sink(ctypes.byref(c), A, A, -1) == mw.MW_EINVAL
+    assert lib.mw_kvcache_set_sink(ctypes.byref(c), A, A, 7) == mw.MW_OK and c.sink_len == 7
+    assert lib.mw_kvcache_set_sink(ctypes.byref(c), None, None, 0) == mw.MW_OK and c.sink_len == 0
+    rope = lambda off, cnt, th=10000.0: ctypes.byref(_lib.mw_rope(off, cnt, th))
+    shift = lib.mw_kvcache_rope_shift
+    assert shift(ctypes.byref(c), 3, None, None) == mw.MW_EINVAL
+    assert shift(ctypes.byref(c), 3, rope(1, 8), None) == mw.MW_EINVAL          # odd offset
+    assert shift(ctypes.byref(c), 3, rope(0, 7), None) == mw.MW_EINVAL          # odd count
+    assert shift(ctypes.byref(c), 3, rope(120, 16), None) == mw.MW_EINVAL       # past D
+    assert shift(ctypes.byref(c), 3, rope(0, 130), None) == mw.MW_EINVAL        # more than 64 pairs
+    assert shift(ctypes.byref(c), 3, rope(0, 44, 0.0), None) == mw.MW_EINVAL    # theta
+    # nothing live or shift 0: valid, no device work
+    assert shift(ctypes.byref(c), 3, rope(0, 44), None) == mw.MW_OK
+    c.head = 2
+    assert shift(ctypes.byref(c), 0, rope(0, 44), None) == mw.MW_OK
 
 
 def test_snapshot_restore_descriptor():
