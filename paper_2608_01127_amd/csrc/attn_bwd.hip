@@ -196,9 +196,11 @@ __global__ __launch_bounds__(64 * NW, (D == 64 ? 8 : 4) / NW) void bwd_dkdv_kern
   }
 }
 
-template <int D, int NW>
+// NW waves, each owning RB blocks of 32 query rows: with RB = 2 every K and V
+// fragment read from LDS feeds two MFMAs (one per row block).
+template <int D, int NW, int RB>
 __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, int n_qtiles) {
-  constexpr int BM = 32 * NW, BN = DQ_BN, NT = 64 * NW;
+  constexpr int BM = 32 * RB * NW, BN = DQ_BN, NT = 64 * NW;
   constexpr int KK = D / 16, DB = D / 32;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BN * D];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[2][BN * D];
@@ -209,28 +211,34 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int T = p.T, L = p.L;
   const int q0 = qt * BM;
-  const int qrow = q0 + wave * 32 + (lane & 31);
   const long long off = (long long)bh * T * D;
 
-  bf16x8 qf[KK], df[KK];
-  {
-    const long long a0 = off + (long long)min(qrow, T - 1) * D + 8 * (lane >> 5);
+  int qrow[RB], e1[RB];
+  float lse2[RB], dlt[RB];
+  bf16x8 qf[RB][KK], df[RB][KK];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    qrow[rb] = q0 + (wave * RB + rb) * 32 + (lane & 31);
+    const int qc = min(qrow[rb], T - 1);
+    const long long a0 = off + (long long)qc * D + 8 * (lane >> 5);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      qf[kk] = *reinterpret_cast<const bf16x8*>(p.q + a0 + 16 * kk);
-      df[kk] = *reinterpret_cast<const bf16x8*>(p.d_o + a0 + 16 * kk);
+      qf[rb][kk] = *reinterpret_cast<const bf16x8*>(p.q + a0 + 16 * kk);
+      df[rb][kk] = *reinterpret_cast<const bf16x8*>(p.d_o + a0 + 16 * kk);
     }
+    lse2[rb] = p.lse2[(long long)bh * T + qc];
+    dlt[rb] = p.delta[(long long)bh * T + qc];
+    e1[rb] = min(T, (qc / L + 1) * L);
   }
-  const float lse2 = p.lse2[(long long)bh * T + min(qrow, T - 1)];
-  const float dlt = p.delta[(long long)bh * T + min(qrow, T - 1)];
-  const int e1 = min(T, (min(qrow, T - 1) / L + 1) * L);
   const int e1f = min(T, (q0 / L + 1) * L);
   const int kend = min(T, ((min(q0 + BM, T) - 1) / L + 1) * L);
   const float c = p.scale_log2;
 
-  f32x16 dq[DB];
+  f32x16 dq[RB][DB];
 #pragma unroll
-  for (int db = 0; db < DB; ++db) dq[db] = zero16();
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) dq[rb][db] = zero16();
 
   auto stage = [&](int k0, int b) {
     stage_rows_direct<D, BN, NT>(Ks[b], [&](int r) { return p.k + off + (long long)min(k0 + r, T - 1) * D; }, tid);
@@ -241,26 +249,45 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
     const bf16_t* Vt = Vs[buf];
 #pragma unroll
     for (int kb = 0; kb < BN / 32; ++kb) {
-      f32x16 s = zero16(), dp = zero16();
+      f32x16 s[RB], dp[RB];
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        s = mfma32(lds_row8<D>(Kt, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), qf[kk], s);
-        dp = mfma32(lds_row8<D>(Vt, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), df[kk], dp);
+      for (int rb = 0; rb < RB; ++rb) {
+        s[rb] = zero16();
+        dp[rb] = zero16();
       }
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float pv = fast_exp2(fmaf(s[i], c, -lse2));
-        if constexpr (decltype(masked)::value) {
-          const int key = k0 + kb * 32 + acc_row(i, lane);
-          pv = key < e1 ? pv : 0.f;
+      for (int kk = 0; kk < KK; ++kk) {
+        const bf16x8 kfrag = lds_row8<D>(Kt, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5));
+        const bf16x8 vfrag = lds_row8<D>(Vt, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5));
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          s[rb] = mfma32(kfrag, qf[rb][kk], s[rb]);
+          dp[rb] = mfma32(vfrag, df[rb][kk], dp[rb]);
         }
-        dp[i] = pv * (dp[i] - dlt);
+      }
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          float pv = fast_exp2(fmaf(s[rb][i], c, -lse2[rb]));
+          if constexpr (decltype(masked)::value) {
+            const int key = k0 + kb * 32 + acc_row(i, lane);
+            pv = key < e1[rb] ? pv : 0.f;
+          }
+          dp[rb][i] = pv * (dp[rb][i] - dlt[rb]);
+        }
       }
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        const bf16x8 dsb = pack8(dp, t);
+        bf16x8 dsb[RB];
 #pragma unroll
-        for (int db = 0; db < DB; ++db) dq[db] = mfma32(lds_tr8<D>(Kt, kb * 32, t, db * 32, lane), dsb, dq[db]);
+        for (int rb = 0; rb < RB; ++rb) dsb[rb] = pack8(dp[rb], t);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const bf16x8 ktr = lds_tr8<D>(Kt, kb * 32, t, db * 32, lane);
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) dq[rb][db] = mfma32(ktr, dsb[rb], dq[rb][db]);
+        }
       }
     }
   };
@@ -284,15 +311,17 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
   run(std::false_type{}, min(kfull, kend));
   run(std::true_type{}, kend);
 
-  if (qrow < T) {
-    bf16_t* row = p.dq + off + (long long)qrow * D;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    if (qrow[rb] >= T) continue;
+    bf16_t* row = p.dq + off + (long long)qrow[rb] * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         bf16x4 w;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) w[j] = to_bf16(dq[db][4 * g + j] * p.scale);
+        for (int j = 0; j < 4; ++j) w[j] = to_bf16(dq[rb][db][4 * g + j] * p.scale);
         *reinterpret_cast<bf16x4*>(row + db * 32 + 8 * g + 4 * (lane >> 5)) = w;
       }
     }
@@ -305,11 +334,14 @@ template <int D>
 struct BwdCfg {
   static constexpr int NW_DKV = 4;
   static constexpr int NW_DQ = 4;
+  // 32-row query blocks per wave in the dQ kernel; at D = 128 two blocks do
+  // not fit the register file without spilling
+  static constexpr int RB_DQ = D == 64 ? 2 : 1;
 };
 
 template <int D>
 static hipError_t launch_bwd_d(const BwdParams& p, hipStream_t stream) {
-  constexpr int NK = BwdCfg<D>::NW_DKV, NQ = BwdCfg<D>::NW_DQ;
+  constexpr int NK = BwdCfg<D>::NW_DKV, NQ = BwdCfg<D>::NW_DQ, RQ = BwdCfg<D>::RB_DQ;
   const long long rows = (long long)p.BH * p.T;
   const long long threads = rows * (D / 8);
   hipLaunchKernelGGL(bwd_rowterms_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p.o,
@@ -320,8 +352,8 @@ static hipError_t launch_bwd_d(const BwdParams& p, hipStream_t stream) {
   hipLaunchKernelGGL((bwd_dkdv_kernel<D, NK>), dim3(nkt * p.BH), dim3(64 * NK), 0, stream, p, nkt);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int nqt = (p.T + 32 * NQ - 1) / (32 * NQ);
-  hipLaunchKernelGGL((bwd_dq_kernel<D, NQ>), dim3(nqt * p.BH), dim3(64 * NQ), 0, stream, p, nqt);
+  const int nqt = (p.T + 32 * RQ * NQ - 1) / (32 * RQ * NQ);
+  hipLaunchKernelGGL((bwd_dq_kernel<D, NQ, RQ>), dim3(nqt * p.BH), dim3(64 * NQ), 0, stream, p, nqt);
   return hipGetLastError();
 }
 

@@ -39,29 +39,65 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
 
 // Staging of one K/V tile straight into LDS.  Key rows past the end of the
 // (virtual) key sequence read the last key instead; the mask hides them.
+// Cached attention: the key sequence is the sink, then the window chunks in
+// ring slots, then the queued chunks.  A tile that lies inside one window
+// chunk or inside the queued keys (almost every tile) is classified once with
+// wave-uniform scalar tests and staged from one base pointer; only tiles that
+// straddle a boundary take the per-row mapping, which finds the window chunk
+// of the tile's first key once and moves a row on by whole chunks from there.
 template <int D, bool CACHED, int BN, int NT>
 __device__ __forceinline__ void stage_kv(const FwdParams& p, int bh, long long kvoff, int k0, bf16_t* Kt,
                                          bf16_t* Vt, int tid) {
-  auto src = [&](const uint16_t* sink_base, const uint16_t* win_base, const uint16_t* base, int r) -> const bf16_t* {
-    const int key = min(k0 + r, p.Tk - 1);
-    if constexpr (CACHED) {
-      if (key < p.sink_len) return sink_base + ((long long)bh * p.sink_len + key) * D;
+  if constexpr (CACHED) {
+    const int kl = min(k0 + BN, p.Tk) - 1;  // last real key of the tile
+    const int kw0 = k0 - p.sink_len;
+    const int w0 = kw0 > 0 ? kw0 / p.L : 0;
+    const int off0 = kw0 - w0 * p.L;
+    if (k0 >= p.wL) {  // queued keys only
+      const long long e = kvoff + (long long)(k0 - p.wL) * D;
+      const int last = p.Tk - 1 - k0;
+      stage_kv_rows_direct<D, BN, NT>(Kt, Vt, [&](int r) -> RowPair {
+        const long long er = e + (long long)min(r, last) * D;
+        return {p.k + er, p.v + er};
+      }, tid);
+      return;
+    }
+    if (kw0 >= 0 && kl < p.wL && off0 + (kl - k0) < p.L) {  // one window chunk
+      int slot = p.first_slot + w0;
+      slot = slot >= p.S ? slot - p.S : slot;
+      const long long e = (long long)slot * p.slot_stride + ((long long)bh * p.L + off0) * D;
+      stage_kv_rows_direct<D, BN, NT>(Kt, Vt, [&](int r) -> RowPair {
+        const long long er = e + (long long)r * D;
+        return {p.k_slots + er, p.v_slots + er};
+      }, tid);
+      return;
+    }
+    stage_kv_rows_direct<D, BN, NT>(Kt, Vt, [&](int r) -> RowPair {
+      const int key = min(k0 + r, p.Tk - 1);
+      if (key < p.sink_len) {
+        const long long e = ((long long)bh * p.sink_len + key) * D;
+        return {p.k_sink + e, p.v_sink + e};
+      }
       if (key < p.wL) {
-        const int kw = key - p.sink_len;
-        const int w = kw / p.L, off = kw - w * p.L;
+        int w = w0, off = key - p.sink_len - w0 * p.L;
+        while (off >= p.L) {  // at most one step when L >= BN
+          off -= p.L;
+          ++w;
+        }
         int slot = p.first_slot + w;
         slot = slot >= p.S ? slot - p.S : slot;
-        return win_base + (long long)slot * p.slot_stride + (long long)bh * p.L * D + (long long)off * D;
+        const long long e = (long long)slot * p.slot_stride + ((long long)bh * p.L + off) * D;
+        return {p.k_slots + e, p.v_slots + e};
       }
-      return base + kvoff + (long long)(key - p.wL) * D;
-    } else {
-      (void)win_base;
-      (void)sink_base;
-      return base + kvoff + (long long)key * D;
-    }
-  };
-  stage_rows_direct<D, BN, NT>(Kt, [&](int r) { return src(p.k_sink, p.k_slots, p.k, r); }, tid);
-  stage_rows_direct<D, BN, NT>(Vt, [&](int r) { return src(p.v_sink, p.v_slots, p.v, r); }, tid);
+      const long long e = kvoff + (long long)(key - p.wL) * D;
+      return {p.k + e, p.v + e};
+    }, tid);
+  } else {
+    stage_kv_rows_direct<D, BN, NT>(Kt, Vt, [&](int r) -> RowPair {
+      const long long e = kvoff + (long long)min(k0 + r, p.Tk - 1) * D;
+      return {p.k + e, p.v + e};
+    }, tid);
+  }
 }
 
 // Rows of the running max only move when a tile raises it by more than this

@@ -160,6 +160,30 @@ __device__ __forceinline__ void stage_rows_direct(bf16_t* lds_tile, RowPtr row_p
   }
 }
 
+// Same staging for a K tile and a V tile whose rows come from the same
+// positions: row_src(row) returns the pair of row pointers, so the address
+// arithmetic of a row is done once for both tiles.
+struct RowPair {
+  const bf16_t* k;
+  const bf16_t* v;
+};
+template <int D, int ROWS, int NT, typename RowSrc>
+__device__ __forceinline__ void stage_kv_rows_direct(bf16_t* k_tile, bf16_t* v_tile, RowSrc row_src, int tid) {
+  constexpr int SLOTS = D / 8;
+  constexpr int ROUNDS = ROWS * SLOTS / NT;
+  static_assert(ROWS * SLOTS % NT == 0, "tile must be a whole number of NT-chunk rounds");
+#pragma unroll
+  for (int it = 0; it < ROUNDS; ++it) {
+    const int ci = it * NT + tid;
+    const int row = ci / SLOTS, ps = ci % SLOTS;
+    const int ls = ps ^ Tile<D>::swz(row);
+    const RowPair src = row_src(row);
+    const int dst = (it * NT + (tid & ~63)) * 8;  // wave-uniform base
+    dma_lds_16(src.k + ls * 8, (MW_LDS void*)(k_tile + dst));
+    dma_lds_16(src.v + ls * 8, (MW_LDS void*)(v_tile + dst));
+  }
+}
+
 // 64 consecutive fp32 values (rows r0..r0+63, clamped to n-1) into LDS by one wave.
 __device__ __forceinline__ void stage_f32x64_direct(float* lds, const float* g, int r0, int n, int lane) {
   const float* src = g + min(r0 + lane, n - 1);
