@@ -269,7 +269,7 @@ def main():
     n_splits = max(1, ws_c.numel() // (st.B * st.H * st.n_queued * st.q_len * (st.D + 2) * 4))
     digest = source_digest(["paper_2608_01127_amd/csrc/attn_fwd.hip", "paper_2608_01127_amd/csrc/mw_device.h"])
     traffic = read_traffic("attn_fwd_cached", digest)
-    kname = "attn_fwd_kernel<128, true, 8, 64, 1>"
+    kname = "attn_fwd_kernel<128, true, 8, 64, 1, 1>"
     if n_splits > 1:
         kname += f" over {n_splits} key ranges + attn_combine_kernel<128>"
     roofline = {"kernel": kname + " (cached chunk attention call)", "bound": "mfma",

@@ -112,13 +112,21 @@ constexpr float kRescaleThreshold = 8.f;
 // MFMAs (one per row block), halving LDS traffic per MFMA: with one 32-row
 // block per wave the LDS bandwidth (128 B/clk/CU) equals what four waves
 // consume at the full MFMA rate.
-template <int D, bool CACHED, int NW, int BN, int RB>
-__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) {
-  constexpr int BM = 32 * RB * NW, NT = 64 * NW, KB = BN / 32;
+// KG key groups: the NW waves form KG groups of NW / KG waves; a step stages
+// KG * BN keys and group g works on its BN-key slice, so KG groups cover
+// different keys of the same query rows and merge (m, l, O) through LDS at
+// the end.  With few query rows this keeps all four SIMDs of a CU busy.
+template <int D, bool CACHED, int NW, int BN, int RB, int KG>
+__global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd_kernel(FwdParams p) {
+  static_assert(NW % KG == 0, "waves split evenly into key groups");
+  constexpr int NWR = NW / KG;           // waves per key group (row waves)
+  constexpr int BM = 32 * RB * NWR, NT = 64 * NW, KB = BN / 32;
+  constexpr int BK = BN * KG;            // keys staged per step
   constexpr int KK = D / 16;  // contraction steps over D
   constexpr int DB = D / 32;  // 32-wide column blocks of D
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BN * D];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][BN * D];
+  __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][BK * D];  // K, V x double buffer
+  bf16_t(*Ks)[BK * D] = lds[0];
+  bf16_t(*Vs)[BK * D] = lds[1];
 
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
   const int NS = p.n_splits;
@@ -126,6 +134,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
   const int bh = (logical / NS) / p.n_qtiles;
   const int qt = p.n_qtiles - 1 - (logical / NS) % p.n_qtiles;  // heaviest (last) query tile first
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int rw = wave % NWR, kg = wave / NWR;  // row wave, key group
   const int q0 = qt * BM;
   const long long qoff = (long long)bh * p.Tq * D;
 
@@ -137,7 +146,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
   bf16x8 qf[RB][KK];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    qrow[rb] = q0 + (wave * RB + rb) * 32 + (lane & 31);
+    qrow[rb] = q0 + (rw * RB + rb) * 32 + (lane & 31);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       if (qrow[rb] < p.Tq) {
@@ -154,13 +163,13 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
   vis.range(min(q0 + BM, p.Tq) - 1, e1l, s2l, e2l);
   const int kend_all = max(e1l, e2l);
   // this workgroup's share of the key tiles [0, kend_all): split `split` of NS
-  const int ntiles = (kend_all + BN - 1) / BN;
-  const int kbeg = (int)((long long)ntiles * split / NS) * BN;
-  const int kend = min(kend_all, (int)((long long)ntiles * (split + 1) / NS) * BN);
+  const int ntiles = (kend_all + BK - 1) / BK;
+  const int kbeg = (int)((long long)ntiles * split / NS) * BK;
+  const int kend = min(kend_all, (int)((long long)ntiles * (split + 1) / NS) * BK);
   // next visited key tile after k: tiles no row of this workgroup can see are skipped
   auto advance = [&](int k) {
-    int n = k + BN;
-    if (n >= e1l && n + BN <= s2f) n = (s2f / BN) * BN;
+    int n = k + BK;
+    if (n >= e1l && n + BK <= s2f) n = (s2f / BK) * BK;
     return n;
   };
 
@@ -181,7 +190,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
   // any mask code; the remaining tiles (chunk edges, the ragged end, the gap of
   // the isolated rule) run the masked instantiation.  Separate loops keep the
   // fast loop free of the mask and of register copies between the two bodies.
-  const int kfull = max(0, (e1f / BN) * BN);
+  const int kfull = max(0, (e1f / BK) * BK);
 
   auto step = [&](auto masked, const int k0, const bf16_t* Kt, const bf16_t* Vt) {
     // S^T for KB 32-key blocks x RB row blocks; each K fragment is read once
@@ -281,26 +290,93 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
     }
   };
 
-  int k0 = advance(kbeg - BN);
-  int buf = 0;
-  if (k0 < kend) stage_kv<D, CACHED, BN, NT>(p, bh, kvoff, k0, Ks[0], Vs[0], tid);
-  wait_vmem();
-  __syncthreads();
-
-  auto run = [&](auto masked, const int kstop) {
-    while (k0 < kstop) {
-      const int kn = advance(k0);
-      // next tile streams into the other buffer during this step's math
-      if (kn < kend) stage_kv<D, CACHED, BN, NT>(p, bh, kvoff, kn, Ks[buf ^ 1], Vs[buf ^ 1], tid);
-      step(masked, k0, Ks[buf], Vs[buf]);
-      wait_vmem();
-      __syncthreads();
-      buf ^= 1;
-      k0 = kn;
-    }
+  // this wave's slice of a staged step: keys [kg * BN, (kg + 1) * BN)
+  auto slice = [&](auto masked, const int k0, const int st) {
+    step(masked, k0 + kg * BN, Ks[st] + kg * BN * D, Vs[st] + kg * BN * D);
   };
-  run(std::false_type{}, min(kfull, kend));
-  run(std::true_type{}, kend);
+  int kc = advance(kbeg - BK);  // next tile to use
+  {
+    // double buffering: the next tile streams in during this step's math
+    int buf = 0;
+    if (kc < kend) stage_kv<D, CACHED, BK, NT>(p, bh, kvoff, kc, Ks[0], Vs[0], tid);
+    wait_vmem();
+    __syncthreads();
+    auto run = [&](auto masked, const int kstop) {
+      while (kc < kstop) {
+        const int kn = advance(kc);
+        if (kn < kend) stage_kv<D, CACHED, BK, NT>(p, bh, kvoff, kn, Ks[buf ^ 1], Vs[buf ^ 1], tid);
+        slice(masked, kc, buf);
+        wait_vmem();
+        __syncthreads();
+        buf ^= 1;
+        kc = kn;
+      }
+    };
+    run(std::false_type{}, min(kfull, kend));
+    run(std::true_type{}, kend);
+  }
+
+  if constexpr (KG > 1) {
+    // Merge the key groups' partial results into group 0 through LDS (the K/V
+    // stages are free once every wave has passed this barrier):
+    // M = max_g m_g, w_g = 2^(m_g - M), O = sum_g w_g O_g, l = sum_g w_g l_g.
+    constexpr int XO = (KG - 1) * NWR * RB * DB * 16 * 64;  // floats of O
+    constexpr int XM = (KG - 1) * NWR * RB * 2 * 64;        // floats of (m, l)
+    static_assert((XO + XM) * 4 <= (int)sizeof(lds), "exchange fits the K/V stages");
+    float* xo = reinterpret_cast<float*>(&lds[0][0][0]);
+    float* xm = xo + XO;
+    __syncthreads();
+    if (kg > 0) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int slot = ((kg - 1) * NWR + rw) * RB + rb;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i) xo[((slot * DB + db) * 16 + i) * 64 + lane] = o[rb][db][i];
+        }
+        xm[(slot * 2) * 64 + lane] = m[rb];
+        xm[(slot * 2 + 1) * 64 + lane] = lsum[rb];
+      }
+    }
+    __syncthreads();
+    if (kg > 0) return;  // no barrier follows
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      float mg[KG], wg[KG];
+      mg[0] = m[rb];
+      float M = m[rb];
+#pragma unroll
+      for (int g = 1; g < KG; ++g) {
+        const int slot = ((g - 1) * NWR + rw) * RB + rb;
+        mg[g] = xm[(slot * 2) * 64 + lane];
+        M = fmaxf(M, mg[g]);
+      }
+#pragma unroll
+      for (int g = 0; g < KG; ++g) wg[g] = (mg[g] == -INFINITY) ? 0.f : fast_exp2(mg[g] - M);
+      float l = wg[0] * lsum[rb];
+#pragma unroll
+      for (int g = 1; g < KG; ++g) {
+        const int slot = ((g - 1) * NWR + rw) * RB + rb;
+        l += wg[g] * xm[(slot * 2 + 1) * 64 + lane];
+      }
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          float acc = wg[0] * o[rb][db][i];
+#pragma unroll
+          for (int g = 1; g < KG; ++g) {
+            const int slot = ((g - 1) * NWR + rw) * RB + rb;
+            acc += wg[g] * xo[((slot * DB + db) * 16 + i) * 64 + lane];
+          }
+          o[rb][db][i] = acc;
+        }
+      }
+      m[rb] = M;
+      lsum[rb] = l;
+    }
+  }
 
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
@@ -348,14 +424,28 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_kernel(FwdParams p) 
 }
 
 // Tile configuration per head dimension: waves per workgroup (32 query rows
-// each) and keys per step.  With D = 128 a workgroup of 8 waves shares each
-// staged K/V tile among 256 queries, halving L2 -> LDS traffic per MFMA; with
-// D = 64 four waves and a third workgroup per CU measured faster.
+// each), keys per step, row blocks per wave and LDS stages.  With D = 128 a
+// workgroup of 8 waves shares each staged K/V tile among 256 queries, halving
+// L2 -> LDS traffic per MFMA; with D = 64 four waves of two row blocks and a
+// third workgroup per CU measured faster.
 template <int D>
 struct FwdCfg {
   static constexpr int NW = D == 64 ? 4 : 8;
   static constexpr int BN = 64;
   static constexpr int RB = D == 64 ? 2 : 1;  // 32-row query blocks per wave
+  static constexpr int KG = 1;
+};
+
+// Cached attention with few queued rows (a short chunk over a long window) is
+// bound by streaming the window from HBM.  Eight waves split into key groups
+// (4 groups of 2 row waves for 64 rows, 2 groups of 4 for 128 rows) stage 128
+// keys per step, so every SIMD of the CU has two waves at work on the rows.
+template <int D, int NWR>
+struct FwdDecodeCfg {
+  static constexpr int NW = 8;
+  static constexpr int KG = NW / NWR;
+  static constexpr int BN = 128 / KG;
+  static constexpr int RB = 1;
 };
 
 // Merge of the per-split partials: with M = max_s m_s and w_s = 2^(m_s - M),
@@ -370,18 +460,36 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   if (row >= rows) return;
   const int c = (int)(gid % TPR) * 4;
   const float* ml = part + (long long)NS * rows * D;
+  // splits are read in groups of G so that G loads are in flight at once
+  constexpr int G = 8;
   float M = -INFINITY;
-  for (int s = 0; s < NS; ++s) M = fmaxf(M, ml[2 * ((long long)s * rows + row)]);
+  for (int s0 = 0; s0 < NS; s0 += G) {
+    float mv[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) mv[g] = s0 + g < NS ? ml[2 * ((long long)(s0 + g) * rows + row)] : -INFINITY;
+#pragma unroll
+    for (int g = 0; g < G; ++g) M = fmaxf(M, mv[g]);
+  }
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   float L = 0.f;
-  for (int s = 0; s < NS; ++s) {
-    const long long r = (long long)s * rows + row;
-    const float ms = ml[2 * r], ls = ml[2 * r + 1];
-    const float w = (ms == -INFINITY) ? 0.f : fast_exp2(ms - M);  // empty split: no keys
-    L = fmaf(w, ls, L);
-    const f32x4 v = *reinterpret_cast<const f32x4*>(part + r * D + c);
+  for (int s0 = 0; s0 < NS; s0 += G) {
+    float mv[G], lv[G];
+    f32x4 v[G];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[j] = fmaf(w, v[j], acc[j]);
+    for (int g = 0; g < G; ++g) {
+      const long long r = (long long)(s0 + g) * rows + row;
+      const bool in = s0 + g < NS;
+      mv[g] = in ? ml[2 * r] : -INFINITY;
+      lv[g] = in ? ml[2 * r + 1] : 0.f;
+      v[g] = in ? *reinterpret_cast<const f32x4*>(part + r * D + c) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float w = (mv[g] == -INFINITY) ? 0.f : fast_exp2(mv[g] - M);  // empty split: no keys
+      L = fmaf(w, lv[g], L);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[j] = fmaf(w, v[g][j], acc[j]);
+    }
   }
   const float inv = 1.f / L;
   bf16x4 out;
@@ -391,13 +499,13 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   if (lse != nullptr && c == 0) lse[row] = (M + __log2f(L)) * 0.69314718055994530942f;
 }
 
-template <int D, bool CACHED>
-static hipError_t launch_fwd_cfg(FwdParams p, hipStream_t stream) {
-  constexpr int NW = FwdCfg<D>::NW, BN = FwdCfg<D>::BN, RB = FwdCfg<D>::RB;
-  p.n_qtiles = (p.Tq + 32 * RB * NW - 1) / (32 * RB * NW);
+template <int D, bool CACHED, int NW, int BN, int RB, int KG>
+static hipError_t launch_fwd_tpl(FwdParams p, hipStream_t stream) {
+  constexpr int BM = 32 * RB * (NW / KG);
+  p.n_qtiles = (p.Tq + BM - 1) / BM;
   if (p.n_splits < 1) p.n_splits = 1;
-  hipLaunchKernelGGL((attn_fwd_kernel<D, CACHED, NW, BN, RB>), dim3(p.n_qtiles * p.BH * p.n_splits), dim3(64 * NW),
-                     0, stream, p);
+  hipLaunchKernelGGL((attn_fwd_kernel<D, CACHED, NW, BN, RB, KG>), dim3(p.n_qtiles * p.BH * p.n_splits),
+                     dim3(64 * NW), 0, stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_splits == 1) return e;
   const long long rows = (long long)p.BH * p.Tq;
@@ -407,22 +515,50 @@ static hipError_t launch_fwd_cfg(FwdParams p, hipStream_t stream) {
   return hipGetLastError();
 }
 
+template <int D, bool CACHED>
+static hipError_t launch_fwd_cfg(const FwdParams& p, hipStream_t stream) {
+  using C = FwdCfg<D>;
+  return launch_fwd_tpl<D, CACHED, C::NW, C::BN, C::RB, C::KG>(p, stream);
+}
+
 // This file is compiled once per head dimension (MW_FWD_HEAD_DIM = 64 or 128),
 // with the instruction-scheduling option measured faster for each; the merge
-// kernel and the split heuristic live in the D = 128 unit.
-#if MW_FWD_HEAD_DIM == 64
+// kernel and the split heuristic live in the D = 128 unit.  The key-group
+// configurations for few queued rows are compiled in a unit of their own
+// (MW_FWD_DECODE) with the default scheduler.
+#if MW_FWD_HEAD_DIM == 64 && !defined(MW_FWD_DECODE)
 hipError_t launch_fwd_64(const FwdParams& p, bool cached, hipStream_t stream) {
   return cached ? launch_fwd_cfg<64, true>(p, stream) : launch_fwd_cfg<64, false>(p, stream);
 }
-#elif MW_FWD_HEAD_DIM == 128
+#elif MW_FWD_HEAD_DIM == 128 && !defined(MW_FWD_DECODE)
 hipError_t launch_fwd_128(const FwdParams& p, bool cached, hipStream_t stream) {
-  return cached ? launch_fwd_cfg<128, true>(p, stream) : launch_fwd_cfg<128, false>(p, stream);
+  if (!cached) return launch_fwd_cfg<128, false>(p, stream);
+  const int bm = fwd_choice(128, true, p.Tq).bm;
+  if (bm != 32 * FwdCfg<128>::RB * FwdCfg<128>::NW) return launch_fwd_decode_128(p, bm, stream);
+  return launch_fwd_cfg<128, true>(p, stream);
+}
+#elif MW_FWD_HEAD_DIM == 128 && defined(MW_FWD_DECODE)
+hipError_t launch_fwd_decode_128(const FwdParams& p, int bm, hipStream_t stream) {
+  if (bm == 64) {
+    using C = FwdDecodeCfg<128, 2>;
+    return launch_fwd_tpl<128, true, C::NW, C::BN, C::RB, C::KG>(p, stream);
+  }
+  using C = FwdDecodeCfg<128, 4>;
+  return launch_fwd_tpl<128, true, C::NW, C::BN, C::RB, C::KG>(p, stream);
 }
 #else
-#error "compile with -DMW_FWD_HEAD_DIM=64 or -DMW_FWD_HEAD_DIM=128"
+#error "compile with -DMW_FWD_HEAD_DIM=64 or -DMW_FWD_HEAD_DIM=128 (optionally -DMW_FWD_DECODE)"
 #endif
 
-#if MW_FWD_HEAD_DIM == 128
+#if MW_FWD_HEAD_DIM == 128 && !defined(MW_FWD_DECODE)
+// Must agree with the dispatch in launch_fwd_128.
+FwdChoice fwd_choice(int D, bool cached, int Tq) {
+  if (cached && D == 128 && Tq <= 64) return {64, 1};
+  if (cached && D == 128 && Tq <= 128) return {128, 1};
+  if (D == 64) return {32 * FwdCfg<64>::RB * FwdCfg<64>::NW, 3};
+  return {32 * FwdCfg<128>::RB * FwdCfg<128>::NW, 2};
+}
+
 size_t fwd_split_bytes(int D, int BH, int Tq, int n_splits) {
   if (n_splits <= 1) return 0;
   return (size_t)n_splits * BH * Tq * (D + 2) * sizeof(float);
@@ -435,12 +571,10 @@ size_t fwd_split_bytes(int D, int BH, int Tq, int n_splits) {
 // back.  The count with the lowest estimate wins (each split keeps at least
 // two key tiles; at most 64 splits; bounded by the workspace).
 int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes) {
-  const int NW = D == 64 ? FwdCfg<64>::NW : FwdCfg<128>::NW;
-  const int BN = D == 64 ? FwdCfg<64>::BN : FwdCfg<128>::BN;
-  const int RB = D == 64 ? FwdCfg<64>::RB : FwdCfg<128>::RB;
-  const int wg_per_cu = D == 64 ? 3 : 2;  // resident workgroups per CU (registers / LDS)
-  const double slots = 256.0 * wg_per_cu;
-  const double base = (double)((Tq + 32 * RB * NW - 1) / (32 * RB * NW)) * BH;
+  const FwdChoice ch = fwd_choice(D, true, Tq);
+  const int BN = 128;  // keys staged per step (at most)
+  const double slots = 256.0 * ch.wg_per_cu;  // resident workgroups (registers / LDS)
+  const double base = (double)((Tq + ch.bm - 1) / ch.bm) * BH;
   const double pairs = (double)BH * Tq * std::max(1.0, (double)Tk - 0.5 * Tq);
   const double t_work = std::max(4.0 * pairs * D / 0.8e15, 2.0 * BH * (double)Tk * D * 2 / 4.0e12);
   const int ns_max = (int)std::min<long long>(64, std::max(1, (Tk / BN) / 2));

@@ -195,6 +195,7 @@ __device__ __forceinline__ void stage_f32x64_direct(float* lds, const float* g, 
 // counter at zero.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0); }
 
+
 // Row (within a 32-row accumulator block) of accumulator register i in lane l.
 __device__ __forceinline__ int acc_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
 

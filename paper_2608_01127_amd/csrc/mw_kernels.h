@@ -64,9 +64,18 @@ constexpr int DQ_BN = 64;     // keys per step in the dQ kernel
 
 hipError_t launch_fwd_64(const FwdParams& p, bool cached, hipStream_t stream);
 hipError_t launch_fwd_128(const FwdParams& p, bool cached, hipStream_t stream);
+// cached attention at D = 128 with `bm` (64 or 128) query rows per workgroup
+hipError_t launch_fwd_decode_128(const FwdParams& p, int bm, hipStream_t stream);
 inline hipError_t launch_fwd(const FwdParams& p, int D, bool cached, hipStream_t stream) {
   return D == 64 ? launch_fwd_64(p, cached, stream) : launch_fwd_128(p, cached, stream);
 }
+// Query rows per workgroup and resident workgroups per CU of the tile
+// configuration the forward launcher picks for a shape.
+struct FwdChoice {
+  int bm;
+  int wg_per_cu;
+};
+FwdChoice fwd_choice(int D, bool cached, int Tq);
 // Split count the cached launcher uses for this shape given `ws_bytes` of
 // workspace (1 = no split), and the workspace bytes a split count needs.
 int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes);

@@ -164,7 +164,7 @@ def test_ring_errors_and_slots(mw):
     assert cache.slot_of(0) == -1
 
 
-@pytest.mark.parametrize("q_len", [64, 256])
+@pytest.mark.parametrize("q_len", [64, 128, 256])
 def test_decode_shape_split_vs_oracle(mw, q_len):
     """One short queued chunk over a full 6-chunk window (B1 H16 D128, 2640-token chunks):
     few query tiles, so the key range is split over many workgroups."""
@@ -186,6 +186,48 @@ def test_decode_shape_split_vs_oracle(mw, q_len):
     assert_close("o split", to_f64(o), ro)
     assert_close("lse split", to_f64(lse), rl, max_abs=2e-3, mean_abs=2e-4)
     assert_close("o single pass", to_f64(o1), ro)
+
+
+@pytest.mark.parametrize("split", [True, False])
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("B,H,L,S,n_commit,window,nq,qlen,sink_len", [
+    (1, 2, 250, 4, 5, 3, 1, 64, 0),     # 64 rows: four key groups of two row waves
+    (1, 3, 300, 4, 6, 3, 2, 50, 0),     # 100 rows in two queued chunks: two key groups of four
+    (2, 1, 200, 5, 5, 4, 3, 40, 17),    # 120 rows, three queued chunks, sink of 17 tokens
+    (1, 1, 96, 3, 4, 2, 1, 7, 0),       # 7 rows, window shorter than one 128-key step
+    (1, 2, 130, 4, 6, -1, 2, 33, 5),    # all live chunks, ragged 66 rows, sink
+])
+def test_few_rows_key_groups_vs_oracle(mw, split, mode, B, H, L, S, n_commit, window, nq, qlen, sink_len):
+    """Cached attention with at most 128 queued rows (D=128), the configuration whose waves
+    split the keys of each step into groups and merge at the end; both visibility modes, with
+    and without the key-range split, sinks and ragged row counts."""
+    D = 128
+    print(f"[case] few rows split={split} mode={mode} B={B} H={H} L={L} S={S} commits={n_commit} w={window} "
+          f"nq={nq} qlen={qlen} sink={sink_len}", flush=True)
+    cache = mw.KVCache(S, B, H, L, D)
+    chunks = make_chunks(n_commit, B, H, L, D, seed=3100 + L)
+    ring = oracle.RingModel(S)
+    for kc, vc in chunks:
+        if ring.live == S:
+            ring.evict(1)
+            mw.mw_kvcache_evict(cache, 1)
+        assert mw.mw_kvcache_append(cache, to_gpu(kc), to_gpu(vc)) == ring.append()
+    sk = sv = None
+    if sink_len:
+        sk, sv = (synth.normal_bf16((B, H, sink_len, D), 3200 + i) for i in range(2))
+        gsk, gsv = to_gpu(sk), to_gpu(sv)
+        cache.set_sink(gsk, gsv)
+    win = ring.window(None if window == -1 else window)
+    inp = queued(B, H, nq, qlen, D, seed=3300 + qlen)
+    o, lse = mw.mw_chunk_attn_cached(to_gpu(inp["q"]), to_gpu(inp["k_new"]), to_gpu(inp["v_new"]), nq, qlen, cache,
+                                     window=window, flags=mode, want_lse=True, split=split)
+    sync()
+    ro, rl = oracle.cached_chunk_attn(f64(inp["q"]), f64(inp["k_new"]), f64(inp["v_new"]),
+                                      [f64(chunks[c][0]) for c in win], [f64(chunks[c][1]) for c in win],
+                                      nq, qlen, mode=mode,
+                                      sink_k=None if sk is None else f64(sk), sink_v=None if sv is None else f64(sv))
+    assert_close("o", to_f64(o), ro)
+    assert_close("lse", to_f64(lse), rl, max_abs=2e-3, mean_abs=2e-4)
 
 
 @pytest.fixture(scope="module")
