@@ -124,11 +124,12 @@ def cpu_baseline(target_s: float):
 def decode_shapes(mw, torch, cache, st, dev, reps=20):
     """Cache-bound shapes: one queued chunk of q_len tokens over the full window
     (6 committed chunks of 2640 tokens, B1 H16 D128).  Each timed call is
-    preceded by a 512 MB write that evicts the 256 MB Infinity Cache, so the
-    window's K/V come from HBM.  Algorithmic bytes = window K and V + Q, K_new,
-    V_new and O of the queued chunk."""
+    preceded by a 512 MB read (a sum) that evicts the 256 MB Infinity Cache, so
+    the window's K/V come from HBM; a read leaves no dirty lines whose
+    write-back would compete with the timed call.  Algorithmic bytes = window K
+    and V + Q, K_new, V_new and O of the queued chunk."""
     out = []
-    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    flush = torch.ones(128 << 20, dtype=torch.float32, device=dev)
     g = torch.Generator(device=dev).manual_seed(1234)
     for ql in (64, 128, 256):
         q, kn, vn = (torch.randn(st.B, st.H, ql, st.D, device=dev, generator=g).to(torch.bfloat16) for _ in range(3))
@@ -140,7 +141,7 @@ def decode_shapes(mw, torch, cache, st, dev, reps=20):
             run()
         tot = 0.0
         for _ in range(reps):
-            flush.fill_(1)
+            flush.sum()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
             run()

@@ -12,7 +12,9 @@
  *     "Structured Rolling KV Cache", "Pipelined Denoising").
  *
  * Conventions (every entry point):
- *   - Tensors are device pointers to contiguous row-major arrays.  bf16 means
+ *   - Tensors are device pointers to contiguous row-major arrays, except in
+ *     the *_strided entry points, which take [B, H, T, D] views described by
+ *     mw_strides (the head dimension D contiguous).  bf16 means
  *     IEEE bfloat16 stored as 16-bit words.  Every pointer must be 16-byte
  *     aligned.  The caller allocates and owns every buffer, including the
  *     backward workspace; the library never allocates or frees device memory.
@@ -53,6 +55,20 @@ const char* mw_last_error(void);
 /* Library version as major*10000 + minor*100 + patch. */
 int mw_version(void);
 
+/* Element strides of a bf16 [B, H, T, D] tensor view whose D elements are
+ * contiguous: element (b, h, t, d) is at base + b*b + h*h + t*t + d (in
+ * elements).  A contiguous [B, H, T, D] tensor has {H*T*D, T*D, D}; a
+ * [B, T, H, D] tensor (the layout of a QKV projection's output) seen as
+ * [B, H, T, D] has {T*H*D, D, H*D}; q, k, v inside one fused [B, T, 3, H, D]
+ * tensor have {3*T*H*D, D, 3*H*D}.  Requirements, checked before anything is
+ * enqueued: every stride a multiple of 8 (16-byte aligned rows; MW_EALIGN),
+ * b and h >= 0, t >= D (MW_EINVAL); a view that is written (an output) must
+ * not overlap itself (MW_EINVAL).  Inputs may overlap one another; outputs
+ * must not overlap inputs or other outputs (not checked). */
+typedef struct {
+  int64_t b, h, t;
+} mw_strides;
+
 /* Largest supported window (committed chunks attended to) and queued-chunk count. */
 #define MW_MAX_WINDOW 64
 #define MW_MAX_QUEUED 64
@@ -81,6 +97,15 @@ int mw_block_causal_attn_fwd(const void* q, const void* k, const void* v, void* 
                              int B, int H, int T, int D, int chunk_len, float scale,
                              mw_stream_t stream);
 
+/* The same on strided views, so that q, k, v can be read (and o written) in
+ * the layout the projections use, with no transposing copy.
+ * strides: 4 entries, for q, k, v, o in that order (NULL = all contiguous).
+ * lse stays contiguous fp32 [B, H, T].  Errors: as above, plus the stride
+ * checks of mw_strides. */
+int mw_block_causal_attn_fwd_strided(const void* q, const void* k, const void* v, void* o, float* lse,
+                                     const mw_strides* strides, int B, int H, int T, int D, int chunk_len,
+                                     float scale, mw_stream_t stream);
+
 /* Bytes of device workspace mw_block_causal_attn_bwd needs (fp32 row terms). */
 size_t mw_block_causal_attn_bwd_workspace_size(int B, int H, int T, int D);
 
@@ -104,6 +129,15 @@ int mw_block_causal_attn_bwd(const void* q, const void* k, const void* v, const 
                              void* workspace, size_t workspace_bytes,
                              int B, int H, int T, int D, int chunk_len, float scale,
                              mw_stream_t stream);
+
+/* The backward on strided views.  strides: 8 entries, for q, k, v, o, d_o, dq,
+ * dk, dv in that order (NULL = all contiguous); lse and the workspace stay
+ * contiguous.  Errors: as above, plus the stride checks of mw_strides. */
+int mw_block_causal_attn_bwd_strided(const void* q, const void* k, const void* v, const void* o,
+                                     const void* d_o, const float* lse, void* dq, void* dk, void* dv,
+                                     void* workspace, size_t workspace_bytes, const mw_strides* strides,
+                                     int B, int H, int T, int D, int chunk_len, float scale,
+                                     mw_stream_t stream);
 
 /* ------------------------------------------------------------------------
  * Rolling KV cache (Sec. 3.5, "Structured Rolling KV Cache").
@@ -167,6 +201,13 @@ int mw_kvcache_rope_shift(mw_kvcache* c, int shift, const mw_rope* rope, mw_stre
  * Errors: MW_EINVAL, MW_EALIGN, MW_EFULL (head - tail == S), MW_EHIP. */
 int mw_kvcache_append(mw_kvcache* c, const void* k_chunk, const void* v_chunk, mw_stream_t stream);
 
+/* Commit from strided [B, H, L, D] views (e.g. K and V straight out of a
+ * [B, L, H, D] projection); the slot itself is contiguous.  strides: 2
+ * entries, for k_chunk and v_chunk (NULL = contiguous).  Errors: as above,
+ * plus the stride checks of mw_strides. */
+int mw_kvcache_append_strided(mw_kvcache* c, const void* k_chunk, const void* v_chunk,
+                              const mw_strides* strides, mw_stream_t stream);
+
 /* Discard the n_chunks oldest live chunks (tail += n_chunks).  Host only.
  * Errors: MW_EINVAL (null, n_chunks < 0), MW_EEMPTY (n_chunks > head - tail). */
 int mw_kvcache_evict(mw_kvcache* c, int n_chunks);
@@ -218,6 +259,15 @@ int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new,
                          int n_queued, int q_len, const mw_kvcache* c, int window, int flags,
                          void* o, float* lse, float scale, void* workspace, size_t workspace_bytes,
                          mw_stream_t stream);
+
+/* Cached chunk attention on strided [B, H, n_queued*q_len, D] views of q,
+ * k_new, v_new and o.  strides: 4 entries in that order (NULL = contiguous);
+ * lse, the ring and the sink keep their layouts.  Errors: as above, plus the
+ * stride checks of mw_strides. */
+int mw_chunk_attn_cached_strided(const void* q, const void* k_new, const void* v_new,
+                                 int n_queued, int q_len, const mw_kvcache* c, int window, int flags,
+                                 void* o, float* lse, float scale, void* workspace, size_t workspace_bytes,
+                                 const mw_strides* strides, mw_stream_t stream);
 
 #ifdef __cplusplus
 }

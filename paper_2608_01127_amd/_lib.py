@@ -47,9 +47,14 @@ class mw_rope(ctypes.Structure):
     _fields_ = [("dim_offset", ctypes.c_int), ("dim_count", ctypes.c_int), ("theta", ctypes.c_float)]
 
 
+class mw_strides(ctypes.Structure):
+    _fields_ = [("b", ctypes.c_int64), ("h", ctypes.c_int64), ("t", ctypes.c_int64)]
+
+
 # Exported symbols and their signatures (mirrors include/mw.h).
 _vp, _i, _f, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
 _cache_p = ctypes.POINTER(mw_kvcache)
+_str_p = ctypes.POINTER(mw_strides)
 SIGNATURES = {
     "mw_last_error": ([], ctypes.c_char_p),
     "mw_version": ([], _i),
@@ -65,6 +70,11 @@ SIGNATURES = {
     "mw_kvcache_slot_of": ([_cache_p, ctypes.c_int64], _i),
     "mw_chunk_attn_cached_workspace_size": ([_cache_p, _i, _i, _i], _sz),
     "mw_chunk_attn_cached": ([_vp, _vp, _vp, _i, _i, _cache_p, _i, _i, _vp, _vp, _f, _vp, _sz, _vp], _i),
+    "mw_block_causal_attn_fwd_strided": ([_vp, _vp, _vp, _vp, _vp, _str_p, _i, _i, _i, _i, _i, _f, _vp], _i),
+    "mw_block_causal_attn_bwd_strided": ([_vp] * 9 + [_vp, _sz, _str_p, _i, _i, _i, _i, _i, _f, _vp], _i),
+    "mw_kvcache_append_strided": ([_cache_p, _vp, _vp, _str_p, _vp], _i),
+    "mw_chunk_attn_cached_strided": ([_vp, _vp, _vp, _i, _i, _cache_p, _i, _i, _vp, _vp, _f, _vp, _sz, _str_p,
+                                      _vp], _i),
 }
 
 _lib = None
@@ -110,16 +120,29 @@ def _ptr(t) -> int:
     return 0 if t is None else t.data_ptr()
 
 
-def _bf16_4d(name, t):
+def _bf16_4d(name, t, view: bool = False):
+    """bf16 [B,H,T,D] on a GPU; contiguous, or (view=True) any view whose last
+    dimension is contiguous (the library checks the remaining strides)."""
     torch = _torch()
     if t.dtype != torch.bfloat16:
         raise TypeError(f"{name} must be bfloat16, got {t.dtype}")
     if t.dim() != 4:
         raise ValueError(f"{name} must be [B,H,T,D], got shape {tuple(t.shape)}")
-    if not t.is_contiguous():
+    if view:
+        if t.shape[-1] > 1 and t.stride(-1) != 1:
+            raise ValueError(f"{name} must have a contiguous last (head) dimension")
+    elif not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if t.device.type != "cuda":
         raise ValueError(f"{name} must be on a GPU device")
+
+
+def _strides(*ts):
+    """mw_strides array (B, H, T element strides) of the given [B,H,T,D] views."""
+    arr = (mw_strides * len(ts))()
+    for i, t in enumerate(ts):
+        arr[i] = mw_strides(t.stride(0), t.stride(1), t.stride(2))
+    return arr
 
 
 def _same_device(*ts):
@@ -131,10 +154,11 @@ def _same_device(*ts):
 
 
 def mw_block_causal_attn_fwd(q, k, v, chunk_len: int, scale=None, out=None, lse=None):
-    """Block-causal attention forward.  q, k, v: bf16 [B,H,T,D].  Returns (o, lse)."""
+    """Block-causal attention forward.  q, k, v: bf16 [B,H,T,D] (views with a
+    contiguous head dimension are read in place).  Returns (o, lse)."""
     torch = _torch()
     for n, t in (("q", q), ("k", k), ("v", v)):
-        _bf16_4d(n, t)
+        _bf16_4d(n, t, view=True)
     if k.shape != q.shape or v.shape != q.shape:
         raise ValueError("q, k, v must have the same shape")
     B, H, T, D = q.shape
@@ -142,12 +166,13 @@ def mw_block_causal_attn_fwd(q, k, v, chunk_len: int, scale=None, out=None, lse=
     scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
     o = torch.empty_like(q) if out is None else out
     lse = torch.empty((B, H, T), dtype=torch.float32, device=dev) if lse is None else lse
-    _bf16_4d("out", o)
+    _bf16_4d("out", o, view=True)
     if o.shape != q.shape or lse.shape != (B, H, T) or lse.dtype != torch.float32 or not lse.is_contiguous():
         raise ValueError("out/lse have the wrong shape or dtype")
     _same_device(q, o, lse)
-    _check(load().mw_block_causal_attn_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, T, D,
-                                           int(chunk_len), scale, _stream_handle(dev)))
+    _check(load().mw_block_causal_attn_fwd_strided(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
+                                                   _strides(q, k, v, o), B, H, T, D, int(chunk_len), scale,
+                                                   _stream_handle(dev)))
     return o, lse
 
 
@@ -157,10 +182,11 @@ def mw_block_causal_attn_bwd_workspace_size(B: int, H: int, T: int, D: int) -> i
 
 def mw_block_causal_attn_bwd(q, k, v, o, d_o, lse, chunk_len: int, scale=None, workspace=None,
                              dq=None, dk=None, dv=None):
-    """Backward of mw_block_causal_attn_fwd.  Returns (dq, dk, dv), bf16 [B,H,T,D]."""
+    """Backward of mw_block_causal_attn_fwd.  Returns (dq, dk, dv), bf16 [B,H,T,D]
+    (views with a contiguous head dimension are accepted for every tensor)."""
     torch = _torch()
     for n, t in (("q", q), ("k", k), ("v", v), ("o", o), ("d_o", d_o)):
-        _bf16_4d(n, t)
+        _bf16_4d(n, t, view=True)
         if t.shape != q.shape:
             raise ValueError(f"{n} must have the shape of q")
     B, H, T, D = q.shape
@@ -175,12 +201,15 @@ def mw_block_causal_attn_bwd(q, k, v, o, d_o, lse, chunk_len: int, scale=None, w
     dk = torch.empty_like(q) if dk is None else dk
     dv = torch.empty_like(q) if dv is None else dv
     for n, t in (("dq", dq), ("dk", dk), ("dv", dv)):
-        _bf16_4d(n, t)
+        _bf16_4d(n, t, view=True)
+        if t.shape != q.shape:
+            raise ValueError(f"{n} must have the shape of q")
     _same_device(q, workspace, dq, dk, dv)
     nbytes = workspace.numel() * workspace.element_size()
-    _check(load().mw_block_causal_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(d_o), _ptr(lse), _ptr(dq),
-                                           _ptr(dk), _ptr(dv), _ptr(workspace), nbytes, B, H, T, D,
-                                           int(chunk_len), scale, _stream_handle(dev)))
+    _check(load().mw_block_causal_attn_bwd_strided(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(d_o), _ptr(lse),
+                                                   _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), nbytes,
+                                                   _strides(q, k, v, o, d_o, dq, dk, dv), B, H, T, D,
+                                                   int(chunk_len), scale, _stream_handle(dev)))
     return dq, dk, dv
 
 
@@ -239,15 +268,17 @@ class KVCache:
 
 
 def mw_kvcache_append(cache: KVCache, k_chunk, v_chunk) -> int:
-    """Commit one chunk (bf16 [B,H,L,D]); returns the slot it was written to."""
+    """Commit one chunk (bf16 [B,H,L,D], or a view of one with a contiguous head
+    dimension); returns the slot it was written to."""
     d = cache.desc
     for n, t in (("k_chunk", k_chunk), ("v_chunk", v_chunk)):
-        _bf16_4d(n, t)
+        _bf16_4d(n, t, view=True)
         if tuple(t.shape) != (d.B, d.H, d.L, d.D):
             raise ValueError(f"{n} must be [B,H,L,D] = {(d.B, d.H, d.L, d.D)}")
     dev = _same_device(cache.k_slots, k_chunk, v_chunk)
     slot = int(d.head % d.S)
-    _check(load().mw_kvcache_append(ctypes.byref(d), _ptr(k_chunk), _ptr(v_chunk), _stream_handle(dev)))
+    _check(load().mw_kvcache_append_strided(ctypes.byref(d), _ptr(k_chunk), _ptr(v_chunk),
+                                            _strides(k_chunk, v_chunk), _stream_handle(dev)))
     return slot
 
 
@@ -286,13 +317,15 @@ def mw_chunk_attn_cached(q, k_new, v_new, n_queued: int, q_len: int, cache: KVCa
     torch = _torch()
     d = cache.desc
     for n, t in (("q", q), ("k_new", k_new), ("v_new", v_new)):
-        _bf16_4d(n, t)
+        _bf16_4d(n, t, view=True)
         if tuple(t.shape) != (d.B, d.H, n_queued * q_len, d.D):
             raise ValueError(f"{n} must be [B,H,n_queued*q_len,D] = {(d.B, d.H, n_queued * q_len, d.D)}")
     dev = _same_device(cache.k_slots, q, k_new, v_new)
     scale = 1.0 / math.sqrt(d.D) if scale is None else float(scale)
     o = torch.empty_like(q) if out is None else out
-    _bf16_4d("out", o)
+    _bf16_4d("out", o, view=True)
+    if o.shape != q.shape:
+        raise ValueError("out must have the shape of q")
     if want_lse and lse is None:
         lse = torch.empty((d.B, d.H, n_queued * q_len), dtype=torch.float32, device=dev)
     if split and workspace is None:
@@ -301,7 +334,8 @@ def mw_chunk_attn_cached(q, k_new, v_new, n_queued: int, q_len: int, cache: KVCa
     if not split:
         workspace = None
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check(load().mw_chunk_attn_cached(_ptr(q), _ptr(k_new), _ptr(v_new), int(n_queued), int(q_len),
-                                       ctypes.byref(d), int(window), int(flags), _ptr(o), _ptr(lse), scale,
-                                       _ptr(workspace), nbytes, _stream_handle(dev)))
+    _check(load().mw_chunk_attn_cached_strided(_ptr(q), _ptr(k_new), _ptr(v_new), int(n_queued), int(q_len),
+                                               ctypes.byref(d), int(window), int(flags), _ptr(o), _ptr(lse), scale,
+                                               _ptr(workspace), nbytes, _strides(q, k_new, v_new, o),
+                                               _stream_handle(dev)))
     return o, lse

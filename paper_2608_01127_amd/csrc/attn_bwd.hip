@@ -31,17 +31,16 @@ __device__ __forceinline__ int xcd_remap_b(int bid, int n) {
 // Row terms of the backward pass: Delta = rowsum(dO * O) and LSE scaled to
 // base 2 (LSE * log2 e), one 16-byte chunk per thread, reduced over the row's lanes.
 template <int D>
-__global__ __launch_bounds__(256) void bwd_rowterms_kernel(const uint16_t* __restrict__ o, const uint16_t* __restrict__ d_o,
-                                                           const float* __restrict__ lse, float* __restrict__ delta,
-                                                           float* __restrict__ lse2, long long n_rows) {
+__global__ __launch_bounds__(256) void bwd_rowterms_kernel(BwdParams p, long long n_rows) {
   constexpr int CPR = D / 8;  // lanes per row (8 or 16)
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long row = gid / CPR;
   const int c = (int)(gid % CPR);
   float acc = 0.f;
   if (row < n_rows) {
-    const u32x4 a = *reinterpret_cast<const u32x4*>(o + row * D + c * 8);
-    const u32x4 b = *reinterpret_cast<const u32x4*>(d_o + row * D + c * 8);
+    const long long bh = row / p.T, t = row - bh * p.T, bi = bh / p.H, hi = bh - bi * p.H;
+    const u32x4 a = *reinterpret_cast<const u32x4*>(p.o + bi * p.so.b + hi * p.so.h + t * p.so.t + c * 8);
+    const u32x4 b = *reinterpret_cast<const u32x4*>(p.d_o + bi * p.sdo.b + hi * p.sdo.h + t * p.sdo.t + c * 8);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const float a0 = __uint_as_float(a[j] << 16), a1 = __uint_as_float(a[j] & 0xffff0000u);
@@ -53,8 +52,8 @@ __global__ __launch_bounds__(256) void bwd_rowterms_kernel(const uint16_t* __res
 #pragma unroll
   for (int w = CPR / 2; w >= 1; w >>= 1) acc += __shfl_xor(acc, w);
   if (row < n_rows && c == 0) {
-    delta[row] = acc;
-    lse2[row] = lse[row] * 1.4426950408889634f;
+    p.delta[row] = acc;
+    p.lse2[row] = p.lse[row] * 1.4426950408889634f;
   }
 }
 
@@ -77,7 +76,8 @@ __global__ __launch_bounds__(64 * NW, (D == 64 ? 8 : 4) / NW) void bwd_dkdv_kern
   const int T = p.T, L = p.L;
   const int k0 = kt * BN;
   const int mykey = k0 + wave * 32 + (lane & 31);
-  const long long off = (long long)bh * T * D;
+  const int bi = bh / p.H, hi = bh - bi * p.H;
+  const long long qb_ = bi * p.sq.b + hi * p.sq.h, dob_ = bi * p.sdo.b + hi * p.sdo.h;
   const float* lse2_bh = p.lse2 + (long long)bh * T;
   const float* dlt_bh = p.delta + (long long)bh * T;
 
@@ -85,11 +85,13 @@ __global__ __launch_bounds__(64 * NW, (D == 64 ? 8 : 4) / NW) void bwd_dkdv_kern
   // read the last key; their dK/dV are never stored.
   bf16x8 kf[KK], vf[KK];
   {
-    const long long a0 = off + (long long)min(mykey, T - 1) * D + 8 * (lane >> 5);
+    const long long kr = min(mykey, T - 1);
+    const bf16_t* ka = p.k + bi * p.sk.b + hi * p.sk.h + kr * p.sk.t + 8 * (lane >> 5);
+    const bf16_t* va = p.v + bi * p.sv.b + hi * p.sv.h + kr * p.sv.t + 8 * (lane >> 5);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      kf[kk] = *reinterpret_cast<const bf16x8*>(p.k + a0 + 16 * kk);
-      vf[kk] = *reinterpret_cast<const bf16x8*>(p.v + a0 + 16 * kk);
+      kf[kk] = *reinterpret_cast<const bf16x8*>(ka + 16 * kk);
+      vf[kk] = *reinterpret_cast<const bf16x8*>(va + 16 * kk);
     }
   }
   f32x16 dv[DB], dk[DB];
@@ -105,8 +107,8 @@ __global__ __launch_bounds__(64 * NW, (D == 64 ? 8 : 4) / NW) void bwd_dkdv_kern
   const float c = p.scale_log2;
 
   auto stage = [&](int q0, int b) {
-    stage_rows_direct<D, BM, NT>(Qs[b], [&](int r) { return p.q + off + (long long)min(q0 + r, T - 1) * D; }, tid);
-    stage_rows_direct<D, BM, NT>(dOs[b], [&](int r) { return p.d_o + off + (long long)min(q0 + r, T - 1) * D; }, tid);
+    stage_rows_direct<D, BM, NT>(Qs[b], [&](int r) { return p.q + qb_ + min(q0 + r, T - 1) * p.sq.t; }, tid);
+    stage_rows_direct<D, BM, NT>(dOs[b], [&](int r) { return p.d_o + dob_ + min(q0 + r, T - 1) * p.sdo.t; }, tid);
     if (wave == 0) stage_f32x64_direct(lse_s[b], lse2_bh, q0, T, lane);
     if (wave == 1) stage_f32x64_direct(dlt_s[b], dlt_bh, q0, T, lane);
   };
@@ -176,8 +178,8 @@ __global__ __launch_bounds__(64 * NW, (D == 64 ? 8 : 4) / NW) void bwd_dkdv_kern
   run(std::true_type{}, T);
 
   if (mykey < T) {
-    bf16_t* dkrow = p.dk + off + (long long)mykey * D;
-    bf16_t* dvrow = p.dv + off + (long long)mykey * D;
+    bf16_t* dkrow = p.dk + bi * p.sdk.b + hi * p.sdk.h + mykey * p.sdk.t;
+    bf16_t* dvrow = p.dv + bi * p.sdv.b + hi * p.sdv.h + mykey * p.sdv.t;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
@@ -211,7 +213,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int T = p.T, L = p.L;
   const int q0 = qt * BM;
-  const long long off = (long long)bh * T * D;
+  const int bi = bh / p.H, hi = bh - bi * p.H;
+  const long long kb_ = bi * p.sk.b + hi * p.sk.h, vb_ = bi * p.sv.b + hi * p.sv.h;
 
   int qrow[RB], e1[RB];
   float lse2[RB], dlt[RB];
@@ -220,11 +223,12 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
   for (int rb = 0; rb < RB; ++rb) {
     qrow[rb] = q0 + (wave * RB + rb) * 32 + (lane & 31);
     const int qc = min(qrow[rb], T - 1);
-    const long long a0 = off + (long long)qc * D + 8 * (lane >> 5);
+    const bf16_t* qa = p.q + bi * p.sq.b + hi * p.sq.h + qc * p.sq.t + 8 * (lane >> 5);
+    const bf16_t* da = p.d_o + bi * p.sdo.b + hi * p.sdo.h + qc * p.sdo.t + 8 * (lane >> 5);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      qf[rb][kk] = *reinterpret_cast<const bf16x8*>(p.q + a0 + 16 * kk);
-      df[rb][kk] = *reinterpret_cast<const bf16x8*>(p.d_o + a0 + 16 * kk);
+      qf[rb][kk] = *reinterpret_cast<const bf16x8*>(qa + 16 * kk);
+      df[rb][kk] = *reinterpret_cast<const bf16x8*>(da + 16 * kk);
     }
     lse2[rb] = p.lse2[(long long)bh * T + qc];
     dlt[rb] = p.delta[(long long)bh * T + qc];
@@ -241,8 +245,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
     for (int db = 0; db < DB; ++db) dq[rb][db] = zero16();
 
   auto stage = [&](int k0, int b) {
-    stage_rows_direct<D, BN, NT>(Ks[b], [&](int r) { return p.k + off + (long long)min(k0 + r, T - 1) * D; }, tid);
-    stage_rows_direct<D, BN, NT>(Vs[b], [&](int r) { return p.v + off + (long long)min(k0 + r, T - 1) * D; }, tid);
+    stage_rows_direct<D, BN, NT>(Ks[b], [&](int r) { return p.k + kb_ + min(k0 + r, T - 1) * p.sk.t; }, tid);
+    stage_rows_direct<D, BN, NT>(Vs[b], [&](int r) { return p.v + vb_ + min(k0 + r, T - 1) * p.sv.t; }, tid);
   };
   auto step = [&](auto masked, const int k0, const int buf) {
     const bf16_t* Kt = Ks[buf];
@@ -314,7 +318,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
     if (qrow[rb] >= T) continue;
-    bf16_t* row = p.dq + off + (long long)qrow[rb] * D;
+    bf16_t* row = p.dq + bi * p.sdq.b + hi * p.sdq.h + qrow[rb] * p.sdq.t;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
@@ -344,8 +348,8 @@ static hipError_t launch_bwd_d(const BwdParams& p, hipStream_t stream) {
   constexpr int NK = BwdCfg<D>::NW_DKV, NQ = BwdCfg<D>::NW_DQ, RQ = BwdCfg<D>::RB_DQ;
   const long long rows = (long long)p.BH * p.T;
   const long long threads = rows * (D / 8);
-  hipLaunchKernelGGL(bwd_rowterms_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p.o,
-                     p.d_o, p.lse, p.delta, p.lse2, rows);
+  hipLaunchKernelGGL(bwd_rowterms_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p,
+                     rows);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int nkt = (p.T + 32 * NK - 1) / (32 * NK);

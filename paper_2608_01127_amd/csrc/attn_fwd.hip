@@ -46,19 +46,20 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
 // straddle a boundary take the per-row mapping, which finds the window chunk
 // of the tile's first key once and moves a row on by whole chunks from there.
 template <int D, bool CACHED, int BN, int NT>
-__device__ __forceinline__ void stage_kv(const FwdParams& p, int bh, long long kvoff, int k0, bf16_t* Kt,
-                                         bf16_t* Vt, int tid) {
+__device__ __forceinline__ void stage_kv(const FwdParams& p, int bh, long long kbase, long long vbase, int k0,
+                                         bf16_t* Kt, bf16_t* Vt, int tid) {
+  const long long skt = p.sk.t, svt = p.sv.t;
   if constexpr (CACHED) {
     const int kl = min(k0 + BN, p.Tk) - 1;  // last real key of the tile
     const int kw0 = k0 - p.sink_len;
     const int w0 = kw0 > 0 ? kw0 / p.L : 0;
     const int off0 = kw0 - w0 * p.L;
     if (k0 >= p.wL) {  // queued keys only
-      const long long e = kvoff + (long long)(k0 - p.wL) * D;
+      const long long ek = kbase + (long long)(k0 - p.wL) * skt, ev = vbase + (long long)(k0 - p.wL) * svt;
       const int last = p.Tk - 1 - k0;
       stage_kv_rows_direct<D, BN, NT>(Kt, Vt, [&](int r) -> RowPair {
-        const long long er = e + (long long)min(r, last) * D;
-        return {p.k + er, p.v + er};
+        const int rr = min(r, last);
+        return {p.k + ek + rr * skt, p.v + ev + rr * svt};
       }, tid);
       return;
     }
@@ -89,13 +90,13 @@ __device__ __forceinline__ void stage_kv(const FwdParams& p, int bh, long long k
         const long long e = (long long)slot * p.slot_stride + ((long long)bh * p.L + off) * D;
         return {p.k_slots + e, p.v_slots + e};
       }
-      const long long e = kvoff + (long long)(key - p.wL) * D;
-      return {p.k + e, p.v + e};
+      const long long j = key - p.wL;
+      return {p.k + kbase + j * skt, p.v + vbase + j * svt};
     }, tid);
   } else {
     stage_kv_rows_direct<D, BN, NT>(Kt, Vt, [&](int r) -> RowPair {
-      const long long e = kvoff + (long long)min(k0 + r, p.Tk - 1) * D;
-      return {p.k + e, p.v + e};
+      const long long j = min(k0 + r, p.Tk - 1);
+      return {p.k + kbase + j * skt, p.v + vbase + j * svt};
     }, tid);
   }
 }
@@ -136,7 +137,10 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int rw = wave % NWR, kg = wave / NWR;  // row wave, key group
   const int q0 = qt * BM;
-  const long long qoff = (long long)bh * p.Tq * D;
+  const int b_ = bh / p.H, h_ = bh - b_ * p.H;
+  const long long qbase = b_ * p.sq.b + h_ * p.sq.h;
+  const long long kbase = b_ * p.sk.b + h_ * p.sk.h;
+  const long long vbase = b_ * p.sv.b + h_ * p.sv.h;
 
   Vis vis{p.vis_mode, p.L, p.Tk, p.qlen, p.wL};
 
@@ -150,7 +154,7 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       if (qrow[rb] < p.Tq) {
-        qf[rb][kk] = *reinterpret_cast<const bf16x8*>(p.q + qoff + (long long)qrow[rb] * D + 16 * kk + 8 * (lane >> 5));
+        qf[rb][kk] = *reinterpret_cast<const bf16x8*>(p.q + qbase + qrow[rb] * p.sq.t + 16 * kk + 8 * (lane >> 5));
       } else {
 #pragma unroll
         for (int j = 0; j < 8; ++j) qf[rb][kk][j] = (__bf16)0.f;
@@ -183,8 +187,6 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
     lsum[rb] = 0.f;
   }
   const float c = p.scale_log2;
-
-  const long long kvoff = (long long)bh * (CACHED ? (long long)p.Tq * D : (long long)p.Tk * D);
 
   // Tiles [0, kfull) are visible to every row of the workgroup and run without
   // any mask code; the remaining tiles (chunk edges, the ragged end, the gap of
@@ -298,13 +300,13 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   {
     // double buffering: the next tile streams in during this step's math
     int buf = 0;
-    if (kc < kend) stage_kv<D, CACHED, BK, NT>(p, bh, kvoff, kc, Ks[0], Vs[0], tid);
+    if (kc < kend) stage_kv<D, CACHED, BK, NT>(p, bh, kbase, vbase, kc, Ks[0], Vs[0], tid);
     wait_vmem();
     __syncthreads();
     auto run = [&](auto masked, const int kstop) {
       while (kc < kstop) {
         const int kn = advance(kc);
-        if (kn < kend) stage_kv<D, CACHED, BK, NT>(p, bh, kvoff, kn, Ks[buf ^ 1], Vs[buf ^ 1], tid);
+        if (kn < kend) stage_kv<D, CACHED, BK, NT>(p, bh, kbase, vbase, kn, Ks[buf ^ 1], Vs[buf ^ 1], tid);
         slice(masked, kc, buf);
         wait_vmem();
         __syncthreads();
@@ -405,7 +407,7 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
       }
     } else {
       const float inv = 1.f / lsum[rb];
-      bf16_t* orow = p.o + qoff + (long long)qrow[rb] * D;
+      bf16_t* orow = p.o + b_ * p.so.b + h_ * p.so.h + qrow[rb] * p.so.t;
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
 #pragma unroll
@@ -453,11 +455,14 @@ struct FwdDecodeCfg {
 // One thread per 4 output columns of a row.
 template <int D>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part, uint16_t* __restrict__ o,
-                                                           float* __restrict__ lse, int NS, long long rows) {
+                                                           Strides so, int H, int Tq, float* __restrict__ lse,
+                                                           int NS, long long rows) {
   constexpr int TPR = D / 4;  // threads per row
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long row = gid / TPR;
   if (row >= rows) return;
+  const long long bh = row / Tq;
+  const long long orow = (bh / H) * so.b + (bh % H) * so.h + (row - bh * Tq) * so.t;
   const int c = (int)(gid % TPR) * 4;
   const float* ml = part + (long long)NS * rows * D;
   // splits are read in groups of G so that G loads are in flight at once
@@ -495,7 +500,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   bf16x4 out;
 #pragma unroll
   for (int j = 0; j < 4; ++j) out[j] = to_bf16(acc[j] * inv);
-  *reinterpret_cast<bf16x4*>(o + row * D + c) = out;
+  *reinterpret_cast<bf16x4*>(o + orow + c) = out;
   if (lse != nullptr && c == 0) lse[row] = (M + __log2f(L)) * 0.69314718055994530942f;
 }
 
@@ -511,7 +516,7 @@ static hipError_t launch_fwd_tpl(FwdParams p, hipStream_t stream) {
   const long long rows = (long long)p.BH * p.Tq;
   const long long threads = rows * (D / 4);
   hipLaunchKernelGGL(attn_combine_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p.part,
-                     p.o, p.lse, p.n_splits, rows);
+                     p.o, p.so, p.H, p.Tq, p.lse, p.n_splits, rows);
   return hipGetLastError();
 }
 

@@ -18,6 +18,24 @@ __global__ __launch_bounds__(256) void kv_copy_kernel(const u32x4* __restrict__ 
   }
 }
 
+// Commit of a strided chunk view: the destination slot is contiguous
+// [B, H, L, D]; 16-byte pieces are gathered from the two source views.
+__global__ __launch_bounds__(256) void kv_gather_kernel(const uint16_t* __restrict__ ks, const uint16_t* __restrict__ vs,
+                                                        Strides sk, Strides sv, u32x4* __restrict__ kd,
+                                                        u32x4* __restrict__ vd, int H, int L, int pieces_per_row,
+                                                        long long n16) {
+  const long long stride = (long long)gridDim.x * blockDim.x;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride) {
+    const long long row = i / pieces_per_row;
+    const int c = (int)(i - row * pieces_per_row) * 8;
+    const long long bh = row / L, t = row - bh * L, b = bh / H, h = bh - b * H;
+    const u32x4 a = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ks + b * sk.b + h * sk.h + t * sk.t + c));
+    const u32x4 w = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vs + b * sv.b + h * sv.h + t * sv.t + c));
+    kd[i] = a;
+    vd[i] = w;
+  }
+}
+
 // RoPE re-shift of cached keys (paper Sec. 3.5): every key row of the live
 // chunks gets its rope band rotated by the angles whose cos/sin the host put in
 // `tab`.  One thread per (row, pair): a 4-byte load of the pair, an fp32
@@ -64,6 +82,17 @@ hipError_t launch_kv_copy(const uint16_t* k_src, const uint16_t* v_src, uint16_t
   hipLaunchKernelGGL(kv_copy_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
                      reinterpret_cast<const u32x4*>(k_src), reinterpret_cast<const u32x4*>(v_src),
                      reinterpret_cast<u32x4*>(k_dst), reinterpret_cast<u32x4*>(v_dst), n16);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_gather(const uint16_t* k_src, const uint16_t* v_src, Strides sk, Strides sv, uint16_t* k_dst,
+                            uint16_t* v_dst, int B, int H, int L, int D, hipStream_t stream) {
+  const long long n16 = (long long)B * H * L * (D / 8);
+  long long blocks = (n16 + 255) / 256;
+  if (blocks > 256 * 16) blocks = 256 * 16;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(kv_gather_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, k_src, v_src, sk, sv,
+                     reinterpret_cast<u32x4*>(k_dst), reinterpret_cast<u32x4*>(v_dst), H, L, D / 8, n16);
   return hipGetLastError();
 }
 

@@ -59,6 +59,42 @@ int hip_status(const char* fn, hipError_t e) {
 
 const float kLog2e = 1.4426950408889634f;
 
+mw::Strides contiguous(int H, int T, int D) { return {(long long)H * T * D, (long long)T * D, D}; }
+
+// A [B, H, T, D] view with D contiguous: strides non-negative, rows 16-byte
+// aligned (every stride a multiple of 8 elements), rows at least D apart.
+// Output views must also not overlap themselves: sorted by stride, each
+// dimension must step past everything the smaller ones span.
+int check_view(const char* fn, const char* name, const mw_strides& s, int B, int H, int T, int D, bool output) {
+  if (s.b < 0 || s.h < 0 || s.t < D)
+    return fail(MW_EINVAL, "%s: strides of %s must be >= 0 with a T stride >= D (got %lld, %lld, %lld)", fn, name,
+                (long long)s.b, (long long)s.h, (long long)s.t);
+  if (s.b % 8 || s.h % 8 || s.t % 8)
+    return fail(MW_EALIGN, "%s: strides of %s must be multiples of 8 elements (16-byte rows)", fn, name);
+  const long double span = (long double)(B - 1) * s.b + (long double)(H - 1) * s.h + (long double)(T - 1) * s.t + D;
+  if (span > (long double)(1LL << 60)) return fail(MW_EUNSUPPORTED, "%s: view %s spans too many elements", fn, name);
+  if (!output) return MW_OK;
+  struct Dim {
+    long long stride, extent;
+  } dims[3] = {{s.t, T}, {s.h, H}, {s.b, B}};
+  for (int i = 0; i < 3; ++i)  // sort by stride (three elements)
+    for (int j = i + 1; j < 3; ++j)
+      if (dims[j].stride < dims[i].stride) {
+        Dim t = dims[i];
+        dims[i] = dims[j];
+        dims[j] = t;
+      }
+  long long covered = D;  // elements spanned by the dimensions below
+  for (auto& d : dims) {
+    if (d.extent == 1) continue;
+    if (d.stride < covered) return fail(MW_EINVAL, "%s: output view %s overlaps itself", fn, name);
+    covered = d.stride * (d.extent - 1) + covered;
+  }
+  return MW_OK;
+}
+
+mw::Strides to_internal(const mw_strides& s) { return {s.b, s.h, s.t}; }
+
 }  // namespace
 
 extern "C" {
@@ -67,13 +103,25 @@ const char* mw_last_error(void) { return g_err.c_str(); }
 
 int mw_version(void) { return 100; }
 
-int mw_block_causal_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int T,
-                             int D, int chunk_len, float scale, mw_stream_t stream) {
+int mw_block_causal_attn_fwd_strided(const void* q, const void* k, const void* v, void* o, float* lse,
+                                     const mw_strides* strides, int B, int H, int T, int D, int chunk_len,
+                                     float scale, mw_stream_t stream) {
   const char* fn = "mw_block_causal_attn_fwd";
   int st = check_ptrs(fn, {{"q", q}, {"k", k}, {"v", v}, {"o", o}, {"lse", lse}});
   if (st) return st;
   st = check_train_dims(fn, B, H, T, D, chunk_len, scale);
   if (st) return st;
+  mw::Strides sv[4];
+  const char* names[4] = {"q", "k", "v", "o"};
+  for (int i = 0; i < 4; ++i) {
+    if (strides == nullptr) {
+      sv[i] = contiguous(H, T, D);
+      continue;
+    }
+    st = check_view(fn, names[i], strides[i], B, H, T, D, i == 3);
+    if (st) return st;
+    sv[i] = to_internal(strides[i]);
+  }
   mw::FwdParams p{};
   p.q = static_cast<const uint16_t*>(q);
   p.k = static_cast<const uint16_t*>(k);
@@ -81,6 +129,7 @@ int mw_block_causal_attn_fwd(const void* q, const void* k, const void* v, void* 
   p.o = static_cast<uint16_t*>(o);
   p.lse = lse;
   p.BH = B * H;
+  p.H = H;
   p.Tq = T;
   p.vis_mode = 0;
   p.L = chunk_len > T ? T : chunk_len;
@@ -89,7 +138,16 @@ int mw_block_causal_attn_fwd(const void* q, const void* k, const void* v, void* 
   p.wL = 0;
   p.scale_log2 = scale * kLog2e;
   p.scale_ln = scale;
+  p.sq = sv[0];
+  p.sk = sv[1];
+  p.sv = sv[2];
+  p.so = sv[3];
   return hip_status(fn, mw::launch_fwd(p, D, false, static_cast<hipStream_t>(stream)));
+}
+
+int mw_block_causal_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int T,
+                             int D, int chunk_len, float scale, mw_stream_t stream) {
+  return mw_block_causal_attn_fwd_strided(q, k, v, o, lse, nullptr, B, H, T, D, chunk_len, scale, stream);
 }
 
 size_t mw_block_causal_attn_bwd_workspace_size(int B, int H, int T, int D) {
@@ -99,9 +157,10 @@ size_t mw_block_causal_attn_bwd_workspace_size(int B, int H, int T, int D) {
   return 2 * ((bytes + 255) & ~(size_t)255);  // Delta and base-2 LSE, one fp32 per row each
 }
 
-int mw_block_causal_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* d_o,
-                             const float* lse, void* dq, void* dk, void* dv, void* workspace, size_t workspace_bytes,
-                             int B, int H, int T, int D, int chunk_len, float scale, mw_stream_t stream) {
+int mw_block_causal_attn_bwd_strided(const void* q, const void* k, const void* v, const void* o, const void* d_o,
+                                     const float* lse, void* dq, void* dk, void* dv, void* workspace,
+                                     size_t workspace_bytes, const mw_strides* strides, int B, int H, int T, int D,
+                                     int chunk_len, float scale, mw_stream_t stream) {
   const char* fn = "mw_block_causal_attn_bwd";
   int st = check_ptrs(fn, {{"q", q}, {"k", k}, {"v", v}, {"o", o}, {"d_o", d_o}, {"lse", lse}, {"dq", dq},
                            {"dk", dk}, {"dv", dv}, {"workspace", workspace}});
@@ -112,6 +171,17 @@ int mw_block_causal_attn_bwd(const void* q, const void* k, const void* v, const 
   if (workspace_bytes < need)
     return fail(MW_EINVAL, "%s: workspace of %zu bytes is smaller than the %zu bytes needed", fn, workspace_bytes,
                 need);
+  mw::Strides sv[8];
+  const char* names[8] = {"q", "k", "v", "o", "d_o", "dq", "dk", "dv"};
+  for (int i = 0; i < 8; ++i) {
+    if (strides == nullptr) {
+      sv[i] = contiguous(H, T, D);
+      continue;
+    }
+    st = check_view(fn, names[i], strides[i], B, H, T, D, i >= 5);
+    if (st) return st;
+    sv[i] = to_internal(strides[i]);
+  }
   mw::BwdParams p{};
   p.q = static_cast<const uint16_t*>(q);
   p.k = static_cast<const uint16_t*>(k);
@@ -125,12 +195,28 @@ int mw_block_causal_attn_bwd(const void* q, const void* k, const void* v, const 
   p.dk = static_cast<uint16_t*>(dk);
   p.dv = static_cast<uint16_t*>(dv);
   p.BH = B * H;
+  p.H = H;
   p.T = T;
   p.L = chunk_len > T ? T : chunk_len;
   p.scale = scale;
   p.scale_log2 = scale * kLog2e;
+  p.sq = sv[0];
+  p.sk = sv[1];
+  p.sv = sv[2];
+  p.so = sv[3];
+  p.sdo = sv[4];
+  p.sdq = sv[5];
+  p.sdk = sv[6];
+  p.sdv = sv[7];
   hipStream_t hs = static_cast<hipStream_t>(stream);
   return hip_status(fn, D == 64 ? mw::launch_bwd_64(p, hs) : mw::launch_bwd_128(p, hs));
+}
+
+int mw_block_causal_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* d_o,
+                             const float* lse, void* dq, void* dk, void* dv, void* workspace, size_t workspace_bytes,
+                             int B, int H, int T, int D, int chunk_len, float scale, mw_stream_t stream) {
+  return mw_block_causal_attn_bwd_strided(q, k, v, o, d_o, lse, dq, dk, dv, workspace, workspace_bytes, nullptr, B, H,
+                                          T, D, chunk_len, scale, stream);
 }
 
 int mw_kvcache_init(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, int H, int L, int D) {
@@ -166,22 +252,40 @@ static int check_cache(const char* fn, const mw_kvcache* c) {
   return MW_OK;
 }
 
-int mw_kvcache_append(mw_kvcache* c, const void* k_chunk, const void* v_chunk, mw_stream_t stream) {
+int mw_kvcache_append_strided(mw_kvcache* c, const void* k_chunk, const void* v_chunk, const mw_strides* strides,
+                              mw_stream_t stream) {
   const char* fn = "mw_kvcache_append";
   int st = check_cache(fn, c);
   if (st) return st;
   st = check_ptrs(fn, {{"k_chunk", k_chunk}, {"v_chunk", v_chunk}});
   if (st) return st;
+  if (strides != nullptr) {
+    st = check_view(fn, "k_chunk", strides[0], c->B, c->H, c->L, c->D, false);
+    if (st) return st;
+    st = check_view(fn, "v_chunk", strides[1], c->B, c->H, c->L, c->D, false);
+    if (st) return st;
+  }
   if (c->head - c->tail == c->S) return fail(MW_EFULL, "%s: all %d slots hold live chunks; evict first", fn, c->S);
   const long long n = (long long)c->B * c->H * c->L * c->D;
   const int slot = (int)(c->head % c->S);
   uint16_t* kd = static_cast<uint16_t*>(c->k_slots) + (long long)slot * n;
   uint16_t* vd = static_cast<uint16_t*>(c->v_slots) + (long long)slot * n;
-  hipError_t e = mw::launch_kv_copy(static_cast<const uint16_t*>(k_chunk), static_cast<const uint16_t*>(v_chunk),
-                                    kd, vd, n, static_cast<hipStream_t>(stream));
+  const uint16_t* ks = static_cast<const uint16_t*>(k_chunk);
+  const uint16_t* vs = static_cast<const uint16_t*>(v_chunk);
+  const mw::Strides cs = contiguous(c->H, c->L, c->D);
+  const bool dense = strides == nullptr ||
+                     (strides[0].b == cs.b && strides[0].h == cs.h && strides[0].t == cs.t && strides[1].b == cs.b &&
+                      strides[1].h == cs.h && strides[1].t == cs.t);
+  hipError_t e = dense ? mw::launch_kv_copy(ks, vs, kd, vd, n, static_cast<hipStream_t>(stream))
+                       : mw::launch_kv_gather(ks, vs, to_internal(strides[0]), to_internal(strides[1]), kd, vd, c->B,
+                                              c->H, c->L, c->D, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_status(fn, e);
   c->head += 1;
   return ok();
+}
+
+int mw_kvcache_append(mw_kvcache* c, const void* k_chunk, const void* v_chunk, mw_stream_t stream) {
+  return mw_kvcache_append_strided(c, k_chunk, v_chunk, nullptr, stream);
 }
 
 int mw_kvcache_set_sink(mw_kvcache* c, const void* k_sink, const void* v_sink, int sink_len) {
@@ -271,9 +375,10 @@ size_t mw_chunk_attn_cached_workspace_size(const mw_kvcache* c, int n_queued, in
   return mw::fwd_split_bytes(c->D, bh, (int)tq, ns);
 }
 
-int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new, int n_queued, int q_len,
-                         const mw_kvcache* c, int window, int flags, void* o, float* lse, float scale,
-                         void* workspace, size_t workspace_bytes, mw_stream_t stream) {
+int mw_chunk_attn_cached_strided(const void* q, const void* k_new, const void* v_new, int n_queued, int q_len,
+                                 const mw_kvcache* c, int window, int flags, void* o, float* lse, float scale,
+                                 void* workspace, size_t workspace_bytes, const mw_strides* strides,
+                                 mw_stream_t stream) {
   const char* fn = "mw_chunk_attn_cached";
   int st = check_cache(fn, c);
   if (st) return st;
@@ -292,6 +397,17 @@ int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new, in
   if (n_queued > MW_MAX_QUEUED) return fail(MW_EUNSUPPORTED, "%s: n_queued %d exceeds %d", fn, n_queued, MW_MAX_QUEUED);
   const long long nq_tok = (long long)n_queued * q_len;
   if (nq_tok + w * c->L + c->sink_len > kMaxT) return fail(MW_EUNSUPPORTED, "%s: too many tokens", fn);
+  mw::Strides sv[4];
+  const char* names[4] = {"q", "k_new", "v_new", "o"};
+  for (int i = 0; i < 4; ++i) {
+    if (strides == nullptr) {
+      sv[i] = contiguous(c->H, (int)nq_tok, c->D);
+      continue;
+    }
+    st = check_view(fn, names[i], strides[i], c->B, c->H, (int)nq_tok, c->D, i == 3);
+    if (st) return st;
+    sv[i] = to_internal(strides[i]);
+  }
   mw::FwdParams p{};
   p.q = static_cast<const uint16_t*>(q);
   p.k = static_cast<const uint16_t*>(k_new);
@@ -299,6 +415,7 @@ int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new, in
   p.o = static_cast<uint16_t*>(o);
   p.lse = lse;
   p.BH = c->B * c->H;
+  p.H = c->H;
   p.Tq = (int)nq_tok;
   p.vis_mode = flags == MW_QUEUED_CAUSAL ? 1 : 2;
   p.L = c->L;
@@ -317,7 +434,18 @@ int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new, in
   p.first_slot = (int)((c->head - w) % c->S);
   p.n_splits = mw::fwd_choose_splits(c->D, p.BH, p.Tq, p.Tk, workspace != nullptr ? workspace_bytes : 0);
   p.part = static_cast<float*>(workspace);
+  p.sq = sv[0];
+  p.sk = sv[1];
+  p.sv = sv[2];
+  p.so = sv[3];
   return hip_status(fn, mw::launch_fwd(p, c->D, true, static_cast<hipStream_t>(stream)));
+}
+
+int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new, int n_queued, int q_len,
+                         const mw_kvcache* c, int window, int flags, void* o, float* lse, float scale,
+                         void* workspace, size_t workspace_bytes, mw_stream_t stream) {
+  return mw_chunk_attn_cached_strided(q, k_new, v_new, n_queued, q_len, c, window, flags, o, lse, scale, workspace,
+                                      workspace_bytes, nullptr, stream);
 }
 
 }  // extern "C"

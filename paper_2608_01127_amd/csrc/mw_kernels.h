@@ -6,6 +6,14 @@
 
 namespace mw {
 
+// Element strides of a [B, H, T, D] tensor view (D contiguous): element
+// (b, h, t, d) is at base + b * b_ + h * h_ + t * t_ + d.
+struct Strides {
+  long long b;
+  long long h;
+  long long t;
+};
+
 // Forward / cached attention.  Queries: [BH, Tq, D]; keys: the (virtual) key
 // sequence of length vis.Tk described below; output O [BH, Tq, D], lse [BH, Tq].
 struct FwdParams {
@@ -15,6 +23,7 @@ struct FwdParams {
   uint16_t* o;
   float* lse;  // may be null (cached attention)
   int BH;
+  int H;
   int Tq;
   int n_qtiles;   // set by the launcher from its tile configuration
   int vis_mode;  // VisMode
@@ -37,6 +46,9 @@ struct FwdParams {
   // query tile's key tiles and writes fp32 partials (see attn_fwd.hip)
   int n_splits;
   float* part;  // [n_splits][BH][Tq][D] unnormalised O, then [n_splits][BH][Tq][2] (m, l)
+  // views of q, k (training keys / queued keys), v and o; lse and the ring
+  // are always contiguous
+  Strides sq, sk, sv, so;
 };
 
 struct BwdParams {
@@ -52,10 +64,13 @@ struct BwdParams {
   uint16_t* dk;
   uint16_t* dv;
   int BH;
+  int H;
   int T;
   int L;
   float scale;
   float scale_log2;
+  // views of the [B, H, T, D] tensors; lse, delta and lse2 are contiguous [B, H, T]
+  Strides sq, sk, sv, so, sdo, sdq, sdk, sdv;
 };
 
 // Tile sizes (shared with the host for grid computation).
@@ -92,5 +107,8 @@ hipError_t launch_rope_shift(uint16_t* k_slots, long long slot_stride, int S, in
                              hipStream_t stream);
 hipError_t launch_kv_copy(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_dst,
                           uint16_t* v_dst, long long n_elems, hipStream_t stream);
+// Gather of a strided [B, H, L, D] K/V chunk into a contiguous slot.
+hipError_t launch_kv_gather(const uint16_t* k_src, const uint16_t* v_src, Strides sk, Strides sv, uint16_t* k_dst,
+                            uint16_t* v_dst, int B, int H, int L, int D, hipStream_t stream);
 
 }  // namespace mw

@@ -75,6 +75,50 @@ def test_bwd_validation_and_workspace():
     assert b(*args, ws, 2, 3, 100, 32, 10, 0.125, None) == mw.MW_EUNSUPPORTED
 
 
+def strides(*triples):
+    arr = (_lib.mw_strides * len(triples))()
+    for i, t in enumerate(triples):
+        arr[i] = _lib.mw_strides(*t)
+    return arr
+
+
+def test_strided_validation():
+    """Views: strides >= 0, multiples of 8 elements, T stride >= D; outputs must not overlap
+    themselves.  Every call here fails validation, so nothing is launched."""
+    lib = mw.load()
+    f = lib.mw_block_causal_attn_fwd_strided
+    B, H, T, D = 2, 3, 40, 64
+    cont = (H * T * D, T * D, D)
+    bthd = (T * H * D, D, H * D)             # [B,T,H,D] seen as [B,H,T,D]
+    fused = (3 * T * H * D, D, 3 * H * D)    # q/k/v inside [B,T,3,H,D]
+    # valid input views get past the stride checks and stop at a bad output view
+    for good in (cont, bthd, fused):
+        st = strides(good, good, good, (H * T * D, D, D))
+        assert f(A, A, A, A, A, st, B, H, T, D, 8, 0.125, None) == mw.MW_EINVAL and "o overlaps" in err()
+    bad_cases = [
+        (strides((-8, T * D, D), cont, cont, cont), mw.MW_EINVAL, "strides of q"),
+        (strides(cont, (H * T * D, T * D, 60), cont, cont), mw.MW_EINVAL, "strides of k"),
+        (strides(cont, cont, (H * T * D, T * D + 4, D + 4), cont), mw.MW_EALIGN, "multiples of 8"),
+        (strides(cont, cont, cont, (H * T * D, D, D)), mw.MW_EINVAL, "overlaps"),
+        (strides(cont, cont, cont, (0, T * D, D)), mw.MW_EINVAL, "overlaps"),
+    ]
+    for st, code, msg in bad_cases:
+        assert f(A, A, A, A, A, st, B, H, T, D, 8, 0.125, None) == code, msg
+        assert msg in err()
+    # inputs may broadcast (stride 0) and overlap each other; outputs may not overlap themselves
+    bwd = lib.mw_block_causal_attn_bwd_strided
+    ws = lib.mw_block_causal_attn_bwd_workspace_size(B, H, T, D)
+    st8 = strides(cont, cont, cont, cont, cont, cont, (H * T * D, D, D), cont)
+    assert bwd(*([A] * 10), ws, st8, B, H, T, D, 8, 0.125, None) == mw.MW_EINVAL and "dk overlaps" in err()
+    c = new_cache(S=4, B=1, H=2, L=16, D=64)
+    ap = lib.mw_kvcache_append_strided
+    assert ap(ctypes.byref(c), A, A, strides((2 * 16 * 64, 16 * 64, 63), (2 * 16 * 64, 16 * 64, 64)), None) \
+        == mw.MW_EINVAL and c.head == 0
+    ca = lib.mw_chunk_attn_cached_strided
+    st4 = strides(cont, cont, cont, (0, 0, 64))
+    assert ca(A, A, A, 1, 16, ctypes.byref(c), 0, 0, A, None, 0.125, None, 0, st4, None) == mw.MW_EINVAL
+
+
 def new_cache(S=8, B=1, H=2, L=16, D=64):
     c = _lib.mw_kvcache()
     assert mw.load().mw_kvcache_init(ctypes.byref(c), A, A, S, B, H, L, D) == mw.MW_OK
