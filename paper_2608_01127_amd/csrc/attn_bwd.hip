@@ -106,9 +106,15 @@ __global__ __launch_bounds__(64 * NW, (D == 64 ? 8 : 4) / NW) void bwd_dkdv_kern
   const int qstart = ((k0 / L) * L / BM) * BM;  // first query tile with a query of chunk >= chunk(k0)
   const float c = p.scale_log2;
 
+  const RowOffsets<D, BM, NT> ro_q(p.sq.t, tid), ro_do(p.sdo.t, tid);
   auto stage = [&](int q0, int b) {
-    stage_rows_direct<D, BM, NT>(Qs[b], [&](int r) { return p.q + qb_ + min(q0 + r, T - 1) * p.sq.t; }, tid);
-    stage_rows_direct<D, BM, NT>(dOs[b], [&](int r) { return p.d_o + dob_ + min(q0 + r, T - 1) * p.sdo.t; }, tid);
+    if (q0 + BM <= T) {  // whole tile: scalar base + per-thread offsets
+      stage_rows_s<D, BM, NT>(Qs[b], p.q + qb_ + q0 * p.sq.t, ro_q, tid);
+      stage_rows_s<D, BM, NT>(dOs[b], p.d_o + dob_ + q0 * p.sdo.t, ro_do, tid);
+    } else {  // the ragged last tile: rows past T read the last row
+      stage_rows_direct<D, BM, NT>(Qs[b], [&](int r) { return p.q + qb_ + min(q0 + r, T - 1) * p.sq.t; }, tid);
+      stage_rows_direct<D, BM, NT>(dOs[b], [&](int r) { return p.d_o + dob_ + min(q0 + r, T - 1) * p.sdo.t; }, tid);
+    }
     if (wave == 0) stage_f32x64_direct(lse_s[b], lse2_bh, q0, T, lane);
     if (wave == 1) stage_f32x64_direct(dlt_s[b], dlt_bh, q0, T, lane);
   };
@@ -244,9 +250,15 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
 #pragma unroll
     for (int db = 0; db < DB; ++db) dq[rb][db] = zero16();
 
+  const RowOffsets<D, BN, NT> ro_k(p.sk.t, tid), ro_v(p.sv.t, tid);
   auto stage = [&](int k0, int b) {
-    stage_rows_direct<D, BN, NT>(Ks[b], [&](int r) { return p.k + kb_ + min(k0 + r, T - 1) * p.sk.t; }, tid);
-    stage_rows_direct<D, BN, NT>(Vs[b], [&](int r) { return p.v + vb_ + min(k0 + r, T - 1) * p.sv.t; }, tid);
+    if (k0 + BN <= T) {  // whole tile: scalar base + per-thread offsets
+      stage_rows_s<D, BN, NT>(Ks[b], p.k + kb_ + k0 * p.sk.t, ro_k, tid);
+      stage_rows_s<D, BN, NT>(Vs[b], p.v + vb_ + k0 * p.sv.t, ro_v, tid);
+    } else {  // the ragged last tile: rows past T read the last row
+      stage_rows_direct<D, BN, NT>(Ks[b], [&](int r) { return p.k + kb_ + min(k0 + r, T - 1) * p.sk.t; }, tid);
+      stage_rows_direct<D, BN, NT>(Vs[b], [&](int r) { return p.v + vb_ + min(k0 + r, T - 1) * p.sv.t; }, tid);
+    }
   };
   auto step = [&](auto masked, const int k0, const int buf) {
     const bf16_t* Kt = Ks[buf];

@@ -37,42 +37,49 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
   return (bid % 8) * (n / 8) + bid / 8;
 }
 
+// Per-thread row offsets of the K and V tiles: queued / training keys (their
+// views' T strides) and ring slots (rows D apart).
+template <int D, bool CACHED, int BN, int NT>
+struct KVOffsets {
+  RowOffsets<D, BN, NT> k, v, w;
+  __device__ __forceinline__ KVOffsets(const FwdParams& p, int tid)
+      : k(p.sk.t, tid), v(p.sv.t, tid), w(CACHED ? D : 0, tid) {}
+};
+
 // Staging of one K/V tile straight into LDS.  Key rows past the end of the
 // (virtual) key sequence read the last key instead; the mask hides them.
-// Cached attention: the key sequence is the sink, then the window chunks in
-// ring slots, then the queued chunks.  A tile that lies inside one window
-// chunk or inside the queued keys (almost every tile) is classified once with
-// wave-uniform scalar tests and staged from one base pointer; only tiles that
-// straddle a boundary take the per-row mapping, which finds the window chunk
-// of the tile's first key once and moves a row on by whole chunks from there.
+// A tile of equally spaced rows (almost every tile) is staged from one
+// wave-uniform base pointer plus the per-thread offsets above.  Cached
+// attention: the key sequence is the sink, then the window chunks in ring
+// slots, then the queued chunks; a tile inside one window chunk or inside the
+// queued keys is recognised with scalar tests, and only tiles that straddle a
+// boundary (or the ragged end) take the per-row mapping.
 template <int D, bool CACHED, int BN, int NT>
 __device__ __forceinline__ void stage_kv(const FwdParams& p, int bh, long long kbase, long long vbase, int k0,
-                                         bf16_t* Kt, bf16_t* Vt, int tid) {
+                                         bf16_t* Kt, bf16_t* Vt, const KVOffsets<D, CACHED, BN, NT>& ro, int tid) {
   const long long skt = p.sk.t, svt = p.sv.t;
   if constexpr (CACHED) {
     const int kl = min(k0 + BN, p.Tk) - 1;  // last real key of the tile
     const int kw0 = k0 - p.sink_len;
     const int w0 = kw0 > 0 ? kw0 / p.L : 0;
     const int off0 = kw0 - w0 * p.L;
-    if (k0 >= p.wL) {  // queued keys only
-      const long long ek = kbase + (long long)(k0 - p.wL) * skt, ev = vbase + (long long)(k0 - p.wL) * svt;
-      const int last = p.Tk - 1 - k0;
-      stage_kv_rows_direct<D, BN, NT>(Kt, Vt, [&](int r) -> RowPair {
-        const int rr = min(r, last);
-        return {p.k + ek + rr * skt, p.v + ev + rr * svt};
-      }, tid);
+    if (k0 >= p.wL && k0 + BN <= p.Tk) {  // queued keys only, a whole tile
+      const long long j = k0 - p.wL;
+      stage_rows_s<D, BN, NT>(Kt, p.k + kbase + j * skt, ro.k, tid);
+      stage_rows_s<D, BN, NT>(Vt, p.v + vbase + j * svt, ro.v, tid);
       return;
     }
     if (kw0 >= 0 && kl < p.wL && off0 + (kl - k0) < p.L) {  // one window chunk
       int slot = p.first_slot + w0;
       slot = slot >= p.S ? slot - p.S : slot;
       const long long e = (long long)slot * p.slot_stride + ((long long)bh * p.L + off0) * D;
-      stage_kv_rows_direct<D, BN, NT>(Kt, Vt, [&](int r) -> RowPair {
-        const long long er = e + (long long)r * D;
-        return {p.k_slots + er, p.v_slots + er};
-      }, tid);
+      stage_rows_s<D, BN, NT>(Kt, p.k_slots + e, ro.w, tid);
+      stage_rows_s<D, BN, NT>(Vt, p.v_slots + e, ro.w, tid);
       return;
     }
+    // a tile straddling the sink, chunk or queued boundaries, or the end:
+    // row by row (the window chunk of the first key is found once; a row
+    // moves on by whole chunks from there)
     stage_kv_rows_direct<D, BN, NT>(Kt, Vt, [&](int r) -> RowPair {
       const int key = min(k0 + r, p.Tk - 1);
       if (key < p.sink_len) {
@@ -94,7 +101,12 @@ __device__ __forceinline__ void stage_kv(const FwdParams& p, int bh, long long k
       return {p.k + kbase + j * skt, p.v + vbase + j * svt};
     }, tid);
   } else {
-    stage_kv_rows_direct<D, BN, NT>(Kt, Vt, [&](int r) -> RowPair {
+    if (k0 + BN <= p.Tk) {
+      stage_rows_s<D, BN, NT>(Kt, p.k + kbase + (long long)k0 * skt, ro.k, tid);
+      stage_rows_s<D, BN, NT>(Vt, p.v + vbase + (long long)k0 * svt, ro.v, tid);
+      return;
+    }
+    stage_kv_rows_direct<D, BN, NT>(Kt, Vt, [&](int r) -> RowPair {  // the ragged last tile
       const long long j = min(k0 + r, p.Tk - 1);
       return {p.k + kbase + j * skt, p.v + vbase + j * svt};
     }, tid);
@@ -239,7 +251,7 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
 #pragma unroll
         for (int i = 0; i < 16; ++i) mx[rb] = fmaxf(mx[rb], s[rb][kb][i]);
       }
-      mx[rb] = fmaxf(mx[rb], __shfl_xor(mx[rb], 32)) * c;  // scaled row max of this tile (log2 units)
+      mx[rb] = max_halves(mx[rb]) * c;  // scaled row max of this tile (log2 units)
       need[rb] = mx[rb] > m[rb] + kRescaleThreshold;
       need_any |= need[rb];
     }
@@ -296,17 +308,18 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   auto slice = [&](auto masked, const int k0, const int st) {
     step(masked, k0 + kg * BN, Ks[st] + kg * BN * D, Vs[st] + kg * BN * D);
   };
+  const KVOffsets<D, CACHED, BK, NT> kvo(p, tid);
   int kc = advance(kbeg - BK);  // next tile to use
   {
     // double buffering: the next tile streams in during this step's math
     int buf = 0;
-    if (kc < kend) stage_kv<D, CACHED, BK, NT>(p, bh, kbase, vbase, kc, Ks[0], Vs[0], tid);
+    if (kc < kend) stage_kv<D, CACHED, BK, NT>(p, bh, kbase, vbase, kc, Ks[0], Vs[0], kvo, tid);
     wait_vmem();
     __syncthreads();
     auto run = [&](auto masked, const int kstop) {
       while (kc < kstop) {
         const int kn = advance(kc);
-        if (kn < kend) stage_kv<D, CACHED, BK, NT>(p, bh, kbase, vbase, kn, Ks[buf ^ 1], Vs[buf ^ 1], tid);
+        if (kn < kend) stage_kv<D, CACHED, BK, NT>(p, bh, kbase, vbase, kn, Ks[buf ^ 1], Vs[buf ^ 1], kvo, tid);
         slice(masked, kc, buf);
         wait_vmem();
         __syncthreads();
@@ -382,7 +395,7 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
 
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    lsum[rb] += __shfl_xor(lsum[rb], 32);
+    lsum[rb] = sum_halves(lsum[rb]);
     if (qrow[rb] >= p.Tq) continue;
     if (NS > 1) {
       // partial result of this key range: unnormalised O, the reference max m

@@ -71,6 +71,8 @@ int check_view(const char* fn, const char* name, const mw_strides& s, int B, int
                 (long long)s.b, (long long)s.h, (long long)s.t);
   if (s.b % 8 || s.h % 8 || s.t % 8)
     return fail(MW_EALIGN, "%s: strides of %s must be multiples of 8 elements (16-byte rows)", fn, name);
+  if (s.t > (1LL << 23))  // byte offsets within a staged tile of up to 128 rows stay below 2^32
+    return fail(MW_EUNSUPPORTED, "%s: T stride of %s exceeds 2^23 elements", fn, name);
   const long double span = (long double)(B - 1) * s.b + (long double)(H - 1) * s.h + (long double)(T - 1) * s.t + D;
   if (span > (long double)(1LL << 60)) return fail(MW_EUNSUPPORTED, "%s: view %s spans too many elements", fn, name);
   if (!output) return MW_OK;

@@ -160,6 +160,47 @@ __device__ __forceinline__ void stage_rows_direct(bf16_t* lds_tile, RowPtr row_p
   }
 }
 
+// The same load with a wave-uniform 64-bit base held in SGPRs and a per-lane
+// 32-bit byte offset (the saddr form): a tile whose rows are equally spaced is
+// staged from one scalar base per tile and offsets computed once per kernel.
+__device__ __forceinline__ void dma_lds_16_s(const void* sbase, unsigned voff, MW_LDS void* wave_dst) {
+  const unsigned base = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)wave_dst);
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(base)
+               : "m0", "memory");
+}
+
+// Byte offsets, from the tile's first row, of the 16-byte pieces this thread
+// stages of a ROWS x D tile whose rows are `row_stride` elements apart (same
+// piece assignment and swizzle as stage_rows_direct).  Computed once; the
+// offsets must fit 32 bits (ROWS * row_stride * 2 < 2^32, checked by the host).
+template <int D, int ROWS, int NT>
+struct RowOffsets {
+  static constexpr int SLOTS = D / 8;
+  static constexpr int ROUNDS = ROWS * SLOTS / NT;
+  unsigned off[ROUNDS];
+  __device__ __forceinline__ RowOffsets(long long row_stride, int tid) {
+#pragma unroll
+    for (int it = 0; it < ROUNDS; ++it) {
+      const int ci = it * NT + tid;
+      const int row = ci / SLOTS, ps = ci % SLOTS;
+      const int ls = ps ^ Tile<D>::swz(row);
+      off[it] = (unsigned)((long long)row * row_stride * 2 + ls * 16);
+    }
+  }
+};
+
+// Stage a tile whose row 0 is at `tile` (wave-uniform) with rows laid out as
+// `ro` describes.
+template <int D, int ROWS, int NT>
+__device__ __forceinline__ void stage_rows_s(bf16_t* lds_tile, const bf16_t* tile, const RowOffsets<D, ROWS, NT>& ro,
+                                             int tid) {
+#pragma unroll
+  for (int it = 0; it < RowOffsets<D, ROWS, NT>::ROUNDS; ++it) {
+    bf16_t* dst = lds_tile + (it * NT + (tid & ~63)) * 8;  // wave-uniform base
+    dma_lds_16_s(tile, ro.off[it], (MW_LDS void*)dst);
+  }
+}
+
 // Same staging for a K tile and a V tile whose rows come from the same
 // positions: row_src(row) returns the pair of row pointers, so the address
 // arithmetic of a row is done once for both tiles.
@@ -195,6 +236,19 @@ __device__ __forceinline__ void stage_f32x64_direct(float* lds, const float* g, 
 // counter at zero.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0); }
 
+
+// Combine a value with the one held by lane l ^ 32: gfx950's permlane32 swap
+// exchanges the two 32-lane halves of a register in the VALU, without the LDS
+// round trip of a generic shuffle.  The two results are {x[l], x[l ^ 32]} in
+// some order, so a symmetric combination needs no select.
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 // Row (within a 32-row accumulator block) of accumulator register i in lane l.
 __device__ __forceinline__ int acc_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
