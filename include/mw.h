@@ -269,6 +269,63 @@ int mw_chunk_attn_cached_strided(const void* q, const void* k_new, const void* v
                                  void* o, float* lse, float scale, void* workspace, size_t workspace_bytes,
                                  const mw_strides* strides, mw_stream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Pipelined denoising schedule (Sec. 3.5, "Pipelined Denoising" and the
+ * latent update of Eq. 7; non-decreasing chunk timesteps, Eq. 4; timestep
+ * shift, Eq. 6).  Host-only planning of the streaming loop: which chunks are
+ * in flight at each tick (one DiT pass over the active window), their noise
+ * levels and updates, and which chunks are committed, evicted and re-shifted
+ * afterwards.  No device work and no state: a tick's plan is a function of the
+ * configuration and the tick number.
+ *
+ * Chunks are numbered 0 .. n_chunks-1 in generation order.  `stride` new
+ * chunks enter per tick at tau = 1 (fewer at the end of the stream); each
+ * stays U = floor(window / stride) ticks and gets one update per tick, so the
+ * window never holds more than U * stride <= window chunks.  Before its k-th
+ * update a chunk is at tau = g(k/U), g(x) = shift(1 - x),
+ * shift(t) = s t / (1 + (s - 1) t); its update is g((k+1)/U) - g(k/U) <= 0
+ * and its last update lands on tau = 0 exactly, after which it is committed
+ * (Delta-tau allocated from the stride and the window so that every chunk
+ * reaches the data endpoint before commit).  With n_bins > 0 each level is
+ * rounded to the nearest multiple of 1/n_bins.  Older chunks are never noisier
+ * than newer ones (Eq. 4).  After the tick's commits the FIFO keeps the newest
+ * cache_chunks committed chunks; the evicted chunks' frames are the RoPE
+ * re-shift of the retained keys.  Positions are frames of the re-indexed
+ * sequence [sink (sink_frames) | cached chunks | in-flight chunks].
+ * ---------------------------------------------------------------------- */
+typedef struct {
+  int window;           /* in-flight chunk capacity, 1 .. MW_MAX_QUEUED */
+  int stride;           /* chunks entering per tick, 1 .. window */
+  int n_chunks;         /* chunks to generate, >= 1 */
+  int cache_chunks;     /* capacity of the committed FIFO, >= 0 */
+  int frames_per_chunk; /* latent frames (RoPE positions) per chunk, >= 1 */
+  int sink_frames;      /* frames of the sink anchor, >= 0 */
+  double shift;         /* timestep shift s > 0 (1: none) */
+  int n_bins;           /* 0, or the number of discrete timestep bins */
+} mw_sched_config;
+
+typedef struct {
+  int64_t tick;
+  int first;             /* oldest in-flight chunk; in flight: first .. first+n_active-1 */
+  int n_active;          /* in-flight chunks this tick (n_queued of mw_chunk_attn_cached) */
+  int updates_per_chunk; /* U */
+  double tau[MW_MAX_QUEUED];  /* noise level of each in-flight chunk before this tick's update */
+  double dtau[MW_MAX_QUEUED]; /* its update (<= 0); unused entries are 0 */
+  int n_commit;          /* chunks first .. first+n_commit-1 reach tau = 0 and are committed, in order */
+  int n_evict;           /* oldest cached chunks evicted after the commits */
+  int rope_shift;        /* frames the retained keys move back: n_evict * frames_per_chunk */
+  int cache_live;        /* cached chunks after this tick */
+  int pos_first;         /* frame of the oldest in-flight chunk during this tick */
+} mw_sched_tick;
+
+/* Ticks until every chunk is committed (floor((n_chunks-1)/stride) + U), or a
+ * negative mw_status for an invalid configuration (MW_EINVAL, MW_EUNSUPPORTED). */
+int64_t mw_sched_num_ticks(const mw_sched_config* cfg);
+
+/* Plan of tick `tick` (0-based) into *out.  Errors: MW_EINVAL (invalid
+ * configuration, NULL out), MW_EUNSUPPORTED, MW_EEMPTY (tick out of range). */
+int mw_sched_plan(const mw_sched_config* cfg, int64_t tick, mw_sched_tick* out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -15,6 +15,9 @@ Contents
   (paper Sec. 3.5, "Structured Rolling KV Cache").
 - rope_rotate (attention.py): rotary position embedding on a band of head
   dimensions, used for the re-shifting of cached keys (paper Sec. 3.5).
+- scheduler.py: the pipelined asynchronous denoiser simulated tick by tick
+  (paper Sec. 3.5, Eq. 4, Eq. 6, Eq. 7): which chunks are in flight, their
+  timesteps and updates, commits, evictions and re-shifts.
 
 Parity status: every function here is pinned by the not-gpu tests in
 tests/test_oracle.py (library special cases, closed forms, invariants,
@@ -35,3 +38,4 @@ from .attention import (  # noqa: F401
     QUEUED_ISOLATED,
 )
 from .ring import RingModel, RingError  # noqa: F401
+from .scheduler import simulate as simulate_pipeline, shifted_tau, tau_level  # noqa: F401

@@ -2,7 +2,8 @@
 
 Python face of libmw.so (C ABI in include/mw.h): block-causal multi-head
 attention forward/backward (paper Sec. 3.2), the ring-buffered rolling KV
-cache and cached attention of queued in-flight chunks (paper Sec. 3.5).
+cache and cached attention of queued in-flight chunks, and the host plan of
+the pipelined denoiser (paper Sec. 3.5).
 The functions carry the C entry points' names; all compute runs in the HIP
 kernels of csrc/.
 """
@@ -33,4 +34,10 @@ from ._lib import (  # noqa: F401
     mw_kvcache_set_sink,
     mw_rope,
     mw_kvcache_slot_of,
+    mw_sched_config,
+    mw_sched_num_ticks,
+    mw_sched_plan,
+    mw_sched_tick,
+    mw_strides,
+    sched_config,
 )

@@ -51,6 +51,20 @@ class mw_strides(ctypes.Structure):
     _fields_ = [("b", ctypes.c_int64), ("h", ctypes.c_int64), ("t", ctypes.c_int64)]
 
 
+class mw_sched_config(ctypes.Structure):
+    _fields_ = [("window", ctypes.c_int), ("stride", ctypes.c_int), ("n_chunks", ctypes.c_int),
+                ("cache_chunks", ctypes.c_int), ("frames_per_chunk", ctypes.c_int), ("sink_frames", ctypes.c_int),
+                ("shift", ctypes.c_double), ("n_bins", ctypes.c_int)]
+
+
+class mw_sched_tick(ctypes.Structure):
+    _fields_ = [("tick", ctypes.c_int64), ("first", ctypes.c_int), ("n_active", ctypes.c_int),
+                ("updates_per_chunk", ctypes.c_int),
+                ("tau", ctypes.c_double * MW_MAX_QUEUED), ("dtau", ctypes.c_double * MW_MAX_QUEUED),
+                ("n_commit", ctypes.c_int), ("n_evict", ctypes.c_int), ("rope_shift", ctypes.c_int),
+                ("cache_live", ctypes.c_int), ("pos_first", ctypes.c_int)]
+
+
 # Exported symbols and their signatures (mirrors include/mw.h).
 _vp, _i, _f, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
 _cache_p = ctypes.POINTER(mw_kvcache)
@@ -75,6 +89,8 @@ SIGNATURES = {
     "mw_kvcache_append_strided": ([_cache_p, _vp, _vp, _str_p, _vp], _i),
     "mw_chunk_attn_cached_strided": ([_vp, _vp, _vp, _i, _i, _cache_p, _i, _i, _vp, _vp, _f, _vp, _sz, _str_p,
                                       _vp], _i),
+    "mw_sched_num_ticks": ([ctypes.POINTER(mw_sched_config)], ctypes.c_int64),
+    "mw_sched_plan": ([ctypes.POINTER(mw_sched_config), ctypes.c_int64, ctypes.POINTER(mw_sched_tick)], _i),
 }
 
 _lib = None
@@ -339,3 +355,27 @@ def mw_chunk_attn_cached(q, k_new, v_new, n_queued: int, q_len: int, cache: KVCa
                                                _ptr(workspace), nbytes, _strides(q, k_new, v_new, o),
                                                _stream_handle(dev)))
     return o, lse
+
+
+# ----------------------------------------------------------------------------- pipelined denoising schedule
+
+def sched_config(window: int, stride: int, n_chunks: int, cache_chunks: int, frames_per_chunk: int,
+                 sink_frames: int = 0, shift: float = 1.0, n_bins: int = 0) -> mw_sched_config:
+    return mw_sched_config(int(window), int(stride), int(n_chunks), int(cache_chunks), int(frames_per_chunk),
+                           int(sink_frames), float(shift), int(n_bins))
+
+
+def mw_sched_num_ticks(cfg: mw_sched_config) -> int:
+    return int(_check(load().mw_sched_num_ticks(ctypes.byref(cfg))))
+
+
+def mw_sched_plan(cfg: mw_sched_config, tick: int) -> dict:
+    """Plan of one tick of the pipelined denoiser (see include/mw.h) as a dict."""
+    out = mw_sched_tick()
+    _check(load().mw_sched_plan(ctypes.byref(cfg), int(tick), ctypes.byref(out)))
+    n = out.n_active
+    return {"tick": int(out.tick), "first": out.first, "n_active": n, "updates_per_chunk": out.updates_per_chunk,
+            "ids": list(range(out.first, out.first + n)), "tau": list(out.tau[:n]), "dtau": list(out.dtau[:n]),
+            "n_commit": out.n_commit, "committed": list(range(out.first, out.first + out.n_commit)),
+            "n_evict": out.n_evict, "rope_shift": out.rope_shift, "cache_live": out.cache_live,
+            "pos_first": out.pos_first}

@@ -37,6 +37,7 @@ UNITS = [  # (object name, source, extra flags)
     ("attn_bwd128", "attn_bwd.hip", ["-DMW_BWD_HEAD_DIM=128", *ILP]),
     ("kvcache", "kvcache.hip", []),
     ("mw_api", "mw_api.cpp", []),
+    ("sched", "sched.cpp", []),
 ]
 SOURCES = sorted({u[1] for u in UNITS})
 

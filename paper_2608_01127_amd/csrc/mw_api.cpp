@@ -99,6 +99,13 @@ mw::Strides to_internal(const mw_strides& s) { return {s.b, s.h, s.t}; }
 
 }  // namespace
 
+namespace mw {
+int set_error(int code, const char* msg) {
+  g_err = code == MW_OK ? std::string() : std::string(msg);
+  return code;
+}
+}  // namespace mw
+
 extern "C" {
 
 const char* mw_last_error(void) { return g_err.c_str(); }

@@ -111,4 +111,8 @@ hipError_t launch_kv_copy(const uint16_t* k_src, const uint16_t* v_src, uint16_t
 hipError_t launch_kv_gather(const uint16_t* k_src, const uint16_t* v_src, Strides sk, Strides sv, uint16_t* k_dst,
                             uint16_t* v_dst, int B, int H, int L, int D, hipStream_t stream);
 
+// Record the calling thread's status message (what mw_last_error returns)
+// and return `code`; MW_OK clears it.
+int set_error(int code, const char* msg);
+
 }  // namespace mw
