@@ -156,6 +156,65 @@ def decode_shapes(mw, torch, cache, st, dev, reps=20):
     return out
 
 
+def paper_shapes(mw, torch, dev, reps=5):
+    """The paper's own 1B shapes (12 heads of width 128, 600-token chunks of 2
+    latent frames): training forward+backward over a 32-chunk window, and
+    cached attention of 8 in-flight chunks over 24/12/6 cached chunks plus a
+    300-token sink with the guidance batch of 2, inputs as [B,T,H,D] views.
+    Useful TFLOP/s, HIP events on the launch stream."""
+    import synth
+    out = {}
+    tr = synth.PAPER_1B_TRAIN
+    B, H, T, D, L = tr.B, tr.H, tr.T, tr.D, tr.chunk_len
+    g = torch.Generator(device=dev).manual_seed(6)
+    q, k, v, do = (torch.randn(B, H, T, D, device=dev, generator=g).to(torch.bfloat16) for _ in range(4))
+    o = torch.empty_like(q)
+    lse = torch.empty((B, H, T), dtype=torch.float32, device=dev)
+    ws = torch.empty(mw.mw_block_causal_attn_bwd_workspace_size(B, H, T, D), dtype=torch.uint8, device=dev)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    P = pairs_block_causal(B, H, T, L)
+    tf = timed(lambda: mw.mw_block_causal_attn_fwd(q, k, v, L, out=o, lse=lse))
+    tb = timed(lambda: mw.mw_block_causal_attn_bwd(q, k, v, o, do, lse, L, workspace=ws, dq=dq, dk=dk, dv=dv))
+    out["train"] = {"workload": tr.name, "fwd_ms": round(tf, 4), "bwd_ms": round(tb, 4),
+                    "fwd_bwd_tflops": round(14.0 * P * D / ((tf + tb) * 1e-3) / 1e12, 2)}
+    st = synth.PAPER_1B_STREAM
+    B, H, D, L, nq = st.B, st.H, st.D, st.chunk_len, st.n_queued
+    Tq = nq * st.q_len
+    sk, sv = (torch.randn(B, H, st.sink_len, D, device=dev, generator=g).to(torch.bfloat16) for _ in range(2))
+    qb, kb, vb = (torch.randn(B, Tq, H, D, device=dev, generator=g).to(torch.bfloat16) for _ in range(3))
+    qv, kv, vv = (x.transpose(1, 2) for x in (qb, kb, vb))
+    ob = torch.empty_like(qb)
+    streams = []
+    for window in (24, 12, 6):
+        cache = mw.KVCache(window + 1, B, H, L, D, device=dev)
+        kc = torch.randn(B, H, L, D, device=dev, generator=g).to(torch.bfloat16)
+        for _ in range(window):
+            mw.mw_kvcache_append(cache, kc, kc)
+        cache.set_sink(sk, sv)
+        wsb = torch.empty(max(16, mw.mw_chunk_attn_cached_workspace_size(cache, nq, st.q_len, window)),
+                          dtype=torch.uint8, device=dev)
+        tc = timed(lambda: mw.mw_chunk_attn_cached(qv, kv, vv, nq, st.q_len, cache, window=window,
+                                                   out=ob.transpose(1, 2), workspace=wsb))
+        hist = st.sink_len + window * L
+        pairs = B * H * sum(st.q_len * (hist + (j + 1) * st.q_len) for j in range(nq))
+        streams.append({"window": window, "ms": round(tc, 4), "tflops": round(4.0 * pairs * D / (tc * 1e-3) / 1e12, 2)})
+    out["stream"] = {"workload": st.name.replace("_W24_S25", ""), "B_cfg": B, "by_window": streams}
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -311,6 +370,7 @@ def main():
         "roofline": roofline,
     }
     res["decode"] = decode_shapes(mw, torch, cache, st, dev)
+    res["paper_1b"] = paper_shapes(mw, torch, dev)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     else:

@@ -85,6 +85,7 @@ class StreamShape:
     slots: int          # ring capacity in chunks
     steps: int          # rollout length (chunk steps)
     seed_base: int
+    sink_len: int = 0   # tokens of the sink anchor (0: none)
 
 
 # tiny: 4 chunks x 64 tokens, two heads of width 64
@@ -100,7 +101,16 @@ STREAM = StreamShape("stream_B1H16D128L2640_nq4_W6_S8", 1, 16, 128, 2640, 4, 264
 ROLLOUT = StreamShape("rollout_B1H16D128L2640_nq4_W6_S8_200steps", 1, 16, 128, 2640, 4, 2640,
                       6, 8, 200, 100000 * 5)
 
-TRAIN_SHAPES = {s.name: s for s in (TINY, TRAIN_D64, TRAIN_D128)}
+# The paper's own shapes (MiniWorld-1B: 12 heads of width 128; a chunk is 2
+# latent frames of a 15 x 20 latent grid = 600 tokens; Sec. 4.1, Sec. 4.3):
+# training over a 32-chunk window, and streaming with 8 in-flight chunks over a
+# 24-chunk cache plus a one-frame (300-token) sink, with the classifier-free
+# guidance batch of 2 (conditional and unconditional).
+PAPER_1B_TRAIN = TrainShape("paper1b_train_B1H12T19200D128L600", 1, 12, 19200, 128, 600, 100000 * 6)
+PAPER_1B_STREAM = StreamShape("paper1b_stream_B2H12D128L600_nq8_W24_S25_sink300", 2, 12, 128, 600, 8, 600, 24, 25,
+                              1, 100000 * 7, sink_len=300)
+
+TRAIN_SHAPES = {s.name: s for s in (TINY, TRAIN_D64, TRAIN_D128, PAPER_1B_TRAIN)}
 
 
 def training_inputs(shape: TrainShape, which=("q", "k", "v", "do")) -> dict:
