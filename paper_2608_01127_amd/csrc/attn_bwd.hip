@@ -350,9 +350,9 @@ template <int D>
 struct BwdCfg {
   static constexpr int NW_DKV = 4;
   static constexpr int NW_DQ = 4;
-  // 32-row query blocks per wave in the dQ kernel; at D = 128 two blocks do
-  // not fit the register file without spilling
-  static constexpr int RB_DQ = D == 64 ? 2 : 1;
+  // 32-row query blocks per wave in the dQ kernel (two measured no faster at
+  // D = 64 and spill at D = 128)
+  static constexpr int RB_DQ = 1;
 };
 
 template <int D>
