@@ -60,9 +60,10 @@ __global__ __launch_bounds__(256) void bwd_rowterms_kernel(BwdParams p, long lon
 // D = 128 keeps 192 registers of per-wave state (K and V fragments, dK and dV
 // accumulators) and runs one wave per SIMD with the full register file; D = 64
 // fits two waves per SIMD.
-template <int D, int NW>
+template <int D, int NW, int BM>
 __global__ __launch_bounds__(64 * NW, (D == 64 ? 8 : 4) / NW) void bwd_dkdv_kernel(BwdParams p, int n_ktiles) {
-  constexpr int BN = 32 * NW, BM = DKV_BM, NT = 64 * NW;
+  constexpr int BN = 32 * NW, NT = 64 * NW;
+  static_assert(BM % 64 == 0, "row terms are staged 64 at a time");
   constexpr int KK = D / 16, DB = D / 32;
   __shared__ __attribute__((aligned(16))) bf16_t Qs[2][BM * D];
   __shared__ __attribute__((aligned(16))) bf16_t dOs[2][BM * D];
@@ -115,8 +116,16 @@ __global__ __launch_bounds__(64 * NW, (D == 64 ? 8 : 4) / NW) void bwd_dkdv_kern
       stage_rows_direct<D, BM, NT>(Qs[b], [&](int r) { return p.q + qb_ + min(q0 + r, T - 1) * p.sq.t; }, tid);
       stage_rows_direct<D, BM, NT>(dOs[b], [&](int r) { return p.d_o + dob_ + min(q0 + r, T - 1) * p.sdo.t; }, tid);
     }
-    if (wave == 0) stage_f32x64_direct(lse_s[b], lse2_bh, q0, T, lane);
-    if (wave == 1) stage_f32x64_direct(dlt_s[b], dlt_bh, q0, T, lane);
+    // row terms of the tile: 64 fp32 per wave, LSE then Delta
+#pragma unroll
+    for (int c = wave; c < 2 * (BM / 64); c += NW) {
+      const int part = c % (BM / 64);
+      if (c < BM / 64) {
+        stage_f32x64_direct(lse_s[b] + 64 * part, lse2_bh, q0 + 64 * part, T, lane);
+      } else {
+        stage_f32x64_direct(dlt_s[b] + 64 * part, dlt_bh, q0 + 64 * part, T, lane);
+      }
+    }
   };
 
   auto step = [&](auto masked, const int q0, const int buf) {
@@ -206,9 +215,9 @@ __global__ __launch_bounds__(64 * NW, (D == 64 ? 8 : 4) / NW) void bwd_dkdv_kern
 
 // NW waves, each owning RB blocks of 32 query rows: with RB = 2 every K and V
 // fragment read from LDS feeds two MFMAs (one per row block).
-template <int D, int NW, int RB>
+template <int D, int NW, int RB, int BN>
 __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, int n_qtiles) {
-  constexpr int BM = 32 * RB * NW, BN = DQ_BN, NT = 64 * NW;
+  constexpr int BM = 32 * RB * NW, NT = 64 * NW;
   constexpr int KK = D / 16, DB = D / 32;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BN * D];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[2][BN * D];
@@ -353,11 +362,14 @@ struct BwdCfg {
   // 32-row query blocks per wave in the dQ kernel (two measured no faster at
   // D = 64 and spill at D = 128)
   static constexpr int RB_DQ = 1;
+  static constexpr int BM_DKV = 64;  // queries per step of the dK/dV kernel
+  static constexpr int BN_DQ = D == 64 ? 128 : 64;  // keys per step of the dQ kernel
 };
 
 template <int D>
 static hipError_t launch_bwd_d(const BwdParams& p, hipStream_t stream) {
   constexpr int NK = BwdCfg<D>::NW_DKV, NQ = BwdCfg<D>::NW_DQ, RQ = BwdCfg<D>::RB_DQ;
+  constexpr int BMK = BwdCfg<D>::BM_DKV, BNQ = BwdCfg<D>::BN_DQ;
   const long long rows = (long long)p.BH * p.T;
   const long long threads = rows * (D / 8);
   hipLaunchKernelGGL(bwd_rowterms_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p,
@@ -365,11 +377,11 @@ static hipError_t launch_bwd_d(const BwdParams& p, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int nkt = (p.T + 32 * NK - 1) / (32 * NK);
-  hipLaunchKernelGGL((bwd_dkdv_kernel<D, NK>), dim3(nkt * p.BH), dim3(64 * NK), 0, stream, p, nkt);
+  hipLaunchKernelGGL((bwd_dkdv_kernel<D, NK, BMK>), dim3(nkt * p.BH), dim3(64 * NK), 0, stream, p, nkt);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int nqt = (p.T + 32 * RQ * NQ - 1) / (32 * RQ * NQ);
-  hipLaunchKernelGGL((bwd_dq_kernel<D, NQ, RQ>), dim3(nqt * p.BH), dim3(64 * NQ), 0, stream, p, nqt);
+  hipLaunchKernelGGL((bwd_dq_kernel<D, NQ, RQ, BNQ>), dim3(nqt * p.BH), dim3(64 * NQ), 0, stream, p, nqt);
   return hipGetLastError();
 }
 

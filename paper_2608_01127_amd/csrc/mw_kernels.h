@@ -73,9 +73,6 @@ struct BwdParams {
   Strides sq, sk, sv, so, sdo, sdq, sdk, sdv;
 };
 
-// Tile sizes (shared with the host for grid computation).
-constexpr int DKV_BM = 64;    // queries per step in the dK/dV kernel
-constexpr int DQ_BN = 64;     // keys per step in the dQ kernel
 
 hipError_t launch_fwd_64(const FwdParams& p, bool cached, hipStream_t stream);
 hipError_t launch_fwd_128(const FwdParams& p, bool cached, hipStream_t stream);
