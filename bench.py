@@ -158,7 +158,8 @@ def decode_shapes(mw, torch, cache, st, dev, reps=20):
 
 def paper_shapes(mw, torch, dev, reps=5):
     """The paper's own 1B shapes (12 heads of width 128, 600-token chunks of 2
-    latent frames): training forward+backward over a 32-chunk window, and
+    latent frames): training forward+backward over a 32-chunk window (and the
+    same with the 0.5B model's 16 heads of width 72), and
     cached attention of 8 in-flight chunks over 24/12/6 cached chunks plus a
     300-token sink with the guidance batch of 2, inputs as [B,T,H,D] views.
     Useful TFLOP/s, HIP events on the launch stream."""
@@ -190,6 +191,20 @@ def paper_shapes(mw, torch, dev, reps=5):
     tb = timed(lambda: mw.mw_block_causal_attn_bwd(q, k, v, o, do, lse, L, workspace=ws, dq=dq, dk=dk, dv=dv))
     out["train"] = {"workload": tr.name, "fwd_ms": round(tf, 4), "bwd_ms": round(tb, 4),
                     "fwd_bwd_tflops": round(14.0 * P * D / ((tf + tb) * 1e-3) / 1e12, 2)}
+    # the 0.5B model's heads: 16 of width 72, same chunks and window
+    H5, D5 = 16, 72
+    q5, k5, v5, do5 = (torch.randn(B, H5, T, D5, device=dev, generator=g).to(torch.bfloat16) for _ in range(4))
+    o5 = torch.empty_like(q5)
+    lse5 = torch.empty((B, H5, T), dtype=torch.float32, device=dev)
+    ws5 = torch.empty(mw.mw_block_causal_attn_bwd_workspace_size(B, H5, T, D5), dtype=torch.uint8, device=dev)
+    g5 = [torch.empty_like(q5) for _ in range(3)]
+    tf5 = timed(lambda: mw.mw_block_causal_attn_fwd(q5, k5, v5, L, out=o5, lse=lse5))
+    tb5 = timed(lambda: mw.mw_block_causal_attn_bwd(q5, k5, v5, o5, do5, lse5, L, workspace=ws5, dq=g5[0], dk=g5[1],
+                                                    dv=g5[2]))
+    P5 = pairs_block_causal(B, H5, T, L)
+    out["train_05b"] = {"workload": f"paper05b_train_B{B}H{H5}T{T}D{D5}L{L}", "fwd_ms": round(tf5, 4),
+                        "bwd_ms": round(tb5, 4),
+                        "fwd_bwd_tflops": round(14.0 * P5 * D5 / ((tf5 + tb5) * 1e-3) / 1e12, 2)}
     st = synth.PAPER_1B_STREAM
     B, H, D, L, nq = st.B, st.H, st.D, st.chunk_len, st.n_queued
     Tq = nq * st.q_len

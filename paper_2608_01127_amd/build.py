@@ -31,9 +31,11 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", f"-I{os.path.j
 ILP = ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"]
 UNITS = [  # (object name, source, extra flags)
     ("attn_fwd64", "attn_fwd.hip", ["-DMW_FWD_HEAD_DIM=64"]),
+    ("attn_fwd72", "attn_fwd.hip", ["-DMW_FWD_HEAD_DIM=72"]),
     ("attn_fwd128", "attn_fwd.hip", ["-DMW_FWD_HEAD_DIM=128", *ILP]),
     ("attn_fwd128dec", "attn_fwd.hip", ["-DMW_FWD_HEAD_DIM=128", "-DMW_FWD_DECODE"]),
     ("attn_bwd64", "attn_bwd.hip", ["-DMW_BWD_HEAD_DIM=64"]),
+    ("attn_bwd72", "attn_bwd.hip", ["-DMW_BWD_HEAD_DIM=72"]),
     ("attn_bwd128", "attn_bwd.hip", ["-DMW_BWD_HEAD_DIM=128", *ILP]),
     ("kvcache", "kvcache.hip", []),
     ("mw_api", "mw_api.cpp", []),

@@ -30,14 +30,16 @@ __device__ __forceinline__ int xcd_remap_b(int bid, int n) {
 
 // Row terms of the backward pass: Delta = rowsum(dO * O) and LSE scaled to
 // base 2 (LSE * log2 e), one 16-byte chunk per thread, reduced over the row's lanes.
+// CPR lanes per row (a power of two); at D = 72 the 9 pieces of a row leave
+// lanes 9..15 of its group idle.
 template <int D>
 __global__ __launch_bounds__(256) void bwd_rowterms_kernel(BwdParams p, long long n_rows) {
-  constexpr int CPR = D / 8;  // lanes per row (8 or 16)
+  constexpr int CPR = D == 64 ? 8 : 16;
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long row = gid / CPR;
   const int c = (int)(gid % CPR);
   float acc = 0.f;
-  if (row < n_rows) {
+  if (row < n_rows && c < D / 8) {
     const long long bh = row / p.T, t = row - bh * p.T, bi = bh / p.H, hi = bh - bi * p.H;
     const u32x4 a = *reinterpret_cast<const u32x4*>(p.o + bi * p.so.b + hi * p.so.h + t * p.so.t + c * 8);
     const u32x4 b = *reinterpret_cast<const u32x4*>(p.d_o + bi * p.sdo.b + hi * p.sdo.h + t * p.sdo.t + c * 8);
@@ -61,12 +63,13 @@ __global__ __launch_bounds__(256) void bwd_rowterms_kernel(BwdParams p, long lon
 // accumulators) and runs one wave per SIMD with the full register file; D = 64
 // fits two waves per SIMD.
 template <int D, int NW, int BM>
-__global__ __launch_bounds__(64 * NW, (D == 64 ? 8 : 4) / NW) void bwd_dkdv_kernel(BwdParams p, int n_ktiles) {
+__global__ __launch_bounds__(64 * NW, (D == 128 ? 4 : 8) / NW) void bwd_dkdv_kernel(BwdParams p, int n_ktiles) {
   constexpr int BN = 32 * NW, NT = 64 * NW;
   static_assert(BM % 64 == 0, "row terms are staged 64 at a time");
-  constexpr int KK = D / 16, DB = D / 32;
-  __shared__ __attribute__((aligned(16))) bf16_t Qs[2][BM * D];
-  __shared__ __attribute__((aligned(16))) bf16_t dOs[2][BM * D];
+  constexpr int KK = (D + 15) / 16, DB = (D + 31) / 32;  // D = 72: 80 and 96 columns
+  constexpr int TE = stage_elems<D, BM, NT>();
+  __shared__ __attribute__((aligned(16))) bf16_t Qs[2][TE];
+  __shared__ __attribute__((aligned(16))) bf16_t dOs[2][TE];
   __shared__ __attribute__((aligned(16))) float lse_s[2][BM];
   __shared__ __attribute__((aligned(16))) float dlt_s[2][BM];
 
@@ -91,8 +94,13 @@ __global__ __launch_bounds__(64 * NW, (D == 64 ? 8 : 4) / NW) void bwd_dkdv_kern
     const bf16_t* va = p.v + bi * p.sv.b + hi * p.sv.h + kr * p.sv.t + 8 * (lane >> 5);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      kf[kk] = *reinterpret_cast<const bf16x8*>(ka + 16 * kk);
-      vf[kk] = *reinterpret_cast<const bf16x8*>(va + 16 * kk);
+      if (D % 16 == 0 || 16 * kk + 8 * (lane >> 5) < D) {
+        kf[kk] = *reinterpret_cast<const bf16x8*>(ka + 16 * kk);
+        vf[kk] = *reinterpret_cast<const bf16x8*>(va + 16 * kk);
+      } else {  // columns past D (D = 72): zeros
+#pragma unroll
+        for (int j = 0; j < 8; ++j) kf[kk][j] = vf[kk][j] = (__bf16)0.f;
+      }
     }
   }
   f32x16 dv[DB], dk[DB];
@@ -206,6 +214,7 @@ __global__ __launch_bounds__(64 * NW, (D == 64 ? 8 : 4) / NW) void bwd_dkdv_kern
           wv[j] = to_bf16(dv[db][4 * g + j]);
         }
         const int col = db * 32 + 8 * g + 4 * (lane >> 5);
+        if (D % 32 != 0 && col >= D) continue;  // (D = 72)
         *reinterpret_cast<bf16x4*>(dkrow + col) = wk;
         *reinterpret_cast<bf16x4*>(dvrow + col) = wv;
       }
@@ -218,9 +227,10 @@ __global__ __launch_bounds__(64 * NW, (D == 64 ? 8 : 4) / NW) void bwd_dkdv_kern
 template <int D, int NW, int RB, int BN>
 __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, int n_qtiles) {
   constexpr int BM = 32 * RB * NW, NT = 64 * NW;
-  constexpr int KK = D / 16, DB = D / 32;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BN * D];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][BN * D];
+  constexpr int KK = (D + 15) / 16, DB = (D + 31) / 32;  // D = 72: 80 and 96 columns
+  constexpr int TE = stage_elems<D, BN, NT>();
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][TE];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][TE];
 
   const int logical = xcd_remap_b(blockIdx.x, gridDim.x);
   const int bh = logical / n_qtiles;
@@ -242,8 +252,13 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
     const bf16_t* da = p.d_o + bi * p.sdo.b + hi * p.sdo.h + qc * p.sdo.t + 8 * (lane >> 5);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      qf[rb][kk] = *reinterpret_cast<const bf16x8*>(qa + 16 * kk);
-      df[rb][kk] = *reinterpret_cast<const bf16x8*>(da + 16 * kk);
+      if (D % 16 == 0 || 16 * kk + 8 * (lane >> 5) < D) {
+        qf[rb][kk] = *reinterpret_cast<const bf16x8*>(qa + 16 * kk);
+        df[rb][kk] = *reinterpret_cast<const bf16x8*>(da + 16 * kk);
+      } else {  // columns past D (D = 72): zeros
+#pragma unroll
+        for (int j = 0; j < 8; ++j) qf[rb][kk][j] = df[rb][kk][j] = (__bf16)0.f;
+      }
     }
     lse2[rb] = p.lse2[(long long)bh * T + qc];
     dlt[rb] = p.delta[(long long)bh * T + qc];
@@ -344,10 +359,12 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
+        const int col = db * 32 + 8 * g + 4 * (lane >> 5);
+        if (D % 32 != 0 && col >= D) continue;  // (D = 72)
         bf16x4 w;
 #pragma unroll
         for (int j = 0; j < 4; ++j) w[j] = to_bf16(dq[rb][db][4 * g + j] * p.scale);
-        *reinterpret_cast<bf16x4*>(row + db * 32 + 8 * g + 4 * (lane >> 5)) = w;
+        *reinterpret_cast<bf16x4*>(row + col) = w;
       }
     }
   }
@@ -371,7 +388,7 @@ static hipError_t launch_bwd_d(const BwdParams& p, hipStream_t stream) {
   constexpr int NK = BwdCfg<D>::NW_DKV, NQ = BwdCfg<D>::NW_DQ, RQ = BwdCfg<D>::RB_DQ;
   constexpr int BMK = BwdCfg<D>::BM_DKV, BNQ = BwdCfg<D>::BN_DQ;
   const long long rows = (long long)p.BH * p.T;
-  const long long threads = rows * (D / 8);
+  const long long threads = rows * (D == 64 ? 8 : 16);
   hipLaunchKernelGGL(bwd_rowterms_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p,
                      rows);
   hipError_t e = hipGetLastError();
@@ -385,15 +402,17 @@ static hipError_t launch_bwd_d(const BwdParams& p, hipStream_t stream) {
   return hipGetLastError();
 }
 
-// This file is compiled once per head dimension (MW_BWD_HEAD_DIM = 64 or 128):
+// This file is compiled once per head dimension (MW_BWD_HEAD_DIM = 64, 72 or 128):
 // the two instantiations get different instruction-scheduling options in the
 // build (each measured the faster one for its size).
 #if MW_BWD_HEAD_DIM == 64
 hipError_t launch_bwd_64(const BwdParams& p, hipStream_t stream) { return launch_bwd_d<64>(p, stream); }
+#elif MW_BWD_HEAD_DIM == 72
+hipError_t launch_bwd_72(const BwdParams& p, hipStream_t stream) { return launch_bwd_d<72>(p, stream); }
 #elif MW_BWD_HEAD_DIM == 128
 hipError_t launch_bwd_128(const BwdParams& p, hipStream_t stream) { return launch_bwd_d<128>(p, stream); }
 #else
-#error "compile with -DMW_BWD_HEAD_DIM=64 or -DMW_BWD_HEAD_DIM=128"
+#error "compile with -DMW_BWD_HEAD_DIM=64, 72 or 128"
 #endif
 
 }  // namespace mw

@@ -135,11 +135,12 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   constexpr int NWR = NW / KG;           // waves per key group (row waves)
   constexpr int BM = 32 * RB * NWR, NT = 64 * NW, KB = BN / 32;
   constexpr int BK = BN * KG;            // keys staged per step
-  constexpr int KK = D / 16;  // contraction steps over D
-  constexpr int DB = D / 32;  // 32-wide column blocks of D
-  __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][BK * D];  // K, V x double buffer
-  bf16_t(*Ks)[BK * D] = lds[0];
-  bf16_t(*Vs)[BK * D] = lds[1];
+  constexpr int KK = (D + 15) / 16;  // contraction steps over D (D = 72: the last one half zeros)
+  constexpr int DB = (D + 31) / 32;  // 32-wide column blocks of D (D = 72: the last one 8 wide)
+  constexpr int TE = stage_elems<D, BK, NT>();  // elements of one staged tile buffer
+  __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][TE];  // K, V x double buffer
+  bf16_t(*Ks)[TE] = lds[0];
+  bf16_t(*Vs)[TE] = lds[1];
 
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
   const int NS = p.n_splits;
@@ -165,9 +166,9 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
     qrow[rb] = q0 + (rw * RB + rb) * 32 + (lane & 31);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      if (qrow[rb] < p.Tq) {
+      if (qrow[rb] < p.Tq && (D % 16 == 0 || 16 * kk + 8 * (lane >> 5) < D)) {
         qf[rb][kk] = *reinterpret_cast<const bf16x8*>(p.q + qbase + qrow[rb] * p.sq.t + 16 * kk + 8 * (lane >> 5));
-      } else {
+      } else {  // rows past Tq and columns past D contribute zeros
 #pragma unroll
         for (int j = 0; j < 8; ++j) qf[rb][kk][j] = (__bf16)0.f;
       }
@@ -407,10 +408,12 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
       for (int db = 0; db < DB; ++db) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
+          const int col = db * 32 + 8 * g + 4 * (lane >> 5);
+          if (D % 32 != 0 && col >= D) continue;  // (D = 72)
           f32x4 w;
 #pragma unroll
           for (int j = 0; j < 4; ++j) w[j] = o[rb][db][4 * g + j];
-          *reinterpret_cast<f32x4*>(po + db * 32 + 8 * g + 4 * (lane >> 5)) = w;
+          *reinterpret_cast<f32x4*>(po + col) = w;
         }
       }
       if (lane < 32) {
@@ -425,10 +428,12 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
       for (int db = 0; db < DB; ++db) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
+          const int col = db * 32 + 8 * g + 4 * (lane >> 5);
+          if (D % 32 != 0 && col >= D) continue;  // (D = 72)
           bf16x4 w;
 #pragma unroll
           for (int j = 0; j < 4; ++j) w[j] = to_bf16(o[rb][db][4 * g + j] * inv);
-          *reinterpret_cast<bf16x4*>(orow + db * 32 + 8 * g + 4 * (lane >> 5)) = w;
+          *reinterpret_cast<bf16x4*>(orow + col) = w;
         }
       }
       if (p.lse != nullptr && lane < 32) {
@@ -450,6 +455,8 @@ struct FwdCfg {
   static constexpr int RB = D == 64 ? 2 : 1;  // 32-row query blocks per wave
   static constexpr int KG = 1;
 };
+// (D = 72, the 0.5B model's head width, runs the D = 128 arrangement: its
+// wider accumulators leave no room for two row blocks per wave.)
 
 // Cached attention with few queued rows (a short chunk over a long window) is
 // bound by streaming the window from HBM.  Eight waves split into key groups
@@ -539,7 +546,7 @@ static hipError_t launch_fwd_cfg(const FwdParams& p, hipStream_t stream) {
   return launch_fwd_tpl<D, CACHED, C::NW, C::BN, C::RB, C::KG>(p, stream);
 }
 
-// This file is compiled once per head dimension (MW_FWD_HEAD_DIM = 64 or 128),
+// This file is compiled once per head dimension (MW_FWD_HEAD_DIM = 64, 72 or 128),
 // with the instruction-scheduling option measured faster for each; the merge
 // kernel and the split heuristic live in the D = 128 unit.  The key-group
 // configurations for few queued rows are compiled in a unit of their own
@@ -547,6 +554,10 @@ static hipError_t launch_fwd_cfg(const FwdParams& p, hipStream_t stream) {
 #if MW_FWD_HEAD_DIM == 64 && !defined(MW_FWD_DECODE)
 hipError_t launch_fwd_64(const FwdParams& p, bool cached, hipStream_t stream) {
   return cached ? launch_fwd_cfg<64, true>(p, stream) : launch_fwd_cfg<64, false>(p, stream);
+}
+#elif MW_FWD_HEAD_DIM == 72 && !defined(MW_FWD_DECODE)
+hipError_t launch_fwd_72(const FwdParams& p, bool cached, hipStream_t stream) {
+  return cached ? launch_fwd_cfg<72, true>(p, stream) : launch_fwd_cfg<72, false>(p, stream);
 }
 #elif MW_FWD_HEAD_DIM == 128 && !defined(MW_FWD_DECODE)
 hipError_t launch_fwd_128(const FwdParams& p, bool cached, hipStream_t stream) {
@@ -565,7 +576,7 @@ hipError_t launch_fwd_decode_128(const FwdParams& p, int bm, hipStream_t stream)
   return launch_fwd_tpl<128, true, C::NW, C::BN, C::RB, C::KG>(p, stream);
 }
 #else
-#error "compile with -DMW_FWD_HEAD_DIM=64 or -DMW_FWD_HEAD_DIM=128 (optionally -DMW_FWD_DECODE)"
+#error "compile with -DMW_FWD_HEAD_DIM=64, 72 or 128 (128 optionally with -DMW_FWD_DECODE)"
 #endif
 
 #if MW_FWD_HEAD_DIM == 128 && !defined(MW_FWD_DECODE)
@@ -574,6 +585,7 @@ FwdChoice fwd_choice(int D, bool cached, int Tq) {
   if (cached && D == 128 && Tq <= 64) return {64, 1};
   if (cached && D == 128 && Tq <= 128) return {128, 1};
   if (D == 64) return {32 * FwdCfg<64>::RB * FwdCfg<64>::NW, 3};
+  if (D == 72) return {32 * FwdCfg<72>::RB * FwdCfg<72>::NW, 2};
   return {32 * FwdCfg<128>::RB * FwdCfg<128>::NW, 2};
 }
 

@@ -45,7 +45,8 @@ int check_ptrs(const char* fn, std::initializer_list<std::pair<const char*, cons
 int check_train_dims(const char* fn, int B, int H, int T, int D, int chunk_len, float scale) {
   if (B < 1 || H < 1 || T < 1 || chunk_len < 1)
     return fail(MW_EINVAL, "%s: B, H, T and chunk_len must be >= 1 (got %d, %d, %d, %d)", fn, B, H, T, chunk_len);
-  if (D != 64 && D != 128) return fail(MW_EUNSUPPORTED, "%s: head dimension %d is not supported (64 or 128)", fn, D);
+  if (D != 64 && D != 72 && D != 128)
+    return fail(MW_EUNSUPPORTED, "%s: head dimension %d is not supported (64, 72 or 128)", fn, D);
   if (T > kMaxT) return fail(MW_EUNSUPPORTED, "%s: T = %d exceeds %d", fn, T, kMaxT);
   if ((long long)B * H > (1LL << 24)) return fail(MW_EUNSUPPORTED, "%s: B*H too large", fn);
   if (!(scale > 0.f) || !std::isfinite(scale)) return fail(MW_EINVAL, "%s: scale must be finite and > 0", fn);
@@ -218,7 +219,7 @@ int mw_block_causal_attn_bwd_strided(const void* q, const void* k, const void* v
   p.sdk = sv[6];
   p.sdv = sv[7];
   hipStream_t hs = static_cast<hipStream_t>(stream);
-  return hip_status(fn, D == 64 ? mw::launch_bwd_64(p, hs) : mw::launch_bwd_128(p, hs));
+  return hip_status(fn, D == 64 ? mw::launch_bwd_64(p, hs) : (D == 72 ? mw::launch_bwd_72(p, hs) : mw::launch_bwd_128(p, hs)));
 }
 
 int mw_block_causal_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* d_o,
@@ -235,7 +236,8 @@ int mw_kvcache_init(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, i
   if (st) return st;
   if (S < 1 || B < 1 || H < 1 || L < 1)
     return fail(MW_EINVAL, "%s: S, B, H and L must be >= 1 (got %d, %d, %d, %d)", fn, S, B, H, L);
-  if (D != 64 && D != 128) return fail(MW_EUNSUPPORTED, "%s: head dimension %d is not supported (64 or 128)", fn, D);
+  if (D != 64 && D != 72 && D != 128)
+    return fail(MW_EUNSUPPORTED, "%s: head dimension %d is not supported (64, 72 or 128)", fn, D);
   if ((long long)L * S > kMaxT) return fail(MW_EUNSUPPORTED, "%s: S*L exceeds %d tokens", fn, kMaxT);
   c->k_slots = k_slots;
   c->v_slots = v_slots;
@@ -255,7 +257,7 @@ int mw_kvcache_init(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, i
 static int check_cache(const char* fn, const mw_kvcache* c) {
   if (c == nullptr) return fail(MW_EINVAL, "%s: cache is NULL", fn);
   if (c->k_slots == nullptr || c->v_slots == nullptr || c->S < 1 || c->B < 1 || c->H < 1 || c->L < 1 ||
-      (c->D != 64 && c->D != 128) || c->tail < 0 || c->head < c->tail || c->head - c->tail > c->S ||
+      (c->D != 64 && c->D != 72 && c->D != 128) || c->tail < 0 || c->head < c->tail || c->head - c->tail > c->S ||
       c->sink_len < 0 || (c->sink_len > 0 && (c->k_sink == nullptr || c->v_sink == nullptr)))
     return fail(MW_EINVAL, "%s: cache descriptor is not initialised or is corrupt", fn);
   return MW_OK;
@@ -374,7 +376,7 @@ static long long window_chunks(const mw_kvcache* c, int window) {
 }
 
 size_t mw_chunk_attn_cached_workspace_size(const mw_kvcache* c, int n_queued, int q_len, int window) {
-  if (c == nullptr || n_queued < 1 || q_len < 1 || c->L < 1 || (c->D != 64 && c->D != 128)) return 0;
+  if (c == nullptr || n_queued < 1 || q_len < 1 || c->L < 1 || (c->D != 64 && c->D != 72 && c->D != 128)) return 0;
   const long long w = window_chunks(c, window);
   const long long tq = (long long)n_queued * q_len;
   const long long tk = c->sink_len + w * c->L + tq;

@@ -69,15 +69,25 @@ __device__ __forceinline__ bf16x8 pack8(const f32x16& c, int t) {
 //   - row reads: lane l reads 16 bytes of row l%32 (MFMA A/B operands);
 //   - transposing reads: 8 consecutive rows x 64 bytes per instruction.
 // ---------------------------------------------------------------------------
+//
+// D = 72 (nine slots, not a power of two) keeps rows dense and unswizzled:
+// rows 144 bytes (36 banks) apart already put 16 consecutive rows on disjoint
+// banks.  Its MFMA steps run over 80 (QK^T) and 96 (PV) columns; the columns
+// past 72 read the next row (or the slack after the tile) and meet zeros in
+// the register operand or land in output columns that are never stored.
 template <int D>
 struct Tile {
+  static_assert(D == 64 || D == 72 || D == 128, "head dimension");
   static constexpr int SLOTS = D / 8;  // 16-byte slots per row
   __device__ __forceinline__ static int swz(int row) {
     if constexpr (D == 128) {
       return 4 * (row & 3) + ((row >> 2) & 3);
-    } else {
+    } else if constexpr (D == 64) {
       const int u = row >> 1;
       return 4 * (u & 1) + ((u >> 1) & 3);
+    } else {
+      (void)row;
+      return 0;
     }
   }
   // element offset of (row, col); col % 4 must be 0 for 8-byte and col % 8 for 16-byte access
@@ -144,14 +154,34 @@ __device__ __forceinline__ void dma_lds_4(const void* src, MW_LDS void* wave_dst
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(base) : "m0", "memory");
 }
 
+// Pieces of a ROWS x D tile staged by NT threads: whole rounds of NT, the last
+// one partial when ROWS * D / 8 is not a multiple of NT (D = 72).  Pieces past
+// the tile fetch row 0 again and land in the slack that follows the tile, so
+// an LDS tile buffer holds stage_elems() elements.
+template <int D, int ROWS, int NT>
+struct StagePlan {
+  static constexpr int SLOTS = D / 8;
+  static constexpr int PIECES = ROWS * SLOTS;
+  static constexpr int ROUNDS = (PIECES + NT - 1) / NT;
+  static constexpr int ELEMS = ROUNDS * NT * 8 > ROWS * D + 32 ? ROUNDS * NT * 8 : ROWS * D + 32;
+  static_assert(PIECES % NT == 0 || D == 72, "only D = 72 stages a partial round");
+  // at D = 72 the last row's reads run 24 elements past the tile into the
+  // slack, which the partial round's extra pieces fill with (finite) data
+  static_assert(D != 72 || PIECES % NT != 0, "D = 72 needs a partial last round to fill the slack");
+};
+template <int D, int ROWS, int NT>
+constexpr int stage_elems() {
+  return D == 72 ? StagePlan<D, ROWS, NT>::ELEMS : ROWS * D;
+}
+
 template <int D, int ROWS, int NT, typename RowPtr>
 __device__ __forceinline__ void stage_rows_direct(bf16_t* lds_tile, RowPtr row_ptr, int tid) {
-  constexpr int SLOTS = D / 8;
-  constexpr int ROUNDS = ROWS * SLOTS / NT;
-  static_assert(ROWS * SLOTS % NT == 0, "tile must be a whole number of NT-chunk rounds");
+  using SP = StagePlan<D, ROWS, NT>;
+  constexpr int SLOTS = SP::SLOTS;
 #pragma unroll
-  for (int it = 0; it < ROUNDS; ++it) {
-    const int ci = it * NT + tid;
+  for (int it = 0; it < SP::ROUNDS; ++it) {
+    const int ci0 = it * NT + tid;
+    const int ci = (SP::PIECES % NT == 0 || ci0 < SP::PIECES) ? ci0 : 0;  // past the tile: row 0 again, into the slack
     const int row = ci / SLOTS, ps = ci % SLOTS;
     const int ls = ps ^ Tile<D>::swz(row);
     const bf16_t* src = row_ptr(row) + ls * 8;
@@ -176,12 +206,13 @@ __device__ __forceinline__ void dma_lds_16_s(const void* sbase, unsigned voff, M
 template <int D, int ROWS, int NT>
 struct RowOffsets {
   static constexpr int SLOTS = D / 8;
-  static constexpr int ROUNDS = ROWS * SLOTS / NT;
+  static constexpr int ROUNDS = StagePlan<D, ROWS, NT>::ROUNDS;
   unsigned off[ROUNDS];
   __device__ __forceinline__ RowOffsets(long long row_stride, int tid) {
 #pragma unroll
     for (int it = 0; it < ROUNDS; ++it) {
-      const int ci = it * NT + tid;
+      const int ci0 = it * NT + tid;
+      const int ci = (StagePlan<D, ROWS, NT>::PIECES % NT == 0 || ci0 < StagePlan<D, ROWS, NT>::PIECES) ? ci0 : 0;
       const int row = ci / SLOTS, ps = ci % SLOTS;
       const int ls = ps ^ Tile<D>::swz(row);
       off[it] = (unsigned)((long long)row * row_stride * 2 + ls * 16);
@@ -210,12 +241,12 @@ struct RowPair {
 };
 template <int D, int ROWS, int NT, typename RowSrc>
 __device__ __forceinline__ void stage_kv_rows_direct(bf16_t* k_tile, bf16_t* v_tile, RowSrc row_src, int tid) {
-  constexpr int SLOTS = D / 8;
-  constexpr int ROUNDS = ROWS * SLOTS / NT;
-  static_assert(ROWS * SLOTS % NT == 0, "tile must be a whole number of NT-chunk rounds");
+  using SP = StagePlan<D, ROWS, NT>;
+  constexpr int SLOTS = SP::SLOTS;
 #pragma unroll
-  for (int it = 0; it < ROUNDS; ++it) {
-    const int ci = it * NT + tid;
+  for (int it = 0; it < SP::ROUNDS; ++it) {
+    const int ci0 = it * NT + tid;
+    const int ci = (SP::PIECES % NT == 0 || ci0 < SP::PIECES) ? ci0 : 0;  // past the tile: row 0 again, into the slack
     const int row = ci / SLOTS, ps = ci % SLOTS;
     const int ls = ps ^ Tile<D>::swz(row);
     const RowPair src = row_src(row);

@@ -75,11 +75,13 @@ struct BwdParams {
 
 
 hipError_t launch_fwd_64(const FwdParams& p, bool cached, hipStream_t stream);
+hipError_t launch_fwd_72(const FwdParams& p, bool cached, hipStream_t stream);
 hipError_t launch_fwd_128(const FwdParams& p, bool cached, hipStream_t stream);
 // cached attention at D = 128 with `bm` (64 or 128) query rows per workgroup
 hipError_t launch_fwd_decode_128(const FwdParams& p, int bm, hipStream_t stream);
 inline hipError_t launch_fwd(const FwdParams& p, int D, bool cached, hipStream_t stream) {
-  return D == 64 ? launch_fwd_64(p, cached, stream) : launch_fwd_128(p, cached, stream);
+  return D == 64 ? launch_fwd_64(p, cached, stream)
+                 : (D == 72 ? launch_fwd_72(p, cached, stream) : launch_fwd_128(p, cached, stream));
 }
 // Query rows per workgroup and resident workgroups per CU of the tile
 // configuration the forward launcher picks for a shape.
@@ -93,6 +95,7 @@ FwdChoice fwd_choice(int D, bool cached, int Tq);
 int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes);
 size_t fwd_split_bytes(int D, int BH, int Tq, int n_splits);
 hipError_t launch_bwd_64(const BwdParams& p, hipStream_t stream);
+hipError_t launch_bwd_72(const BwdParams& p, hipStream_t stream);
 hipError_t launch_bwd_128(const BwdParams& p, hipStream_t stream);
 // cos/sin of the re-shift angle of each rope pair
 struct RopeTable {

@@ -86,3 +86,31 @@ def test_paper_1b_streaming_cfg_batch(mw, window):
     go = to_f64(o.contiguous())
     for b, h in heads:
         assert_close(f"o b{b} h{h}", go[b, h], ro[b, h])
+
+
+def test_paper_05b_training_d72(mw):
+    """MiniWorld-0.5B's heads (16 of width 72 = 1152 / 16) over 600-token chunks: two heads in
+    full (every row and gradient) and sampled rows of all heads, forward and backward."""
+    import torch
+    B, H, T, D, L = 1, 16, 4800, 72, 600
+    print(f"[case] paper 0.5B training B{B} H{H} T{T} D{D} L{L}", flush=True)
+    bits = {n: synth.normal_bf16((B, H, T, D), 8100 + i) for i, n in enumerate(("q", "k", "v", "do"))}
+    q, k, v, do = (to_gpu(bits[n]) for n in ("q", "k", "v", "do"))
+    o, lse = mw.mw_block_causal_attn_fwd(q, k, v, L)
+    dq, dk, dv = mw.mw_block_causal_attn_bwd(q, k, v, o, do, lse, L)
+    torch.cuda.synchronize()
+    g = {"o": to_f64(o), "lse": to_f64(lse), "dq": to_f64(dq), "dk": to_f64(dk), "dv": to_f64(dv)}
+    for h in (0, 15):
+        sel = lambda x: x[:, h:h + 1]
+        qf, kf, vf, dof = (f64(sel(bits[n])) for n in ("q", "k", "v", "do"))
+        ro, rl = oracle.block_causal_attn_fwd(qf, kf, vf, L)
+        assert_close(f"o h{h}", g["o"][:, h:h + 1], ro)
+        assert_close(f"lse h{h}", g["lse"][:, h:h + 1], rl, max_abs=2e-3, mean_abs=2e-4)
+        rdq, rdk, rdv = oracle.block_causal_attn_bwd(qf, kf, vf, dof, L)
+        for name, ref in (("dq", rdq), ("dk", rdk), ("dv", rdv)):
+            assert_close(f"{name} h{h}", g[name][:, h:h + 1], ref)
+    rows = np.array([0, 599, 600, 2999, 4799])
+    qa, ka, va = (f64(bits[n]) for n in ("q", "k", "v"))
+    for h in range(H):
+        ro, rl = oracle.block_causal_attn_fwd_rows(qa, ka, va, L, 0, h, rows)
+        assert_close(f"o rows h{h}", g["o"][0, h, rows], ro)

@@ -36,6 +36,9 @@ SMALL = [
     (1, 2, 130, 64, 1000),   # chunk longer than the sequence
     (1, 1, 1, 64, 1),        # single token
     (1, 1, 77, 128, 13),     # everything smaller than one tile
+    (1, 2, 700, 72, 96),     # D=72 (the 0.5B model's head width): padded MFMA steps, ragged tail
+    (2, 1, 300, 72, 300),    # D=72, one chunk
+    (1, 1, 45, 72, 7),       # D=72, smaller than one tile
 ]
 
 
