@@ -30,6 +30,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA
 
 
 def pairs_block_causal(B, H, T, L):
@@ -230,6 +231,134 @@ def paper_shapes(mw, torch, dev, reps=5):
     return out
 
 
+def fp8_stream(mw, torch, dev, st, reps=10):
+    """The e4m3 inference variant on the streaming shape (B1 H16 D128, 4 in-flight
+    chunks of 2640 tokens over a 6-chunk window of an 8-slot ring): per step,
+    quantize the queued chunks' Q, K, V (bf16 -> e4m3), commit one chunk
+    (quantize-on-commit), evict to the window, and run the e4m3 cached attention.
+    Also the cache-bound decode shapes (one queued chunk of 64 / 128 / 256 tokens
+    over the full window, Infinity Cache flushed before each call; algorithmic
+    bytes = e4m3 window K and V + e4m3 Q, K_new, V_new + bf16 O), and the paper's
+    1B streaming shape (CFG batch 2, 8 in-flight 600-token chunks, 300-token sink)
+    over 24 / 12 / 6 cached chunks.  HIP events on the launch stream."""
+    import synth
+    B, H, D, L, nq, ql, W = st.B, st.H, st.D, st.chunk_len, st.n_queued, st.q_len, st.window
+    sc = 5.0 / 448.0   # per-tensor scale for unit-variance activations
+    g = torch.Generator(device=dev).manual_seed(8)
+    cache = mw.KVCache(st.slots, B, H, L, D, device=dev, fp8=True, k_scale=sc, v_scale=sc)
+    kc = torch.randn(B, H, L, D, device=dev, generator=g).to(torch.bfloat16)
+    vc = torch.randn(B, H, L, D, device=dev, generator=g).to(torch.bfloat16)
+    for _ in range(W):
+        mw.mw_kvcache_append(cache, kc, vc)
+    Tq = nq * ql
+    qb, kb, vb = (torch.randn(B, H, Tq, D, device=dev, generator=g).to(torch.bfloat16) for _ in range(3))
+    q8, k8, v8 = (torch.empty((B, H, Tq, D), dtype=torch.uint8, device=dev) for _ in range(3))
+    o = torch.empty_like(qb)
+    ws = torch.empty(max(16, mw.mw_chunk_attn_cached_workspace_size(cache, nq, ql, W)), dtype=torch.uint8, device=dev)
+
+    def ev():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record()
+        return e
+
+    ph = {"quantize_qkv": 0.0, "append": 0.0, "cached": 0.0}
+
+    def step(rec):
+        e0 = ev()
+        for x, y in ((qb, q8), (kb, k8), (vb, v8)):
+            mw.mw_quantize_fp8(x, sc, out=y)
+        e1 = ev()
+        mw.mw_kvcache_append(cache, kc, vc)
+        e2 = ev()
+        mw.mw_kvcache_evict(cache, cache.live - W)
+        e3 = ev()
+        mw.mw_chunk_attn_cached_fp8(q8, k8, v8, nq, ql, cache, sc, window=W, out=o, workspace=ws)
+        e4 = ev()
+        if rec is not None:
+            rec.append((e0, e1, e2, e3, e4))
+
+    for _ in range(3):
+        step(None)
+    torch.cuda.synchronize()
+    recs = []
+    for _ in range(reps):
+        step(recs)
+    torch.cuda.synchronize()
+    for e in recs:
+        ph["quantize_qkv"] += e[0].elapsed_time(e[1]) / reps
+        ph["append"] += e[1].elapsed_time(e[2]) / reps
+        ph["cached"] += e[3].elapsed_time(e[4]) / reps
+    step_ms = sum(e[0].elapsed_time(e[4]) for e in recs) / reps
+    F = 4.0 * pairs_cached(B, H, W, L, nq, ql, causal=True) * D
+    n_el = B * H * Tq * D
+    out = {"workload": st.name + "_e4m3", "dtype": "e4m3 (fp32 accumulate)", "scale": sc,
+           "step_ms": round(step_ms, 4),
+           "phases_ms": {k: round(v, 4) for k, v in ph.items()},
+           "cached_tflops": round(F / (ph["cached"] * 1e-3) / 1e12, 2),
+           "cached_frac_fp8_peak": round(F / (ph["cached"] * 1e-3) / 1e12 / PEAK_FP8_TFLOPS, 4),
+           "step_tflops": round(F / (step_ms * 1e-3) / 1e12, 2),
+           "quantize_qkv_gbs": round(3 * n_el * 3 / (ph["quantize_qkv"] * 1e-3) / 1e9, 1),
+           "append_gbs": round(2 * B * H * L * D * 3 / (ph["append"] * 1e-3) / 1e9, 1)}
+    # decode shapes
+    flush = torch.ones(128 << 20, dtype=torch.float32, device=dev)
+    dec = []
+    for dq in (64, 128, 256):
+        q1, k1, v1 = (torch.randint(0, 120, (B, H, dq, D), dtype=torch.uint8, device=dev, generator=g)
+                      for _ in range(3))
+        o1 = torch.empty((B, H, dq, D), dtype=torch.bfloat16, device=dev)
+        ws1 = torch.empty(max(16, mw.mw_chunk_attn_cached_workspace_size(cache, 1, dq, W)), dtype=torch.uint8,
+                          device=dev)
+        run = lambda: mw.mw_chunk_attn_cached_fp8(q1, k1, v1, 1, dq, cache, sc, window=W, out=o1, workspace=ws1)
+        for _ in range(3):
+            run()
+        tot = 0.0
+        for _ in range(reps):
+            flush.sum()
+            e0 = ev()
+            run()
+            e1 = ev()
+            torch.cuda.synchronize()
+            tot += e0.elapsed_time(e1)
+        ms = tot / reps
+        nbytes = 2 * W * B * H * L * D + 3 * B * H * dq * D + B * H * dq * D * 2
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        dec.append({"q_len": dq, "us": round(ms * 1e3, 2), "gbs": round(gbs, 1),
+                    "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4), "bytes": nbytes})
+    out["decode"] = dec
+    # the paper's 1B streaming shape
+    ps = synth.PAPER_1B_STREAM
+    B, H, D, L, nq = ps.B, ps.H, ps.D, ps.chunk_len, ps.n_queued
+    Tq = nq * ps.q_len
+    s8 = [torch.randint(0, 120, (B, H, ps.sink_len, D), dtype=torch.uint8, device=dev, generator=g) for _ in range(2)]
+    x8 = [torch.randint(0, 120, (B, H, Tq, D), dtype=torch.uint8, device=dev, generator=g) for _ in range(3)]
+    ob = torch.empty((B, Tq, H, D), dtype=torch.bfloat16, device=dev)
+    kc = torch.randn(B, H, L, D, device=dev, generator=g).to(torch.bfloat16)
+    by = []
+    for window in (24, 12, 6):
+        c8 = mw.KVCache(window + 1, B, H, L, D, device=dev, fp8=True, k_scale=sc, v_scale=sc)
+        for _ in range(window):
+            mw.mw_kvcache_append(c8, kc, kc)
+        c8.set_sink(*s8)
+        wsb = torch.empty(max(16, mw.mw_chunk_attn_cached_workspace_size(c8, nq, ps.q_len, window)),
+                          dtype=torch.uint8, device=dev)
+        fn = lambda: mw.mw_chunk_attn_cached_fp8(*x8, nq, ps.q_len, c8, sc, window=window, out=ob.transpose(1, 2),
+                                                 workspace=wsb)
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0 = ev()
+        for _ in range(reps):
+            fn()
+        e1 = ev()
+        torch.cuda.synchronize()
+        tc = e0.elapsed_time(e1) / reps
+        hist = ps.sink_len + window * L
+        pairs = B * H * sum(ps.q_len * (hist + (j + 1) * ps.q_len) for j in range(nq))
+        by.append({"window": window, "ms": round(tc, 4), "tflops": round(4.0 * pairs * D / (tc * 1e-3) / 1e12, 2)})
+    out["paper_1b_stream"] = {"workload": ps.name.replace("_W24_S25", "") + "_e4m3", "B_cfg": B, "by_window": by}
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -386,6 +515,7 @@ def main():
     }
     res["decode"] = decode_shapes(mw, torch, cache, st, dev)
     res["paper_1b"] = paper_shapes(mw, torch, dev)
+    res["fp8_stream"] = fp8_stream(mw, torch, dev, st)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     else:

@@ -160,6 +160,9 @@ typedef struct {
   const void* k_sink;  /* sink anchor (see mw_kvcache_set_sink), or NULL */
   const void* v_sink;
   int sink_len;        /* sink tokens (0: no sink) */
+  int elem_bytes;      /* 2: bf16 slots (mw_kvcache_init); 1: e4m3 slots (mw_kvcache_init_fp8) */
+  float k_scale;       /* e4m3 slots: key value = code * k_scale (1 for bf16 slots) */
+  float v_scale;       /* e4m3 slots: value value = code * v_scale (1 for bf16 slots) */
 } mw_kvcache;
 
 /* Initialise an empty ring over k_slots/v_slots (bf16 [S,B,H,L,D]), without a
@@ -268,6 +271,66 @@ int mw_chunk_attn_cached_strided(const void* q, const void* k_new, const void* v
                                  int n_queued, int q_len, const mw_kvcache* c, int window, int flags,
                                  void* o, float* lse, float scale, void* workspace, size_t workspace_bytes,
                                  const mw_strides* strides, mw_stream_t stream);
+
+/* ------------------------------------------------------------------------
+ * fp8 inference variant: quantized cached chunk attention.
+ *
+ * The paper names quantization as a way to cut the cost of streaming
+ * inference (Sec. 6, "Efficient deployment").  This variant stores the
+ * committed window, the sink and the queued chunks' Q, K, V as OCP e4m3
+ * (1 sign, 4 exponent bits with bias 7, 3 mantissa bits; finite range
+ * +-448; no infinities) with per-tensor scales, value = code * scale, and
+ * computes the cached chunk attention of Sec. 3.5 (same key sequence and
+ * visibility rules as mw_chunk_attn_cached) with both products in e4m3 on the
+ * matrix cores: scores and softmax statistics in fp32, the probabilities
+ * (at most 2^8 by construction) rounded to e4m3 (nearest even) before the PV
+ * product, O normalised in fp32 and stored as bf16.  Head dimension 128 only.
+ * ---------------------------------------------------------------------- */
+
+/* Quantize a bf16 [B, H, T, D] view (strides as in mw_strides; NULL =
+ * contiguous) into a contiguous e4m3 [B, H, T, D] tensor y (1 byte per
+ * element): code = RNE_e4m3(clamp(fl32(x * fl32(1 / scale)), -448, 448)),
+ * where fl32 is fp32 rounding (nearest even) and 1/scale is computed on the
+ * host in fp32.  x must be finite (non-finite values saturate).  D: a multiple
+ * of 8 (64, 72 or 128).  y must be 16-byte aligned and must not overlap x.
+ * Errors: MW_EINVAL (null, sizes < 1, scale not finite and > 0), MW_EALIGN,
+ * MW_EUNSUPPORTED (D), MW_EHIP. */
+int mw_quantize_fp8(const void* x, const mw_strides* x_strides, void* y, int B, int H, int T, int D,
+                    float scale, mw_stream_t stream);
+
+/* Initialise an empty ring whose slots hold e4m3 K and V: k_slots, v_slots are
+ * e4m3 [S, B, H, L, D] (1 byte per element), with per-tensor scales k_scale,
+ * v_scale (> 0, finite) fixed for the cache's lifetime.  mw_kvcache_append and
+ * mw_kvcache_append_strided take bf16 chunks and quantize them into the slot
+ * with these scales (mw_quantize_fp8's rounding).  The sink
+ * (mw_kvcache_set_sink) must be e4m3 [B, H, sink_len, D] quantized with the
+ * same scales.  mw_kvcache_rope_shift is not available for e4m3 slots
+ * (MW_EUNSUPPORTED): rotating 8-bit keys in place would re-round them at every
+ * shift.  mw_chunk_attn_cached rejects an e4m3 cache (MW_EINVAL); use
+ * mw_chunk_attn_cached_fp8.  Eviction, live counts and slot numbering are
+ * those of the bf16 ring.  No device work.
+ * Errors: MW_EINVAL (null, sizes < 1, bad scales), MW_EALIGN,
+ * MW_EUNSUPPORTED (D other than 128). */
+int mw_kvcache_init_fp8(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, int H, int L, int D,
+                        float k_scale, float v_scale);
+
+/* Cached chunk attention over an e4m3 cache (mw_kvcache_init_fp8).
+ * q8, k8_new, v8_new : e4m3 [B, H, n_queued*q_len, 128], contiguous; q8
+ *                      quantized with q_scale, k8_new and v8_new with the
+ *                      cache's k_scale and v_scale (mw_quantize_fp8)
+ * o                  : bf16 [B, H, n_queued*q_len, 128] view (o_strides, NULL =
+ *                      contiguous); lse: fp32 [B, H, n_queued*q_len] or NULL
+ * scale              : softmax scale applied to the dequantized scores
+ * The scores are (q8 . k8) * q_scale * k_scale * scale, the output
+ * sum_j p_j v8_j * v_scale / sum_j p_j.  window, flags, workspace (size from
+ * mw_chunk_attn_cached_workspace_size on the e4m3 cache) as in
+ * mw_chunk_attn_cached.
+ * Errors: as mw_chunk_attn_cached, plus MW_EINVAL for a bf16 cache or
+ * q_scale not finite and > 0. */
+int mw_chunk_attn_cached_fp8(const void* q8, const void* k8_new, const void* v8_new, int n_queued, int q_len,
+                             const mw_kvcache* c, int window, int flags, void* o, float* lse, float scale,
+                             float q_scale, void* workspace, size_t workspace_bytes, const mw_strides* o_strides,
+                             mw_stream_t stream);
 
 /* ------------------------------------------------------------------------
  * Pipelined denoising schedule (Sec. 3.5, "Pipelined Denoising" and the

@@ -15,12 +15,16 @@ Contents
   (paper Sec. 3.5, "Structured Rolling KV Cache").
 - rope_rotate (attention.py): rotary position embedding on a band of head
   dimensions, used for the re-shifting of cached keys (paper Sec. 3.5).
+- fp8.py: OCP E4M3 encoding, decoding and per-tensor quantization, the
+  number format of the fp8 inference variant (the quantization direction the
+  paper names in Sec. 6); the fp8 attention itself is checked against
+  cached_chunk_attn on the dequantized values.
 - scheduler.py: the pipelined asynchronous denoiser simulated tick by tick
   (paper Sec. 3.5, Eq. 4, Eq. 6, Eq. 7): which chunks are in flight, their
   timesteps and updates, commits, evictions and re-shifts.
 
 Parity status: every function here is pinned by the not-gpu tests in
-tests/test_oracle.py (library special cases, closed forms, invariants,
+tests/test_oracle.py, tests/test_fp8_oracle.py and tests/test_scheduler.py (library special cases, closed forms, invariants,
 finite differences, brute force); none is "parity unpinned".
 """
 from .attention import (  # noqa: F401
@@ -38,4 +42,5 @@ from .attention import (  # noqa: F401
     QUEUED_ISOLATED,
 )
 from .ring import RingModel, RingError  # noqa: F401
+from .fp8 import E4M3_MAX, e4m3_decode, e4m3_encode, quantize_fp8, dequantize_fp8  # noqa: F401
 from .scheduler import simulate as simulate_pipeline, shifted_tau, tau_level  # noqa: F401

@@ -3,7 +3,8 @@
 Python face of libmw.so (C ABI in include/mw.h): block-causal multi-head
 attention forward/backward (paper Sec. 3.2), the ring-buffered rolling KV
 cache and cached attention of queued in-flight chunks, and the host plan of
-the pipelined denoiser (paper Sec. 3.5).
+the pipelined denoiser (paper Sec. 3.5), and an fp8 (e4m3) variant of the
+cached attention for inference (the quantization direction of Sec. 6).
 The functions carry the C entry points' names; all compute runs in the HIP
 kernels of csrc/.
 """
@@ -26,6 +27,7 @@ from ._lib import (  # noqa: F401
     mw_block_causal_attn_bwd_workspace_size,
     mw_block_causal_attn_fwd,
     mw_chunk_attn_cached,
+    mw_chunk_attn_cached_fp8,
     mw_chunk_attn_cached_workspace_size,
     mw_kvcache,
     mw_kvcache_append,
@@ -34,6 +36,7 @@ from ._lib import (  # noqa: F401
     mw_kvcache_set_sink,
     mw_rope,
     mw_kvcache_slot_of,
+    mw_quantize_fp8,
     mw_sched_config,
     mw_sched_num_ticks,
     mw_sched_plan,

@@ -40,7 +40,8 @@ class mw_kvcache(ctypes.Structure):
     _fields_ = [("k_slots", ctypes.c_void_p), ("v_slots", ctypes.c_void_p),
                 ("S", ctypes.c_int), ("B", ctypes.c_int), ("H", ctypes.c_int), ("L", ctypes.c_int),
                 ("D", ctypes.c_int), ("head", ctypes.c_int64), ("tail", ctypes.c_int64),
-                ("k_sink", ctypes.c_void_p), ("v_sink", ctypes.c_void_p), ("sink_len", ctypes.c_int)]
+                ("k_sink", ctypes.c_void_p), ("v_sink", ctypes.c_void_p), ("sink_len", ctypes.c_int),
+                ("elem_bytes", ctypes.c_int), ("k_scale", ctypes.c_float), ("v_scale", ctypes.c_float)]
 
 
 class mw_rope(ctypes.Structure):
@@ -89,6 +90,10 @@ SIGNATURES = {
     "mw_kvcache_append_strided": ([_cache_p, _vp, _vp, _str_p, _vp], _i),
     "mw_chunk_attn_cached_strided": ([_vp, _vp, _vp, _i, _i, _cache_p, _i, _i, _vp, _vp, _f, _vp, _sz, _str_p,
                                       _vp], _i),
+    "mw_quantize_fp8": ([_vp, _str_p, _vp, _i, _i, _i, _i, _f, _vp], _i),
+    "mw_kvcache_init_fp8": ([_cache_p, _vp, _vp, _i, _i, _i, _i, _i, _f, _f], _i),
+    "mw_chunk_attn_cached_fp8": ([_vp, _vp, _vp, _i, _i, _cache_p, _i, _i, _vp, _vp, _f, _f, _vp, _sz, _str_p, _vp],
+                                 _i),
     "mw_sched_num_ticks": ([ctypes.POINTER(mw_sched_config)], ctypes.c_int64),
     "mw_sched_plan": ([ctypes.POINTER(mw_sched_config), ctypes.c_int64, ctypes.POINTER(mw_sched_tick)], _i),
 }
@@ -151,6 +156,15 @@ def _bf16_4d(name, t, view: bool = False):
         raise ValueError(f"{name} must be contiguous")
     if t.device.type != "cuda":
         raise ValueError(f"{name} must be on a GPU device")
+
+
+def _u8_4d(name, t):
+    """e4m3 codes as a contiguous uint8 [B,H,T,D] tensor on a GPU."""
+    torch = _torch()
+    if t.dtype != torch.uint8:
+        raise TypeError(f"{name} must hold e4m3 codes as uint8, got {t.dtype}")
+    if t.dim() != 4 or not t.is_contiguous() or t.device.type != "cuda":
+        raise ValueError(f"{name} must be a contiguous [B,H,T,D] tensor on a GPU")
 
 
 def _strides(*ts):
@@ -230,22 +244,31 @@ def mw_block_causal_attn_bwd(q, k, v, o, d_o, lse, chunk_len: int, scale=None, w
 
 
 class KVCache:
-    """Ring-buffered rolling KV cache over torch-owned slot tensors (bf16 [S,B,H,L,D]).
+    """Ring-buffered rolling KV cache over torch-owned slot tensors: bf16
+    [S,B,H,L,D], or with fp8=True e4m3 codes (uint8 [S,B,H,L,D]) with the
+    per-tensor scales k_scale, v_scale (value = code * scale).
 
     Wraps the mw_kvcache descriptor; `head`/`tail` count commits/evictions.
     """
 
-    def __init__(self, S: int, B: int, H: int, L: int, D: int, device="cuda", k_slots=None, v_slots=None):
+    def __init__(self, S: int, B: int, H: int, L: int, D: int, device="cuda", k_slots=None, v_slots=None,
+                 fp8: bool = False, k_scale: float = 1.0, v_scale: float = 1.0):
         torch = _torch()
         shape = (S, B, H, L, D)
-        self.k_slots = torch.empty(shape, dtype=torch.bfloat16, device=device) if k_slots is None else k_slots
-        self.v_slots = torch.empty(shape, dtype=torch.bfloat16, device=device) if v_slots is None else v_slots
+        dt = torch.uint8 if fp8 else torch.bfloat16
+        self.fp8 = bool(fp8)
+        self.k_slots = torch.empty(shape, dtype=dt, device=device) if k_slots is None else k_slots
+        self.v_slots = torch.empty(shape, dtype=dt, device=device) if v_slots is None else v_slots
         for n, t in (("k_slots", self.k_slots), ("v_slots", self.v_slots)):
-            if t.shape != shape or t.dtype != torch.bfloat16 or not t.is_contiguous():
-                raise ValueError(f"{n} must be bf16 contiguous {shape}")
+            if t.shape != shape or t.dtype != dt or not t.is_contiguous():
+                raise ValueError(f"{n} must be {dt} contiguous {shape}")
         self.desc = mw_kvcache()
-        _check(load().mw_kvcache_init(ctypes.byref(self.desc), _ptr(self.k_slots), _ptr(self.v_slots),
-                                      S, B, H, L, D))
+        if fp8:
+            _check(load().mw_kvcache_init_fp8(ctypes.byref(self.desc), _ptr(self.k_slots), _ptr(self.v_slots),
+                                              S, B, H, L, D, float(k_scale), float(v_scale)))
+        else:
+            _check(load().mw_kvcache_init(ctypes.byref(self.desc), _ptr(self.k_slots), _ptr(self.v_slots),
+                                          S, B, H, L, D))
 
     @property
     def head(self) -> int:
@@ -270,7 +293,10 @@ class KVCache:
             self._sink = None
             return
         for n, t in (("k_sink", k_sink), ("v_sink", v_sink)):
-            _bf16_4d(n, t)
+            if self.fp8:
+                _u8_4d(n, t)
+            else:
+                _bf16_4d(n, t)
             if tuple(t.shape[:2]) != (d.B, d.H) or t.shape[3] != d.D or t.shape != k_sink.shape:
                 raise ValueError(f"{n} must be [B,H,sink_len,D] with B,H,D of the cache")
         _check(load().mw_kvcache_set_sink(ctypes.byref(d), _ptr(k_sink), _ptr(v_sink), int(k_sink.shape[2])))
@@ -354,6 +380,54 @@ def mw_chunk_attn_cached(q, k_new, v_new, n_queued: int, q_len: int, cache: KVCa
                                                ctypes.byref(d), int(window), int(flags), _ptr(o), _ptr(lse), scale,
                                                _ptr(workspace), nbytes, _strides(q, k_new, v_new, o),
                                                _stream_handle(dev)))
+    return o, lse
+
+
+# ----------------------------------------------------------------------------- fp8 inference variant
+
+def mw_quantize_fp8(x, scale: float, out=None):
+    """bf16 [B,H,T,D] view -> contiguous e4m3 codes (uint8 [B,H,T,D]), code = RNE(clamp(x / scale))."""
+    torch = _torch()
+    _bf16_4d("x", x, view=True)
+    B, H, T, D = x.shape
+    y = torch.empty((B, H, T, D), dtype=torch.uint8, device=x.device) if out is None else out
+    _u8_4d("out", y)
+    if tuple(y.shape) != (B, H, T, D):
+        raise ValueError("out must have the shape of x")
+    _same_device(x, y)
+    _check(load().mw_quantize_fp8(_ptr(x), _strides(x), _ptr(y), B, H, T, D, float(scale), _stream_handle(x.device)))
+    return y
+
+
+def mw_chunk_attn_cached_fp8(q8, k8_new, v8_new, n_queued: int, q_len: int, cache: KVCache, q_scale: float,
+                             window: int = -1, flags: int = MW_QUEUED_CAUSAL, scale=None, out=None, lse=None,
+                             want_lse: bool = False, workspace=None, split: bool = True):
+    """Cached chunk attention over an e4m3 cache.  q8, k8_new, v8_new: e4m3 codes
+    (uint8 [B,H,n_queued*q_len,D]; q8 with q_scale, k8/v8 with the cache's
+    scales).  Returns (o bf16, lse or None)."""
+    torch = _torch()
+    d = cache.desc
+    for n, t in (("q8", q8), ("k8_new", k8_new), ("v8_new", v8_new)):
+        _u8_4d(n, t)
+        if tuple(t.shape) != (d.B, d.H, n_queued * q_len, d.D):
+            raise ValueError(f"{n} must be [B,H,n_queued*q_len,D] = {(d.B, d.H, n_queued * q_len, d.D)}")
+    dev = _same_device(cache.k_slots, q8, k8_new, v8_new)
+    scale = 1.0 / math.sqrt(d.D) if scale is None else float(scale)
+    o = torch.empty(tuple(q8.shape), dtype=torch.bfloat16, device=dev) if out is None else out
+    _bf16_4d("out", o, view=True)
+    if o.shape != q8.shape:
+        raise ValueError("out must have the shape of q8")
+    if want_lse and lse is None:
+        lse = torch.empty((d.B, d.H, n_queued * q_len), dtype=torch.float32, device=dev)
+    if split and workspace is None:
+        need = mw_chunk_attn_cached_workspace_size(cache, n_queued, q_len, window)
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev) if need > 0 else None
+    if not split:
+        workspace = None
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(load().mw_chunk_attn_cached_fp8(_ptr(q8), _ptr(k8_new), _ptr(v8_new), int(n_queued), int(q_len),
+                                           ctypes.byref(d), int(window), int(flags), _ptr(o), _ptr(lse), scale,
+                                           float(q_scale), _ptr(workspace), nbytes, _strides(o), _stream_handle(dev)))
     return o, lse
 
 

@@ -37,6 +37,7 @@ UNITS = [  # (object name, source, extra flags)
     ("attn_bwd64", "attn_bwd.hip", ["-DMW_BWD_HEAD_DIM=64"]),
     ("attn_bwd72", "attn_bwd.hip", ["-DMW_BWD_HEAD_DIM=72"]),
     ("attn_bwd128", "attn_bwd.hip", ["-DMW_BWD_HEAD_DIM=128", *ILP]),
+    ("attn_fwd_fp8", "attn_fwd_fp8.hip", []),
     ("kvcache", "kvcache.hip", []),
     ("mw_api", "mw_api.cpp", []),
     ("sched", "sched.cpp", []),

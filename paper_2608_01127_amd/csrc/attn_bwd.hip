@@ -23,11 +23,6 @@
 
 namespace mw {
 
-__device__ __forceinline__ int xcd_remap_b(int bid, int n) {
-  if (n % 8) return bid;
-  return (bid % 8) * (n / 8) + bid / 8;
-}
-
 // Row terms of the backward pass: Delta = rowsum(dO * O) and LSE scaled to
 // base 2 (LSE * log2 e), one 16-byte chunk per thread, reduced over the row's lanes.
 // CPR lanes per row (a power of two); at D = 72 the 9 pieces of a row leave
@@ -73,7 +68,7 @@ __global__ __launch_bounds__(64 * NW, (D == 128 ? 4 : 8) / NW) void bwd_dkdv_ker
   __shared__ __attribute__((aligned(16))) float lse_s[2][BM];
   __shared__ __attribute__((aligned(16))) float dlt_s[2][BM];
 
-  const int logical = xcd_remap_b(blockIdx.x, gridDim.x);
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = logical / n_ktiles;
   const int kt = logical % n_ktiles;  // early keys are seen by the most queries: heaviest first
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -232,7 +227,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][TE];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[2][TE];
 
-  const int logical = xcd_remap_b(blockIdx.x, gridDim.x);
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = logical / n_qtiles;
   const int qt = n_qtiles - 1 - logical % n_qtiles;  // late queries see the most keys: heaviest first
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;

@@ -28,15 +28,6 @@
 
 namespace mw {
 
-// XCD-aware order: consecutive workgroup ids are dealt round-robin to the 8
-// XCDs; remap so that each XCD receives one contiguous range of logical work
-// items (whole heads, heaviest query tiles first), which keeps a head's K/V in
-// one XCD's L2.
-__device__ __forceinline__ int xcd_remap(int bid, int n) {
-  if (n % 8) return bid;
-  return (bid % 8) * (n / 8) + bid / 8;
-}
-
 // Per-thread row offsets of the K and V tiles: queued / training keys (their
 // views' T strides) and ring slots (rows D apart).
 template <int D, bool CACHED, int BN, int NT>
@@ -589,6 +580,15 @@ FwdChoice fwd_choice(int D, bool cached, int Tq) {
   return {32 * FwdCfg<128>::RB * FwdCfg<128>::NW, 2};
 }
 
+hipError_t launch_combine(const FwdParams& p, int D, hipStream_t stream) {
+  if (D != 128) return hipErrorInvalidValue;
+  const long long rows = (long long)p.BH * p.Tq;
+  const long long threads = rows * (128 / 4);
+  hipLaunchKernelGGL(attn_combine_kernel<128>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p.part,
+                     p.o, p.so, p.H, p.Tq, p.lse, p.n_splits, rows);
+  return hipGetLastError();
+}
+
 size_t fwd_split_bytes(int D, int BH, int Tq, int n_splits) {
   if (n_splits <= 1) return 0;
   return (size_t)n_splits * BH * Tq * (D + 2) * sizeof(float);
@@ -601,12 +601,15 @@ size_t fwd_split_bytes(int D, int BH, int Tq, int n_splits) {
 // back.  The count with the lowest estimate wins (each split keeps at least
 // two key tiles; at most 64 splits; bounded by the workspace).
 int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes) {
-  const FwdChoice ch = fwd_choice(D, true, Tq);
+  return fwd_choose_splits_for(fwd_choice(D, true, Tq), 0.8e15, D, BH, Tq, Tk, ws_bytes);
+}
+
+int fwd_choose_splits_for(const FwdChoice& ch, double flops, int D, int BH, int Tq, int Tk, size_t ws_bytes) {
   const int BN = 128;  // keys staged per step (at most)
   const double slots = 256.0 * ch.wg_per_cu;  // resident workgroups (registers / LDS)
   const double base = (double)((Tq + ch.bm - 1) / ch.bm) * BH;
   const double pairs = (double)BH * Tq * std::max(1.0, (double)Tk - 0.5 * Tq);
-  const double t_work = std::max(4.0 * pairs * D / 0.8e15, 2.0 * BH * (double)Tk * D * 2 / 4.0e12);
+  const double t_work = std::max(4.0 * pairs * D / flops, 2.0 * BH * (double)Tk * D * 2 / 4.0e12);
   const int ns_max = (int)std::min<long long>(64, std::max(1, (Tk / BN) / 2));
   int best = 1;
   double best_t = 1e30;

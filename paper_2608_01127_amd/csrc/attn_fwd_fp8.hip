@@ -1,0 +1,473 @@
+// fp8 (OCP e4m3) cached chunk attention at head width 128, and the fp8
+// quantizer (gfx950).
+//
+// The low-precision inference variant follows the deployment direction the
+// paper names in its conclusion (quantization to cut inference cost, Sec. 6);
+// the attention it computes is the cached chunk attention of Sec. 3.5 (queued
+// in-flight chunks over [sink | window | queued keys]).  Q, K and V are e4m3
+// with per-tensor scales (value = code * scale); scores and probabilities are
+// accumulated in fp32, and the probabilities are rounded to e4m3 (RNE) before
+// the PV product.  Both products run on v_mfma_f32_32x32x64_f8f6f4, which has
+// twice the bf16 rate and halves K/V bytes.
+//
+// Layouts (64-lane wave, lane l, h = l / 32):
+//   S^T = K Q^T, contraction over d in two steps of 64: lane l supplies bytes
+//     d = 64 kk + 32 h + 0..31 of key row l % 32 (A) and of query row l % 32
+//     (B).  The instruction pairs byte j of A with byte j of B for every lane
+//     half, so any common assignment of d to bytes is a valid contraction.
+//   O^T += V^T P^T over the tile's 64 keys: byte j of lane l's B operand is
+//     P of key kappa(h, j) = 32 (j / 16) + 8 ((j % 16) / 4) + 4 h + j % 4, which
+//     is the accumulator layout of the two 32-key S^T blocks, so the
+//     probabilities are packed without data movement; the A operand holds
+//     V[kappa(h, j)][d] for d = 32 db + l % 32, read from the row-major V tile
+//     with four transposing reads ds_read_b64_tr_b8 (in each group of 16 lanes,
+//     byte j of lane i is byte i % 8 of the 8 bytes addressed by lane
+//     2 j + (i % 16) / 8).
+#include <algorithm>
+#include <cmath>
+#include <type_traits>
+
+#include "mw_device.h"
+#include "mw_kernels.h"
+
+namespace mw {
+
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x2 __attribute__((ext_vector_type(2)));
+typedef uint8_t fp8_t;
+
+namespace {
+
+constexpr int DH = 128;  // head width = bytes per fp8 row
+constexpr float kE4m3Max = 448.f;
+
+__device__ __forceinline__ f32x16 mfma_fp8(i32x8 a, i32x8 b, f32x16 c) {
+  // formats 0/0: e4m3 x e4m3; block scales unused (the plain instruction)
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
+// [rows][128] bytes with the 16-byte slots of row r permuted by
+// swz(r) = (r & 7) ^ 4 ((r >> 3) & 1): eight consecutive rows hit eight
+// different slots (the K row reads), and so do the rows {4h + 0..3, 8 + 4h +
+// 0..3} of one transposing read (the V reads).
+struct Tile8 {
+  __device__ __forceinline__ static int swz(int row) { return (row & 7) ^ (((row >> 3) & 1) << 2); }
+  __device__ __forceinline__ static int off(int row, int col) {
+    return row * DH + ((((col >> 4) ^ swz(row)) << 4) | (col & 15));
+  }
+};
+
+// K fragment of contraction step kk: K[row][64 kk + 32 h + 0..31].
+__device__ __forceinline__ i32x8 lds_k8(const fp8_t* tile, int row, int kk, int lane) {
+  const int c = 64 * kk + 32 * (lane >> 5);
+  const i32x4 a = *reinterpret_cast<const i32x4*>(tile + Tile8::off(row, c));
+  const i32x4 b = *reinterpret_cast<const i32x4*>(tile + Tile8::off(row, c + 16));
+  return i32x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+// V^T fragment of column block db over the 64 keys of `tile` (row 0 = first key).
+__device__ __forceinline__ i32x8 lds_v8(const fp8_t* tile, int db, int lane) {
+  const int lam = lane & 15;
+  const int col = 32 * db + 16 * ((lane >> 4) & 1) + 8 * (lam & 1);
+  const int rsub = 8 * (lam >> 3) + 4 * (lane >> 5) + ((lam >> 1) & 3);
+  i32x8 r;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const i32x2 x = __builtin_amdgcn_ds_read_tr8_b64_v2i32((MW_LDS i32x2*)(tile + Tile8::off(16 * q + rsub, col)));
+    r[2 * q] = x[0];
+    r[2 * q + 1] = x[1];
+  }
+  return r;
+}
+
+// Probabilities of two 32-key accumulator blocks -> e4m3 B operand (RNE; the
+// values lie in [0, 2^8], inside the e4m3 range).
+__device__ __forceinline__ i32x8 pack_p8(const f32x16& s0, const f32x16& s1) {
+  i32x8 r;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    int x = __builtin_amdgcn_cvt_pk_fp8_f32(s0[4 * w], s0[4 * w + 1], 0, false);
+    r[w] = __builtin_amdgcn_cvt_pk_fp8_f32(s0[4 * w + 2], s0[4 * w + 3], x, true);
+    x = __builtin_amdgcn_cvt_pk_fp8_f32(s1[4 * w], s1[4 * w + 1], 0, false);
+    r[4 + w] = __builtin_amdgcn_cvt_pk_fp8_f32(s1[4 * w + 2], s1[4 * w + 3], x, true);
+  }
+  return r;
+}
+
+// Byte offsets of the 16-byte pieces this thread stages of a ROWS x 128-byte
+// tile whose rows are `row_stride` bytes apart (LDS piece ci = row ci / 8,
+// physical slot ci % 8, fetched from logical slot (ci % 8) ^ swz(row)).
+template <int ROWS, int NT>
+struct RowOffsets8 {
+  static constexpr int PIECES = ROWS * 8;
+  static_assert(PIECES % NT == 0, "whole staging rounds");
+  static constexpr int ROUNDS = PIECES / NT;
+  unsigned off[ROUNDS];
+  __device__ __forceinline__ RowOffsets8(long long row_stride, int tid) {
+#pragma unroll
+    for (int it = 0; it < ROUNDS; ++it) {
+      const int ci = it * NT + tid;
+      const int row = ci >> 3;
+      off[it] = (unsigned)((long long)row * row_stride + 16 * ((ci & 7) ^ Tile8::swz(row)));
+    }
+  }
+};
+
+template <int ROWS, int NT>
+__device__ __forceinline__ void stage8_s(fp8_t* lds_tile, const fp8_t* tile, const RowOffsets8<ROWS, NT>& ro, int tid) {
+#pragma unroll
+  for (int it = 0; it < RowOffsets8<ROWS, NT>::ROUNDS; ++it)
+    dma_lds_16_s(tile, ro.off[it], (MW_LDS void*)(lds_tile + (it * NT + (tid & ~63)) * 16));
+}
+
+struct RowPair8 {
+  const fp8_t* k;
+  const fp8_t* v;
+};
+template <int ROWS, int NT, typename RowSrc>
+__device__ __forceinline__ void stage8_rows(fp8_t* k_tile, fp8_t* v_tile, RowSrc row_src, int tid) {
+#pragma unroll
+  for (int it = 0; it < ROWS * 8 / NT; ++it) {
+    const int ci = it * NT + tid;
+    const int row = ci >> 3;
+    const int ls = (ci & 7) ^ Tile8::swz(row);
+    const RowPair8 src = row_src(row);
+    const int dst = (it * NT + (tid & ~63)) * 16;  // wave-uniform base
+    dma_lds_16(src.k + 16 * ls, (MW_LDS void*)(k_tile + dst));
+    dma_lds_16(src.v + 16 * ls, (MW_LDS void*)(v_tile + dst));
+  }
+}
+
+// One BN-key tile of the virtual key sequence [sink | window slots | queued]
+// into LDS (same classification as the bf16 kernel: a tile inside the queued
+// keys or inside one window chunk is staged from one base; tiles that straddle
+// a boundary or the end map row by row; rows past the end read the last key).
+// fp8 tensors are contiguous: queued [BH, Tq, 128], sink [BH, sink_len, 128],
+// slots [S][BH, L, 128].
+template <int BN, int NT>
+__device__ __forceinline__ void stage_kv8(const FwdParams& p, int bh, int k0, fp8_t* Kt, fp8_t* Vt,
+                                          const RowOffsets8<BN, NT>& ro, int tid) {
+  const fp8_t* qk = reinterpret_cast<const fp8_t*>(p.k) + (long long)bh * p.Tq * DH;
+  const fp8_t* qv = reinterpret_cast<const fp8_t*>(p.v) + (long long)bh * p.Tq * DH;
+  const fp8_t* ks = reinterpret_cast<const fp8_t*>(p.k_slots);
+  const fp8_t* vs = reinterpret_cast<const fp8_t*>(p.v_slots);
+  const int kl = min(k0 + BN, p.Tk) - 1;
+  const int kw0 = k0 - p.sink_len;
+  const int w0 = kw0 > 0 ? kw0 / p.L : 0;
+  const int off0 = kw0 - w0 * p.L;
+  if (k0 >= p.wL && k0 + BN <= p.Tk) {  // queued keys only
+    const long long j = k0 - p.wL;
+    stage8_s<BN, NT>(Kt, qk + j * DH, ro, tid);
+    stage8_s<BN, NT>(Vt, qv + j * DH, ro, tid);
+    return;
+  }
+  if (kw0 >= 0 && kl < p.wL && off0 + (kl - k0) < p.L) {  // one window chunk
+    int slot = p.first_slot + w0;
+    slot = slot >= p.S ? slot - p.S : slot;
+    const long long e = (long long)slot * p.slot_stride + ((long long)bh * p.L + off0) * DH;
+    stage8_s<BN, NT>(Kt, ks + e, ro, tid);
+    stage8_s<BN, NT>(Vt, vs + e, ro, tid);
+    return;
+  }
+  stage8_rows<BN, NT>(Kt, Vt, [&](int r) -> RowPair8 {
+    const int key = min(k0 + r, p.Tk - 1);
+    if (key < p.sink_len) {
+      const long long e = ((long long)bh * p.sink_len + key) * DH;
+      return {reinterpret_cast<const fp8_t*>(p.k_sink) + e, reinterpret_cast<const fp8_t*>(p.v_sink) + e};
+    }
+    if (key < p.wL) {
+      int w = w0, off = key - p.sink_len - w0 * p.L;
+      while (off >= p.L) {  // at most one step when L >= BN
+        off -= p.L;
+        ++w;
+      }
+      int slot = p.first_slot + w;
+      slot = slot >= p.S ? slot - p.S : slot;
+      const long long e = (long long)slot * p.slot_stride + ((long long)bh * p.L + off) * DH;
+      return {ks + e, vs + e};
+    }
+    const long long j = key - p.wL;
+    return {qk + j * DH, qv + j * DH};
+  }, tid);
+}
+
+constexpr float kRescaleThreshold8 = 8.f;  // probabilities stay <= 2^8 < 448
+
+// NW waves of RB 32-row query blocks; BN keys (a multiple of 64) per step.
+template <int NW, int RB, int BN>
+__global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd_fp8_kernel(FwdParams p) {
+  constexpr int BM = 32 * RB * NW, NT = 64 * NW, KB = BN / 32, KP = BN / 64;
+  constexpr int KK = DH / 64, DB = DH / 32;
+  __shared__ __attribute__((aligned(16))) fp8_t lds[2][2][BN * DH];  // K, V x double buffer
+  fp8_t(*Ks)[BN * DH] = lds[0];
+  fp8_t(*Vs)[BN * DH] = lds[1];
+
+  const int logical = xcd_remap(blockIdx.x, gridDim.x);
+  const int NS = p.n_splits;
+  const int split = logical % NS;
+  const int bh = (logical / NS) / p.n_qtiles;
+  const int qt = p.n_qtiles - 1 - (logical / NS) % p.n_qtiles;  // heaviest (last) query tile first
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int q0 = qt * BM;
+  const int b_ = bh / p.H, h_ = bh - b_ * p.H;
+  const fp8_t* qg = reinterpret_cast<const fp8_t*>(p.q) + (long long)bh * p.Tq * DH;
+
+  Vis vis{p.vis_mode, p.L, p.Tk, p.qlen, p.wL};
+
+  int qrow[RB], e1[RB], s2[RB], e2[RB];
+  i32x8 qf[RB][KK];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    qrow[rb] = q0 + (wave * RB + rb) * 32 + (lane & 31);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      if (qrow[rb] < p.Tq) {
+        const fp8_t* src = qg + (long long)qrow[rb] * DH + 64 * kk + 32 * (lane >> 5);
+        const i32x4 a = *reinterpret_cast<const i32x4*>(src);
+        const i32x4 b = *reinterpret_cast<const i32x4*>(src + 16);
+        qf[rb][kk] = i32x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+      } else {
+        qf[rb][kk] = i32x8{0, 0, 0, 0, 0, 0, 0, 0};
+      }
+    }
+    vis.range(min(qrow[rb], p.Tq - 1), e1[rb], s2[rb], e2[rb]);
+  }
+  int e1f, s2f, e2f, e1l, s2l, e2l;
+  vis.range(q0, e1f, s2f, e2f);
+  vis.range(min(q0 + BM, p.Tq) - 1, e1l, s2l, e2l);
+  const int kend_all = max(e1l, e2l);
+  const int ntiles = (kend_all + BN - 1) / BN;
+  const int kbeg = (int)((long long)ntiles * split / NS) * BN;
+  const int kend = min(kend_all, (int)((long long)ntiles * (split + 1) / NS) * BN);
+  auto advance = [&](int k) {
+    int n = k + BN;
+    if (n >= e1l && n + BN <= s2f) n = (s2f / BN) * BN;
+    return n;
+  };
+
+  f32x16 o[RB][DB];
+  float m[RB], lsum[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[rb][db] = zero16();
+    m[rb] = -INFINITY;
+    lsum[rb] = 0.f;
+  }
+  const float c = p.scale_log2;  // softmax scale * q_scale * k_scale * log2(e)
+  const int kfull = max(0, (e1f / BN) * BN);
+
+  auto step = [&](auto masked, const int k0, const fp8_t* Kt, const fp8_t* Vt) {
+    f32x16 s[RB][KB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) s[rb][kb] = zero16();
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        const i32x8 kfrag = lds_k8(Kt, kb * 32 + (lane & 31), kk, lane);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) s[rb][kb] = mfma_fp8(kfrag, qf[rb][kk], s[rb][kb]);
+      }
+    }
+    if constexpr (decltype(masked)::value) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int key = k0 + kb * 32 + acc_row(i, lane);
+            const bool ok = (key < e1[rb]) | ((key >= s2[rb]) & (key < e2[rb]));  // no short circuit
+            s[rb][kb][i] = ok ? s[rb][kb][i] : -INFINITY;
+          }
+        }
+      }
+    }
+    float mx[RB];
+    bool need_any = false;
+    bool need[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      mx[rb] = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx[rb] = fmaxf(mx[rb], s[rb][kb][i]);
+      }
+      mx[rb] = max_halves(mx[rb]) * c;
+      need[rb] = mx[rb] > m[rb] + kRescaleThreshold8;
+      need_any |= need[rb];
+    }
+    if (wave_any(need_any)) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const float alpha = need[rb] ? fast_exp2(m[rb] - mx[rb]) : 1.f;
+        lsum[rb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i) o[rb][db][i] *= alpha;
+        }
+        m[rb] = need[rb] ? mx[rb] : m[rb];
+      }
+    }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const float nm = (m[rb] == -INFINITY) ? 0.f : -m[rb];
+      float ls = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float pv = fast_exp2(fmaf(s[rb][kb][i], c, nm));
+          s[rb][kb][i] = pv;
+          ls += pv;
+        }
+      }
+      lsum[rb] += ls;
+    }
+#pragma unroll
+    for (int kp = 0; kp < KP; ++kp) {
+      i32x8 pb[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) pb[rb] = pack_p8(s[rb][2 * kp], s[rb][2 * kp + 1]);
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const i32x8 vfrag = lds_v8(Vt + kp * 64 * DH, db, lane);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) o[rb][db] = mfma_fp8(vfrag, pb[rb], o[rb][db]);
+      }
+    }
+  };
+
+  const RowOffsets8<BN, NT> ro(DH, tid);
+  int kc = advance(kbeg - BN);
+  {
+    int buf = 0;
+    if (kc < kend) stage_kv8<BN, NT>(p, bh, kc, Ks[0], Vs[0], ro, tid);
+    wait_vmem();
+    __syncthreads();
+    auto run = [&](auto masked, const int kstop) {
+      while (kc < kstop) {
+        const int kn = advance(kc);
+        if (kn < kend) stage_kv8<BN, NT>(p, bh, kn, Ks[buf ^ 1], Vs[buf ^ 1], ro, tid);
+        step(masked, kc, Ks[buf], Vs[buf]);
+        wait_vmem();
+        __syncthreads();
+        buf ^= 1;
+        kc = kn;
+      }
+    };
+    run(std::false_type{}, min(kfull, kend));
+    run(std::true_type{}, kend);
+  }
+
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    lsum[rb] = sum_halves(lsum[rb]);
+    if (qrow[rb] >= p.Tq) continue;
+    if (NS > 1) {
+      // partial of this key range (O already carries the V scale)
+      const long long row = ((long long)split * p.BH + bh) * p.Tq + qrow[rb];
+      float* po = p.part + row * DH;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int col = db * 32 + 8 * g + 4 * (lane >> 5);
+          f32x4 w;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) w[j] = o[rb][db][4 * g + j] * p.o_scale;
+          *reinterpret_cast<f32x4*>(po + col) = w;
+        }
+      }
+      if (lane < 32) {
+        float* ml = p.part + (long long)NS * p.BH * p.Tq * DH + 2 * row;
+        ml[0] = m[rb];
+        ml[1] = lsum[rb];
+      }
+    } else {
+      const float inv = p.o_scale / lsum[rb];
+      bf16_t* orow = p.o + b_ * p.so.b + h_ * p.so.h + qrow[rb] * p.so.t;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int col = db * 32 + 8 * g + 4 * (lane >> 5);
+          bf16x4 w;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) w[j] = to_bf16(o[rb][db][4 * g + j] * inv);
+          *reinterpret_cast<bf16x4*>(orow + col) = w;
+        }
+      }
+      if (p.lse != nullptr && lane < 32) {
+        p.lse[(long long)bh * p.Tq + qrow[rb]] = (m[rb] + __log2f(lsum[rb])) * 0.69314718055994530942f;
+      }
+    }
+  }
+}
+
+// bf16 [B, H, T, D] views -> contiguous e4m3 [B, H, T, D]:
+//   code = RNE_e4m3(clamp(fl32(x * inv_scale), -448, 448)).
+// One thread per 8 elements; blockIdx.y selects the job (K and V of a commit
+// share one launch).
+__global__ __launch_bounds__(256) void quantize_fp8_kernel(QuantJobs jobs, int H, int T, int D, long long n_pieces) {
+  const QuantJob& jb = jobs.j[blockIdx.y];
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= n_pieces) return;
+  const int ppr = D / 8;  // pieces per row
+  const long long row = gid / ppr;
+  const int c = (int)(gid - row * ppr) * 8;
+  const long long bh = row / T;
+  const long long t = row - bh * T;
+  const long long b = bh / H, h = bh - b * H;
+  const bf16x8 x = *reinterpret_cast<const bf16x8*>(jb.x + b * jb.sx.b + h * jb.sx.h + t * jb.sx.t + c);
+  float f[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) f[i] = fminf(fmaxf((float)x[i] * jb.inv_scale, -kE4m3Max), kE4m3Max);
+  u32x2 out;
+#pragma unroll
+  for (int w = 0; w < 2; ++w) {
+    const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(f[4 * w], f[4 * w + 1], 0, false);
+    out[w] = (unsigned)__builtin_amdgcn_cvt_pk_fp8_f32(f[4 * w + 2], f[4 * w + 3], lo, true);
+  }
+  *reinterpret_cast<u32x2*>(jb.y + row * D + c) = out;
+}
+
+// Tile configuration: 8 waves of one 32-row block (256 queries; one workgroup
+// per CU at 166 registers), 64 keys per step.
+struct Fwd8Cfg {
+  static constexpr int NW = 8;
+  static constexpr int RB = 1;
+  static constexpr int BN = 64;
+};
+
+}  // namespace
+
+FwdChoice fwd8_choice() { return {32 * Fwd8Cfg::RB * Fwd8Cfg::NW, 1}; }
+
+hipError_t launch_fwd_fp8(FwdParams p, hipStream_t stream) {
+  using C = Fwd8Cfg;
+  constexpr int BM = 32 * C::RB * C::NW;
+  p.n_qtiles = (p.Tq + BM - 1) / BM;
+  if (p.n_splits < 1) p.n_splits = 1;
+  hipLaunchKernelGGL((attn_fwd_fp8_kernel<C::NW, C::RB, C::BN>), dim3(p.n_qtiles * p.BH * p.n_splits),
+                     dim3(64 * C::NW), 0, stream, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.n_splits == 1) return e;
+  return launch_combine(p, DH, stream);
+}
+
+hipError_t launch_quantize_fp8(const QuantJobs& jobs, int n_jobs, int B, int H, int T, int D, hipStream_t stream) {
+  const long long n_pieces = (long long)B * H * T * (D / 8);
+  if (n_pieces == 0) return hipSuccess;
+  hipLaunchKernelGGL(quantize_fp8_kernel, dim3((unsigned)((n_pieces + 255) / 256), n_jobs), dim3(256), 0, stream,
+                     jobs, H, T, D, n_pieces);
+  return hipGetLastError();
+}
+
+}  // namespace mw

@@ -251,6 +251,28 @@ int mw_kvcache_init(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, i
   c->k_sink = nullptr;
   c->v_sink = nullptr;
   c->sink_len = 0;
+  c->elem_bytes = 2;
+  c->k_scale = 1.f;
+  c->v_scale = 1.f;
+  return ok();
+}
+
+static bool good_scale(float s) { return s > 0.f && std::isfinite(s); }
+
+int mw_kvcache_init_fp8(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, int H, int L, int D, float k_scale,
+                        float v_scale) {
+  const char* fn = "mw_kvcache_init_fp8";
+  if (c == nullptr) return fail(MW_EINVAL, "%s: cache is NULL", fn);
+  if (D != 128) return fail(MW_EUNSUPPORTED, "%s: head dimension %d is not supported (128)", fn, D);
+  if (!good_scale(k_scale) || !good_scale(v_scale))
+    return fail(MW_EINVAL, "%s: k_scale and v_scale must be finite and > 0", fn);
+  mw_kvcache t;
+  const int st = mw_kvcache_init(&t, k_slots, v_slots, S, B, H, L, D);
+  if (st) return fail(st, "%s: %s", fn, mw_last_error());
+  t.elem_bytes = 1;
+  t.k_scale = k_scale;
+  t.v_scale = v_scale;
+  *c = t;
   return ok();
 }
 
@@ -258,7 +280,9 @@ static int check_cache(const char* fn, const mw_kvcache* c) {
   if (c == nullptr) return fail(MW_EINVAL, "%s: cache is NULL", fn);
   if (c->k_slots == nullptr || c->v_slots == nullptr || c->S < 1 || c->B < 1 || c->H < 1 || c->L < 1 ||
       (c->D != 64 && c->D != 72 && c->D != 128) || c->tail < 0 || c->head < c->tail || c->head - c->tail > c->S ||
-      c->sink_len < 0 || (c->sink_len > 0 && (c->k_sink == nullptr || c->v_sink == nullptr)))
+      c->sink_len < 0 || (c->sink_len > 0 && (c->k_sink == nullptr || c->v_sink == nullptr)) ||
+      (c->elem_bytes != 1 && c->elem_bytes != 2) ||
+      (c->elem_bytes == 1 && (c->D != 128 || !good_scale(c->k_scale) || !good_scale(c->v_scale))))
     return fail(MW_EINVAL, "%s: cache descriptor is not initialised or is corrupt", fn);
   return MW_OK;
 }
@@ -279,6 +303,18 @@ int mw_kvcache_append_strided(mw_kvcache* c, const void* k_chunk, const void* v_
   if (c->head - c->tail == c->S) return fail(MW_EFULL, "%s: all %d slots hold live chunks; evict first", fn, c->S);
   const long long n = (long long)c->B * c->H * c->L * c->D;
   const int slot = (int)(c->head % c->S);
+  if (c->elem_bytes == 1) {  // quantize into the e4m3 slot
+    const mw::Strides cs = contiguous(c->H, c->L, c->D);
+    mw::QuantJobs jobs{};
+    jobs.j[0] = {static_cast<const uint16_t*>(k_chunk), strides ? to_internal(strides[0]) : cs,
+                 static_cast<uint8_t*>(c->k_slots) + (long long)slot * n, 1.f / c->k_scale};
+    jobs.j[1] = {static_cast<const uint16_t*>(v_chunk), strides ? to_internal(strides[1]) : cs,
+                 static_cast<uint8_t*>(c->v_slots) + (long long)slot * n, 1.f / c->v_scale};
+    hipError_t e = mw::launch_quantize_fp8(jobs, 2, c->B, c->H, c->L, c->D, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_status(fn, e);
+    c->head += 1;
+    return ok();
+  }
   uint16_t* kd = static_cast<uint16_t*>(c->k_slots) + (long long)slot * n;
   uint16_t* vd = static_cast<uint16_t*>(c->v_slots) + (long long)slot * n;
   const uint16_t* ks = static_cast<const uint16_t*>(k_chunk);
@@ -324,6 +360,8 @@ int mw_kvcache_rope_shift(mw_kvcache* c, int shift, const mw_rope* rope, mw_stre
   int st = check_cache(fn, c);
   if (st) return st;
   if (rope == nullptr) return fail(MW_EINVAL, "%s: rope is NULL", fn);
+  if (c->elem_bytes == 1)
+    return fail(MW_EUNSUPPORTED, "%s: not available for e4m3 slots (an in-place rotation re-rounds them)", fn);
   if (rope->dim_offset < 0 || rope->dim_offset % 2 || rope->dim_count < 2 || rope->dim_count % 2 ||
       rope->dim_count > 128 || rope->dim_offset + rope->dim_count > c->D)
     return fail(MW_EINVAL, "%s: rope band [%d, %d) is not a valid even band of the %d head dims", fn, rope->dim_offset,
@@ -370,6 +408,9 @@ int mw_kvcache_slot_of(const mw_kvcache* c, int64_t chunk) {
   return (int)(chunk % c->S);
 }
 
+// sustained MFMA rate assumed by the split model of the e4m3 kernel
+constexpr double kFp8Flops = 1.4e15;
+
 static long long window_chunks(const mw_kvcache* c, int window) {
   const long long live = c->head - c->tail;
   return window < 0 ? live : window;
@@ -382,7 +423,9 @@ size_t mw_chunk_attn_cached_workspace_size(const mw_kvcache* c, int n_queued, in
   const long long tk = c->sink_len + w * c->L + tq;
   if (tq > kMaxT || tk > kMaxT) return 0;
   const int bh = c->B * c->H;
-  const int ns = mw::fwd_choose_splits(c->D, bh, (int)tq, (int)tk, (size_t)-1);
+  const int ns = c->elem_bytes == 1 ? mw::fwd_choose_splits_for(mw::fwd8_choice(), kFp8Flops, c->D, bh, (int)tq,
+                                                                (int)tk, (size_t)-1)
+                                    : mw::fwd_choose_splits(c->D, bh, (int)tq, (int)tk, (size_t)-1);
   return mw::fwd_split_bytes(c->D, bh, (int)tq, ns);
 }
 
@@ -393,6 +436,7 @@ int mw_chunk_attn_cached_strided(const void* q, const void* k_new, const void* v
   const char* fn = "mw_chunk_attn_cached";
   int st = check_cache(fn, c);
   if (st) return st;
+  if (c->elem_bytes != 2) return fail(MW_EINVAL, "%s: the cache holds e4m3 slots (use mw_chunk_attn_cached_fp8)", fn);
   st = check_ptrs(fn, {{"q", q}, {"k_new", k_new}, {"v_new", v_new}, {"o", o}});
   if (st) return st;
   if (lse != nullptr && !aligned16(lse)) return fail(MW_EALIGN, "%s: lse is not 16-byte aligned", fn);
@@ -457,6 +501,94 @@ int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new, in
                          void* workspace, size_t workspace_bytes, mw_stream_t stream) {
   return mw_chunk_attn_cached_strided(q, k_new, v_new, n_queued, q_len, c, window, flags, o, lse, scale, workspace,
                                       workspace_bytes, nullptr, stream);
+}
+
+int mw_quantize_fp8(const void* x, const mw_strides* x_strides, void* y, int B, int H, int T, int D, float scale,
+                    mw_stream_t stream) {
+  const char* fn = "mw_quantize_fp8";
+  int st = check_ptrs(fn, {{"x", x}, {"y", y}});
+  if (st) return st;
+  if (B < 1 || H < 1 || T < 1) return fail(MW_EINVAL, "%s: B, H and T must be >= 1 (got %d, %d, %d)", fn, B, H, T);
+  if (D != 64 && D != 72 && D != 128)
+    return fail(MW_EUNSUPPORTED, "%s: head dimension %d is not supported (64, 72 or 128)", fn, D);
+  if ((long long)B * H * T > (1LL << 32)) return fail(MW_EUNSUPPORTED, "%s: too many rows", fn);
+  if (!good_scale(scale)) return fail(MW_EINVAL, "%s: scale must be finite and > 0", fn);
+  const float inv = 1.f / scale;
+  if (!std::isfinite(inv) || inv == 0.f) return fail(MW_EINVAL, "%s: 1 / scale is not a finite non-zero fp32", fn);
+  mw::Strides sx = contiguous(H, T, D);
+  if (x_strides != nullptr) {
+    st = check_view(fn, "x", *x_strides, B, H, T, D, false);
+    if (st) return st;
+    sx = to_internal(*x_strides);
+  }
+  mw::QuantJobs jobs{};
+  jobs.j[0] = {static_cast<const uint16_t*>(x), sx, static_cast<uint8_t*>(y), inv};
+  return hip_status(fn, mw::launch_quantize_fp8(jobs, 1, B, H, T, D, static_cast<hipStream_t>(stream)));
+}
+
+int mw_chunk_attn_cached_fp8(const void* q8, const void* k8_new, const void* v8_new, int n_queued, int q_len,
+                             const mw_kvcache* c, int window, int flags, void* o, float* lse, float scale,
+                             float q_scale, void* workspace, size_t workspace_bytes, const mw_strides* o_strides,
+                             mw_stream_t stream) {
+  const char* fn = "mw_chunk_attn_cached_fp8";
+  int st = check_cache(fn, c);
+  if (st) return st;
+  if (c->elem_bytes != 1) return fail(MW_EINVAL, "%s: the cache holds bf16 slots (use mw_chunk_attn_cached)", fn);
+  st = check_ptrs(fn, {{"q8", q8}, {"k8_new", k8_new}, {"v8_new", v8_new}, {"o", o}});
+  if (st) return st;
+  if (lse != nullptr && !aligned16(lse)) return fail(MW_EALIGN, "%s: lse is not 16-byte aligned", fn);
+  if (workspace != nullptr && !aligned16(workspace)) return fail(MW_EALIGN, "%s: workspace is not 16-byte aligned", fn);
+  if (n_queued < 1 || q_len < 1) return fail(MW_EINVAL, "%s: n_queued and q_len must be >= 1", fn);
+  if (flags != MW_QUEUED_CAUSAL && flags != MW_QUEUED_ISOLATED) return fail(MW_EINVAL, "%s: unknown flags %d", fn, flags);
+  if (!good_scale(scale)) return fail(MW_EINVAL, "%s: scale must be finite and > 0", fn);
+  if (!good_scale(q_scale)) return fail(MW_EINVAL, "%s: q_scale must be finite and > 0", fn);
+  const float cscale = scale * q_scale * c->k_scale * kLog2e;
+  if (!(cscale > 0.f) || !std::isfinite(cscale))
+    return fail(MW_EINVAL, "%s: scale * q_scale * k_scale is not a finite non-zero fp32", fn);
+  const long long live = c->head - c->tail;
+  if (window < -1) return fail(MW_EINVAL, "%s: window must be >= -1", fn);
+  const long long w = window_chunks(c, window);
+  if (w > live) return fail(MW_EINVAL, "%s: window %d exceeds the %lld live chunks", fn, window, live);
+  if (w > MW_MAX_WINDOW) return fail(MW_EUNSUPPORTED, "%s: window %lld exceeds %d", fn, w, MW_MAX_WINDOW);
+  if (n_queued > MW_MAX_QUEUED) return fail(MW_EUNSUPPORTED, "%s: n_queued %d exceeds %d", fn, n_queued, MW_MAX_QUEUED);
+  const long long nq_tok = (long long)n_queued * q_len;
+  if (nq_tok + w * c->L + c->sink_len > kMaxT) return fail(MW_EUNSUPPORTED, "%s: too many tokens", fn);
+  mw::Strides so = contiguous(c->H, (int)nq_tok, c->D);
+  if (o_strides != nullptr) {
+    st = check_view(fn, "o", *o_strides, c->B, c->H, (int)nq_tok, c->D, true);
+    if (st) return st;
+    so = to_internal(*o_strides);
+  }
+  mw::FwdParams p{};
+  p.q = static_cast<const uint16_t*>(q8);  // e4m3 bytes (see FwdParams)
+  p.k = static_cast<const uint16_t*>(k8_new);
+  p.v = static_cast<const uint16_t*>(v8_new);
+  p.o = static_cast<uint16_t*>(o);
+  p.lse = lse;
+  p.BH = c->B * c->H;
+  p.H = c->H;
+  p.Tq = (int)nq_tok;
+  p.vis_mode = flags == MW_QUEUED_CAUSAL ? 1 : 2;
+  p.L = c->L;
+  p.sink_len = c->sink_len;
+  p.k_sink = static_cast<const uint16_t*>(c->k_sink);
+  p.v_sink = static_cast<const uint16_t*>(c->v_sink);
+  p.wL = (int)(c->sink_len + w * c->L);
+  p.Tk = p.wL + p.Tq;
+  p.qlen = q_len;
+  p.scale_log2 = cscale;
+  p.scale_ln = scale;
+  p.k_slots = static_cast<const uint16_t*>(c->k_slots);
+  p.v_slots = static_cast<const uint16_t*>(c->v_slots);
+  p.slot_stride = (long long)c->B * c->H * c->L * c->D;  // bytes = elements
+  p.S = c->S;
+  p.first_slot = (int)((c->head - w) % c->S);
+  p.n_splits = mw::fwd_choose_splits_for(mw::fwd8_choice(), kFp8Flops, c->D, p.BH, p.Tq, p.Tk,
+                                         workspace != nullptr ? workspace_bytes : 0);
+  p.part = static_cast<float*>(workspace);
+  p.so = so;
+  p.o_scale = c->v_scale;
+  return hip_status(fn, mw::launch_fwd_fp8(p, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

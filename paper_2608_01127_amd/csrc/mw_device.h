@@ -281,6 +281,15 @@ __device__ __forceinline__ float sum_halves(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// XCD-aware order: consecutive workgroup ids are dealt round-robin to the 8
+// XCDs; remap so that each XCD receives one contiguous range of logical work
+// items (whole heads, heaviest query tiles first), which keeps a head's K/V in
+// one XCD's L2.
+__device__ __forceinline__ int xcd_remap(int bid, int n) {
+  if (n % 8) return bid;
+  return (bid % 8) * (n / 8) + bid / 8;
+}
+
 // Row (within a 32-row accumulator block) of accumulator register i in lane l.
 __device__ __forceinline__ int acc_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
 

@@ -49,6 +49,10 @@ struct FwdParams {
   // views of q, k (training keys / queued keys), v and o; lse and the ring
   // are always contiguous
   Strides sq, sk, sv, so;
+  // fp8 kernel only: q, k, v, the slots and the sink hold e4m3 bytes
+  // (contiguous; element strides are byte strides) and O is multiplied by
+  // o_scale (the V scale) before it is stored
+  float o_scale;
 };
 
 struct BwdParams {
@@ -90,6 +94,26 @@ struct FwdChoice {
   int wg_per_cu;
 };
 FwdChoice fwd_choice(int D, bool cached, int Tq);
+// fp8 (e4m3) cached attention at D = 128: its tile configuration and launcher
+// (FwdParams as described above), and the merge of split partials (D = 128).
+FwdChoice fwd8_choice();
+hipError_t launch_fwd_fp8(FwdParams p, hipStream_t stream);
+hipError_t launch_combine(const FwdParams& p, int D, hipStream_t stream);
+// bf16 view -> contiguous e4m3, code = RNE(clamp(x * inv_scale, +-448)); up to
+// two jobs of the same shape in one launch.
+struct QuantJob {
+  const uint16_t* x;
+  Strides sx;
+  uint8_t* y;
+  float inv_scale;
+};
+struct QuantJobs {
+  QuantJob j[2];
+};
+hipError_t launch_quantize_fp8(const QuantJobs& jobs, int n_jobs, int B, int H, int T, int D, hipStream_t stream);
+// Split count for a cached call run by the configuration `ch` at `flops`
+// FLOP/s of sustained MFMA throughput.
+int fwd_choose_splits_for(const FwdChoice& ch, double flops, int D, int BH, int Tq, int Tk, size_t ws_bytes);
 // Split count the cached launcher uses for this shape given `ws_bytes` of
 // workspace (1 = no split), and the workspace bytes a split count needs.
 int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes);

@@ -8,6 +8,15 @@ import synth
 MAX_ABS = 2e-2
 MEAN_ABS = 2e-3
 
+# fp8 (e4m3) cached attention vs the fp64 oracle on the dequantized codes.  The
+# kernel's only rounding beyond fp32 is that of the probabilities to e4m3
+# before the PV product: a relative error of at most 2^-4 per weight (about
+# 0.036 rms), so an output element moves by about 0.036 * sqrt(sum p^2 (v -
+# o)^2) / sum p, which for unit-variance values over >= 64 visible keys is
+# below 4e-3 on average and 2e-2 at the tails.  Bar: 2.5x the bf16 one.
+FP8_MAX_ABS = 5e-2
+FP8_MEAN_ABS = 5e-3
+
 
 def to_gpu(bits, device="cuda"):
     import torch
@@ -41,3 +50,14 @@ def assert_close(name, got, ref, max_abs=MAX_ABS, mean_abs=MEAN_ABS):
 def bits_equal(a, b) -> bool:
     import torch
     return torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def to_gpu_u8(codes, device="cuda"):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(codes, dtype=np.uint8)).to(device)
+
+
+def amax_scale(bits) -> float:
+    """Per-tensor e4m3 scale that maps the tensor's largest magnitude to 448 (fp32)."""
+    return float(np.float32(np.abs(synth.bf16_bits_to_f64(bits)).max() / 448.0))
+

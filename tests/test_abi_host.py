@@ -36,9 +36,10 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_struct_layout_matches_header():
-    assert ctypes.sizeof(_lib.mw_kvcache) == 80
+    assert ctypes.sizeof(_lib.mw_kvcache) == 88
     assert _lib.mw_kvcache.head.offset == 40 and _lib.mw_kvcache.tail.offset == 48
     assert _lib.mw_kvcache.k_sink.offset == 56 and _lib.mw_kvcache.sink_len.offset == 72
+    assert _lib.mw_kvcache.elem_bytes.offset == 76 and _lib.mw_kvcache.v_scale.offset == 84
     assert ctypes.sizeof(_lib.mw_rope) == 12
 
 
@@ -249,3 +250,57 @@ def test_missing_library_fails_loudly(tmp_path):
             _lib.load(str(tmp_path / "nope.so"))
     finally:
         _lib._lib = saved
+
+
+def test_fp8_validation():
+    """e4m3 cache, quantizer and fp8 attention reject bad arguments before any launch."""
+    lib = mw.load()
+    c = _lib.mw_kvcache()
+    init8 = lib.mw_kvcache_init_fp8
+    assert init8(None, A, A, 4, 1, 2, 16, 128, 1.0, 1.0) == mw.MW_EINVAL
+    assert init8(ctypes.byref(c), A, A, 4, 1, 2, 16, 64, 1.0, 1.0) == mw.MW_EUNSUPPORTED
+    assert init8(ctypes.byref(c), A, A, 4, 1, 2, 16, 128, 0.0, 1.0) == mw.MW_EINVAL
+    assert init8(ctypes.byref(c), A, A, 4, 1, 2, 16, 128, 1.0, float("inf")) == mw.MW_EINVAL
+    assert init8(ctypes.byref(c), A, U, 4, 1, 2, 16, 128, 1.0, 1.0) == mw.MW_EALIGN
+    assert init8(ctypes.byref(c), A, A, 4, 1, 2, 16, 128, 0.5, 0.25) == mw.MW_OK
+    assert (c.elem_bytes, c.k_scale, c.v_scale, c.D) == (1, 0.5, 0.25, 128)
+    b = new_cache(S=4, B=1, H=2, L=16, D=128)
+    assert (b.elem_bytes, b.k_scale, b.v_scale) == (2, 1.0, 1.0)
+    rope = _lib.mw_rope(0, 44, 10000.0)
+    c.head = 2
+    assert lib.mw_kvcache_rope_shift(ctypes.byref(c), 3, ctypes.byref(rope), None) == mw.MW_EUNSUPPORTED
+    cached = lambda cache, *a: lib.mw_chunk_attn_cached(A, A, A, 2, 16, ctypes.byref(cache), 1, 0, A, None, 0.125,
+                                                        None, 0, None)
+    assert cached(c) == mw.MW_EINVAL and "e4m3" in err()
+    f8 = lambda cache, *a: lib.mw_chunk_attn_cached_fp8(*a[:3], 2, 16, ctypes.byref(cache), *a[3:], None, 0, None,
+                                                        None)
+    b.head = 2
+    assert f8(b, A, A, A, 1, 0, A, None, 0.125, 1.0) == mw.MW_EINVAL and "bf16" in err()
+    assert f8(c, A, A, A, 1, 0, A, None, 0.125, 0.0) == mw.MW_EINVAL and "q_scale" in err()
+    assert f8(c, A, A, A, 1, 0, A, None, -1.0, 1.0) == mw.MW_EINVAL
+    assert f8(c, None, A, A, 1, 0, A, None, 0.125, 1.0) == mw.MW_EINVAL
+    assert f8(c, A, U, A, 1, 0, A, None, 0.125, 1.0) == mw.MW_EALIGN
+    assert f8(c, A, A, A, 3, 0, A, None, 0.125, 1.0) == mw.MW_EINVAL and "window" in err()
+    assert f8(c, A, A, A, 1, 5, A, None, 0.125, 1.0) == mw.MW_EINVAL
+    assert lib.mw_chunk_attn_cached_fp8(A, A, A, 2, 16, ctypes.byref(c), 1, 0, A, None, 0.125, 1.0, None, 0,
+                                        strides((0, 0, 128)), None) == mw.MW_EINVAL  # overlapping output view
+    c.elem_bytes = 3                                                    # a corrupt descriptor
+    assert f8(c, A, A, A, 1, 0, A, None, 0.125, 1.0) == mw.MW_EINVAL and "corrupt" in err()
+    q = lib.mw_quantize_fp8
+    assert q(None, None, A, 1, 2, 16, 128, 1.0, None) == mw.MW_EINVAL
+    assert q(A, None, U, 1, 2, 16, 128, 1.0, None) == mw.MW_EALIGN
+    assert q(A, None, A, 1, 2, 16, 96, 1.0, None) == mw.MW_EUNSUPPORTED
+    assert q(A, None, A, 0, 2, 16, 128, 1.0, None) == mw.MW_EINVAL
+    assert q(A, None, A, 1, 2, 16, 128, 0.0, None) == mw.MW_EINVAL
+    assert q(A, None, A, 1, 2, 16, 128, 1e-39, None) == mw.MW_EINVAL   # 1 / scale overflows fp32
+    assert q(A, strides((2 * 16 * 128, 16 * 128, 100)), A, 1, 2, 16, 128, 1.0, None) == mw.MW_EINVAL
+
+
+def test_fp8_workspace_size_policy():
+    lib = mw.load()
+    c = _lib.mw_kvcache()
+    assert lib.mw_kvcache_init_fp8(ctypes.byref(c), A, A, 8, 1, 16, 2640, 128, 0.02, 0.02) == mw.MW_OK
+    c.head = 6
+    small = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 1, 128, 6)
+    assert small % (16 * 128 * 130 * 4) == 0 and small // (16 * 128 * 130 * 4) >= 8
+

@@ -1,0 +1,191 @@
+"""GPU parity of the fp8 (e4m3) inference variant: the quantizer and the quantize-on-commit of
+an e4m3 ring bit-exact against oracle/fp8.py, and the e4m3 cached chunk attention (Sec. 3.5
+attention, quantized as Sec. 6 suggests) against the fp64 oracle on the dequantized codes."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from helpers import (FP8_MAX_ABS, FP8_MEAN_ABS, amax_scale, assert_close, bits_equal, f64, to_f64, to_gpu,
+                     to_gpu_u8)
+
+pytestmark = pytest.mark.gpu
+
+
+def sync():
+    import torch
+    torch.cuda.synchronize()
+
+
+def codes(bits, scale):
+    return oracle.quantize_fp8(synth.bf16_bits_to_f32(bits), scale)
+
+
+def u8(t):
+    return t.detach().cpu().numpy().astype(np.uint8)
+
+
+@pytest.mark.parametrize("shape,scale,mag,bthd", [
+    ((1, 2, 100, 128), 1.0, 1.0, False),
+    ((2, 3, 37, 64), 0.0123, 1.0, False),
+    ((1, 2, 50, 72), 2.0 ** -5, 4.0, True),        # a [B,T,H,D] view
+    ((1, 1, 64, 128), 0.5, 300.0, False),           # many values saturate at +-448 codes
+])
+def test_quantize_bit_exact(mw, shape, scale, mag, bthd):
+    B, H, T, D = shape
+    print(f"[case] quantize {shape} scale={scale} mag={mag} bthd={bthd}", flush=True)
+    bits = synth.random_bf16(shape, 9100 + T, scale=mag)
+    x = to_gpu(bits)
+    if bthd:
+        x = to_gpu(np.ascontiguousarray(np.swapaxes(bits, 1, 2))).transpose(1, 2)   # [B,H,T,D] view of [B,T,H,D]
+    y = mw.mw_quantize_fp8(x, scale)
+    sync()
+    ref = codes(bits, scale)
+    got = u8(y)
+    assert got.shape == ref.shape
+    assert np.array_equal(got, ref), f"{int((got != ref).sum())} codes differ"
+
+
+def test_fp8_append_quantizes_into_the_slot(mw):
+    """Quantize-on-commit: slot contents bit-exact with the oracle's codes at the cache's scales,
+    for contiguous and [B,T,H,D] chunks; the ring bookkeeping is the bf16 ring's."""
+    B, H, L, D, S = 1, 3, 80, 128, 3
+    ks, vs = 0.013, 0.021
+    cache = mw.KVCache(S, B, H, L, D, fp8=True, k_scale=ks, v_scale=vs)
+    ring = oracle.RingModel(S)
+    for i in range(5):
+        kb, vb = (synth.normal_bf16((B, H, L, D), 9200 + 2 * i + j) for j in range(2))
+        if ring.live == S:
+            ring.evict(1)
+            mw.mw_kvcache_evict(cache, 1)
+        if i % 2:
+            kc = to_gpu(np.ascontiguousarray(np.swapaxes(kb, 1, 2))).transpose(1, 2)
+            vc = to_gpu(np.ascontiguousarray(np.swapaxes(vb, 1, 2))).transpose(1, 2)
+        else:
+            kc, vc = to_gpu(kb), to_gpu(vb)
+        slot = mw.mw_kvcache_append(cache, kc, vc)
+        assert slot == ring.append()
+        sync()
+        assert np.array_equal(u8(cache.k_slots[slot]), codes(kb, ks))
+        assert np.array_equal(u8(cache.v_slots[slot]), codes(vb, vs))
+    with pytest.raises(mw.MWError):
+        mw.mw_kvcache_rope_shift(cache, 2, 0, 44)
+
+
+def run_fp8_case(mw, B, H, L, S, n_commit, window, nq, qlen, mode, split, sink_len=0, seed=0):
+    """Quantize everything on the GPU, run the e4m3 cached attention, return it with the oracle's
+    results on the dequantized codes and on the original bf16 values."""
+    D = 128
+    hist = [(synth.normal_bf16((B, H, L, D), seed + 2 * i), synth.normal_bf16((B, H, L, D), seed + 2 * i + 1))
+            for i in range(n_commit)]
+    inp = {n: synth.normal_bf16((B, H, nq * qlen, D), seed + 900 + i) for i, n in enumerate(("q", "k", "v"))}
+    sink = [synth.normal_bf16((B, H, sink_len, D), seed + 950 + i) for i in range(2)] if sink_len else None
+    allk = [c[0] for c in hist] + [inp["k"]] + ([sink[0]] if sink else [])
+    allv = [c[1] for c in hist] + [inp["v"]] + ([sink[1]] if sink else [])
+    ks = amax_scale(np.concatenate([a.ravel() for a in allk]))
+    vs = amax_scale(np.concatenate([a.ravel() for a in allv]))
+    qs = amax_scale(inp["q"])
+    cache = mw.KVCache(S, B, H, L, D, fp8=True, k_scale=ks, v_scale=vs)
+    ring = oracle.RingModel(S)
+    for kc, vc in hist:
+        if ring.live == S:
+            ring.evict(1)
+            mw.mw_kvcache_evict(cache, 1)
+        mw.mw_kvcache_append(cache, to_gpu(kc), to_gpu(vc))
+        ring.append()
+    if sink:
+        gsk, gsv = mw.mw_quantize_fp8(to_gpu(sink[0]), ks), mw.mw_quantize_fp8(to_gpu(sink[1]), vs)
+        cache.set_sink(gsk, gsv)
+    q8 = mw.mw_quantize_fp8(to_gpu(inp["q"]), qs)
+    k8 = mw.mw_quantize_fp8(to_gpu(inp["k"]), ks)
+    v8 = mw.mw_quantize_fp8(to_gpu(inp["v"]), vs)
+    o, lse = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, nq, qlen, cache, qs, window=window, flags=mode, want_lse=True,
+                                         split=split)
+    sync()
+    assert np.array_equal(u8(q8), codes(inp["q"], qs)) and np.array_equal(u8(k8), codes(inp["k"], ks))
+    win = ring.window(None if window == -1 else window)
+    dq = lambda b, s: oracle.dequantize_fp8(codes(b, s), s)
+    ro, rl = oracle.cached_chunk_attn(dq(inp["q"], qs), dq(inp["k"], ks), dq(inp["v"], vs),
+                                      [dq(hist[c][0], ks) for c in win], [dq(hist[c][1], vs) for c in win], nq, qlen,
+                                      mode=mode, sink_k=dq(sink[0], ks) if sink else None,
+                                      sink_v=dq(sink[1], vs) if sink else None)
+    rb, _ = oracle.cached_chunk_attn(f64(inp["q"]), f64(inp["k"]), f64(inp["v"]), [f64(hist[c][0]) for c in win],
+                                     [f64(hist[c][1]) for c in win], nq, qlen, mode=mode,
+                                     sink_k=f64(sink[0]) if sink else None, sink_v=f64(sink[1]) if sink else None)
+    return o, lse, ro, rl, rb
+
+
+@pytest.mark.parametrize("split", [True, False])
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("B,H,L,S,n_commit,window,nq,qlen,sink_len", [
+    (1, 2, 96, 4, 6, 3, 2, 96, 0),       # wrapped ring, chunk edges inside tiles
+    (2, 1, 160, 5, 5, -1, 3, 160, 0),    # all live chunks, batch 2
+    (1, 2, 100, 3, 2, 0, 2, 70, 0),      # empty window: block-causal attention of the queued chunks
+    (1, 1, 64, 8, 9, 7, 4, 33, 0),       # short queued chunks
+    (1, 2, 120, 4, 4, 3, 3, 120, 40),    # with a sink
+])
+def test_fp8_cached_attention_vs_oracle(mw, split, mode, B, H, L, S, n_commit, window, nq, qlen, sink_len):
+    print(f"[case] fp8 cached split={split} mode={mode} B={B} H={H} L={L} S={S} commits={n_commit} w={window} "
+          f"nq={nq} qlen={qlen} sink={sink_len}", flush=True)
+    o, lse, ro, rl, rb = run_fp8_case(mw, B, H, L, S, n_commit, window, nq, qlen, mode, split, sink_len,
+                                      seed=9300 + L + qlen)
+    assert_close("o (vs dequantized)", to_f64(o), ro, FP8_MAX_ABS, FP8_MEAN_ABS)
+    assert_close("lse", to_f64(lse), rl, max_abs=2e-3, mean_abs=2e-4)
+    # end to end (input quantization included) against the unquantized inputs: a looser sanity bar
+    assert_close("o (vs bf16 inputs)", to_f64(o), rb, 0.25, 0.025)
+
+
+def test_fp8_wraparound_invariance_and_determinism(mw):
+    """The same window content at two ring offsets gives bit-identical output; reruns too."""
+    import torch
+    B, H, L, D, nq = 1, 2, 128, 128, 2
+    outs = []
+    for S, pre in ((4, 0), (5, 3)):
+        cache = mw.KVCache(S, B, H, L, D, fp8=True, k_scale=0.01, v_scale=0.01)
+        for i in range(pre):     # filler chunks, evicted again, to move the ring offset
+            mw.mw_kvcache_append(cache, to_gpu(synth.normal_bf16((B, H, L, D), 9500 + i)),
+                                 to_gpu(synth.normal_bf16((B, H, L, D), 9600 + i)))
+        mw.mw_kvcache_evict(cache, pre)
+        for i in range(3):
+            mw.mw_kvcache_append(cache, to_gpu(synth.normal_bf16((B, H, L, D), 9700 + i)),
+                                 to_gpu(synth.normal_bf16((B, H, L, D), 9800 + i)))
+        q8, k8, v8 = (mw.mw_quantize_fp8(to_gpu(synth.normal_bf16((B, H, nq * L, D), 9900 + i)), 0.01)
+                      for i in range(3))
+        for _ in range(2):
+            o, _ = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, nq, L, cache, 0.01, window=3, split=False)
+            outs.append(o.clone())
+    sync()
+    assert all(bits_equal(outs[0], x) for x in outs[1:])
+    assert torch.isfinite(outs[0].float()).all()
+
+
+@pytest.mark.parametrize("window", [24, 6])
+def test_fp8_paper_1b_streaming(mw, window):
+    """MiniWorld-1B streaming shape in e4m3: CFG batch 2, 12 heads of 128, 8 in-flight 600-token
+    chunks over `window` cached chunks and a 300-token sink; heads (0,0) and (1,11) vs the oracle."""
+    import torch
+    B, H, D, L, nq, sink_len = 2, 12, 128, 600, 8, 300
+    print(f"[case] fp8 paper 1B streaming window={window}", flush=True)
+    ks, vs, qs = 0.011, 0.012, 0.0105
+    cache = mw.KVCache(window + 1, B, H, L, D, fp8=True, k_scale=ks, v_scale=vs)
+    hist = [(synth.normal_bf16((B, H, L, D), 9400 + 2 * i), synth.normal_bf16((B, H, L, D), 9401 + 2 * i))
+            for i in range(window)]
+    for kc, vc in hist:
+        mw.mw_kvcache_append(cache, to_gpu(kc), to_gpu(vc))
+    sk, sv = (synth.normal_bf16((B, H, sink_len, D), 9390 + i) for i in range(2))
+    cache.set_sink(mw.mw_quantize_fp8(to_gpu(sk), ks), mw.mw_quantize_fp8(to_gpu(sv), vs))
+    inp = {n: synth.normal_bf16((B, H, nq * L, D), 9380 + i) for i, n in enumerate(("q", "k", "v"))}
+    q8 = mw.mw_quantize_fp8(to_gpu(inp["q"]), qs)
+    k8 = mw.mw_quantize_fp8(to_gpu(inp["k"]), ks)
+    v8 = mw.mw_quantize_fp8(to_gpu(inp["v"]), vs)
+    o_bthd = torch.empty((B, nq * L, H, D), dtype=torch.bfloat16, device="cuda")
+    o, _ = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, nq, L, cache, qs, out=o_bthd.transpose(1, 2))
+    sync()
+    dq = lambda b, s: oracle.dequantize_fp8(codes(b, s), s)
+    heads = [(0, 0), (1, 11)]
+    ro, _ = oracle.cached_chunk_attn(dq(inp["q"], qs), dq(inp["k"], ks), dq(inp["v"], vs),
+                                     [dq(c[0], ks) for c in hist], [dq(c[1], vs) for c in hist], nq, L, heads=heads,
+                                     sink_k=dq(sk, ks), sink_v=dq(sv, vs))
+    go = to_f64(o.contiguous())
+    for b, h in heads:
+        assert_close(f"o b{b} h{h}", go[b, h], ro[b, h], FP8_MAX_ABS, FP8_MEAN_ABS)
