@@ -439,11 +439,13 @@ __global__ __launch_bounds__(256) void quantize_fp8_kernel(QuantJobs jobs, int H
 }
 
 // Tile configuration: 8 waves of one 32-row block (256 queries; one workgroup
-// per CU at 166 registers), 64 keys per step.
+// per CU), 128 keys per step.  Measured on the streaming shapes: 128 keys per
+// step 12-15% faster than 64; two row blocks per wave (4 waves, one per SIMD)
+// 30% slower; 192 keys within 2%.
 struct Fwd8Cfg {
   static constexpr int NW = 8;
   static constexpr int RB = 1;
-  static constexpr int BN = 64;
+  static constexpr int BN = 128;
 };
 
 }  // namespace
