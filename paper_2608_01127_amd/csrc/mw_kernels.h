@@ -96,7 +96,7 @@ struct FwdChoice {
 FwdChoice fwd_choice(int D, bool cached, int Tq);
 // fp8 (e4m3) cached attention at D = 128: its tile configuration and launcher
 // (FwdParams as described above), and the merge of split partials (D = 128).
-FwdChoice fwd8_choice();
+FwdChoice fwd8_choice(int Tq);
 hipError_t launch_fwd_fp8(FwdParams p, hipStream_t stream);
 hipError_t launch_combine(const FwdParams& p, int D, hipStream_t stream);
 // bf16 view -> contiguous e4m3, code = RNE(clamp(x * inv_scale, +-448)); up to
