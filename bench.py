@@ -123,7 +123,7 @@ def cpu_baseline(target_s: float):
 
 
 def decode_shapes(mw, torch, cache, st, dev, reps=20):
-    """Cache-bound shapes: one queued chunk of q_len tokens over the full window
+    """Cache-bound shapes: one queued chunk of 64 / 128 / 256 / 512 tokens over the full window
     (6 committed chunks of 2640 tokens, B1 H16 D128).  Each timed call is
     preceded by a 512 MB read (a sum) that evicts the 256 MB Infinity Cache, so
     the window's K/V come from HBM; a read leaves no dirty lines whose
@@ -132,7 +132,7 @@ def decode_shapes(mw, torch, cache, st, dev, reps=20):
     out = []
     flush = torch.ones(128 << 20, dtype=torch.float32, device=dev)
     g = torch.Generator(device=dev).manual_seed(1234)
-    for ql in (64, 128, 256):
+    for ql in (64, 128, 256, 512):
         q, kn, vn = (torch.randn(st.B, st.H, ql, st.D, device=dev, generator=g).to(torch.bfloat16) for _ in range(3))
         o = torch.empty_like(q)
         ws = torch.empty(max(16, mw.mw_chunk_attn_cached_workspace_size(cache, 1, ql, st.window)), dtype=torch.uint8,

@@ -453,6 +453,9 @@ struct FwdCfg {
 // bound by streaming the window from HBM.  Eight waves split into key groups
 // (4 groups of 2 row waves for 64 rows, 2 groups of 4 for 128 rows) stage 128
 // keys per step, so every SIMD of the CU has two waves at work on the rows.
+// Up to 512 queued rows run as 128-row tiles of this kind (their workgroups read
+// the same window, which the L2 and the Infinity Cache share): measured 20% and
+// 11% faster than 256-row tiles at 256 and 512 rows over a 6 x 2640-token window.
 template <int D, int NWR>
 struct FwdDecodeCfg {
   static constexpr int NW = 8;
@@ -574,7 +577,7 @@ hipError_t launch_fwd_decode_128(const FwdParams& p, int bm, hipStream_t stream)
 // Must agree with the dispatch in launch_fwd_128.
 FwdChoice fwd_choice(int D, bool cached, int Tq) {
   if (cached && D == 128 && Tq <= 64) return {64, 1};
-  if (cached && D == 128 && Tq <= 128) return {128, 1};
+  if (cached && D == 128 && Tq <= 512) return {128, 1};  // several 128-row tiles up to 512 rows
   if (D == 64) return {32 * FwdCfg<64>::RB * FwdCfg<64>::NW, 3};
   if (D == 72) return {32 * FwdCfg<72>::RB * FwdCfg<72>::NW, 2};
   return {32 * FwdCfg<128>::RB * FwdCfg<128>::NW, 2};

@@ -165,7 +165,7 @@ def test_ring_errors_and_slots(mw):
     assert cache.slot_of(0) == -1
 
 
-@pytest.mark.parametrize("q_len", [64, 128, 256])
+@pytest.mark.parametrize("q_len", [64, 128, 256, 300, 512])
 def test_decode_shape_split_vs_oracle(mw, q_len):
     """One short queued chunk over a full 6-chunk window (B1 H16 D128, 2640-token chunks):
     few query tiles, so the key range is split over many workgroups."""
@@ -197,6 +197,7 @@ def test_decode_shape_split_vs_oracle(mw, q_len):
     (2, 1, 200, 5, 5, 4, 3, 40, 17),    # 120 rows, three queued chunks, sink of 17 tokens
     (1, 1, 96, 3, 4, 2, 1, 7, 0),       # 7 rows, window shorter than one 128-key step
     (1, 2, 130, 4, 6, -1, 2, 33, 5),    # all live chunks, ragged 66 rows, sink
+    (1, 2, 200, 4, 5, 3, 3, 100, 9),    # 300 rows: three 128-row tiles of two key groups, sink
 ])
 def test_few_rows_key_groups_vs_oracle(mw, split, mode, B, H, L, S, n_commit, window, nq, qlen, sink_len):
     """Cached attention with at most 128 queued rows (D=128), the configuration whose waves
