@@ -2,8 +2,8 @@
 // paper Sec. 3.2's attention, with P recomputed from Q, K and the forward LSE.
 //
 //   delta kernel : Delta_i = sum_d dO_id O_id                    (HBM-bound)
-//   dK/dV kernel : one workgroup owns 128 keys (32 per wave, K and V held in
-//                  registers); it walks the query tiles that can see those
+//   dK/dV kernel : one workgroup owns 128 or 256 keys (32 or 64 per wave, K and
+//                  V held in registers); it walks the query tiles that can see those
 //                  keys -- queries of the same or a later chunk -- staging Q,
 //                  dO, LSE and Delta in LDS.  Per 32 queries and wave:
 //                    S = Q K^T, dP = dO V^T     (keys on the lane axis)
@@ -23,8 +23,10 @@
 
 namespace mw {
 
-// Row terms of the backward pass: Delta = rowsum(dO * O) and LSE scaled to
-// base 2 (LSE * log2 e), one 16-byte chunk per thread, reduced over the row's lanes.
+// Row terms of the backward pass: -Delta = -rowsum(dO * O) and LSE scaled to
+// base 2 (LSE * log2 e), one 16-byte chunk per thread, reduced over the row's
+// lanes.  Delta is stored negated: the dP products start from it (their MFMA
+// accumulator input), so dP - Delta costs no instruction.
 // CPR lanes per row (a power of two); at D = 72 the 9 pieces of a row leave
 // lanes 9..15 of its group idle.
 template <int D>
@@ -49,17 +51,21 @@ __global__ __launch_bounds__(256) void bwd_rowterms_kernel(BwdParams p, long lon
 #pragma unroll
   for (int w = CPR / 2; w >= 1; w >>= 1) acc += __shfl_xor(acc, w);
   if (row < n_rows && c == 0) {
-    p.delta[row] = acc;
+    p.delta[row] = -acc;
     p.lse2[row] = p.lse[row] * 1.4426950408889634f;
   }
 }
 
-// D = 128 keeps 192 registers of per-wave state (K and V fragments, dK and dV
-// accumulators) and runs one wave per SIMD with the full register file; D = 64
-// fits two waves per SIMD.
-template <int D, int NW, int BM>
-__global__ __launch_bounds__(64 * NW, (D == 128 ? 4 : 8) / NW) void bwd_dkdv_kernel(BwdParams p, int n_ktiles) {
-  constexpr int BN = 32 * NW, NT = 64 * NW;
+// NW waves, each owning KBW blocks of 32 keys (K and V fragments and the dK,
+// dV accumulators in registers).  With KBW = 2 every Q and dO fragment read
+// from LDS feeds two MFMAs (one per key block), halving the LDS reads per
+// MFMA, which otherwise bound this kernel (one 16-byte row read or two
+// transposing reads per MFMA); the register state then needs the full
+// register file of one wave per SIMD, as D = 128 does with one key block.
+template <int D, int NW, int BM, int KBW>
+__global__ __launch_bounds__(64 * NW, (D == 128 || KBW > 1 ? 4 : 8) / NW) void bwd_dkdv_kernel(BwdParams p,
+                                                                                            int n_ktiles) {
+  constexpr int BN = 32 * NW * KBW, NT = 64 * NW;
   static_assert(BM % 64 == 0, "row terms are staged 64 at a time");
   constexpr int KK = (D + 15) / 16, DB = (D + 31) / 32;  // D = 72: 80 and 96 columns
   constexpr int TE = stage_elems<D, BM, NT>();
@@ -74,39 +80,45 @@ __global__ __launch_bounds__(64 * NW, (D == 128 ? 4 : 8) / NW) void bwd_dkdv_ker
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int T = p.T, L = p.L;
   const int k0 = kt * BN;
-  const int mykey = k0 + wave * 32 + (lane & 31);
   const int bi = bh / p.H, hi = bh - bi * p.H;
   const long long qb_ = bi * p.sq.b + hi * p.sq.h, dob_ = bi * p.sdo.b + hi * p.sdo.h;
   const float* lse2_bh = p.lse2 + (long long)bh * T;
   const float* dlt_bh = p.delta + (long long)bh * T;
 
-  // K and V fragments: B operands of S = Q K^T and dP = dO V^T.  Keys past T
-  // read the last key; their dK/dV are never stored.
-  bf16x8 kf[KK], vf[KK];
-  {
-    const long long kr = min(mykey, T - 1);
+  // Per key block: this lane's key, the first query that sees it, and its K and
+  // V fragments (B operands of S = Q K^T and dP = dO V^T).  Keys past T read
+  // the last key; their dK/dV are never stored.
+  int mykey[KBW], qvis[KBW];
+  bf16x8 kf[KBW][KK], vf[KBW][KK];
+#pragma unroll
+  for (int kb = 0; kb < KBW; ++kb) {
+    mykey[kb] = k0 + (wave * KBW + kb) * 32 + (lane & 31);
+    const long long kr = min(mykey[kb], T - 1);
+    qvis[kb] = ((int)kr / L) * L;
     const bf16_t* ka = p.k + bi * p.sk.b + hi * p.sk.h + kr * p.sk.t + 8 * (lane >> 5);
     const bf16_t* va = p.v + bi * p.sv.b + hi * p.sv.h + kr * p.sv.t + 8 * (lane >> 5);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       if (D % 16 == 0 || 16 * kk + 8 * (lane >> 5) < D) {
-        kf[kk] = *reinterpret_cast<const bf16x8*>(ka + 16 * kk);
-        vf[kk] = *reinterpret_cast<const bf16x8*>(va + 16 * kk);
+        kf[kb][kk] = *reinterpret_cast<const bf16x8*>(ka + 16 * kk);
+        vf[kb][kk] = *reinterpret_cast<const bf16x8*>(va + 16 * kk);
       } else {  // columns past D (D = 72): zeros
 #pragma unroll
-        for (int j = 0; j < 8; ++j) kf[kk][j] = vf[kk][j] = (__bf16)0.f;
+        for (int j = 0; j < 8; ++j) kf[kb][kk][j] = vf[kb][kk][j] = (__bf16)0.f;
       }
     }
   }
-  f32x16 dv[DB], dk[DB];
+  f32x16 dv[KBW][DB], dk[KBW][DB];
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    dv[db] = zero16();
-    dk[db] = zero16();
+  for (int kb = 0; kb < KBW; ++kb) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      dv[kb][db] = zero16();
+      dk[kb][db] = zero16();
+    }
   }
 
   const int klast = min(k0 + BN, T) - 1;
-  const int qvis = (min(mykey, T - 1) / L) * L;  // first query that sees mykey
   const int qstart = ((k0 / L) * L / BM) * BM;  // first query tile with a query of chunk >= chunk(k0)
   const float c = p.scale_log2;
 
@@ -119,7 +131,7 @@ __global__ __launch_bounds__(64 * NW, (D == 128 ? 4 : 8) / NW) void bwd_dkdv_ker
       stage_rows_direct<D, BM, NT>(Qs[b], [&](int r) { return p.q + qb_ + min(q0 + r, T - 1) * p.sq.t; }, tid);
       stage_rows_direct<D, BM, NT>(dOs[b], [&](int r) { return p.d_o + dob_ + min(q0 + r, T - 1) * p.sdo.t; }, tid);
     }
-    // row terms of the tile: 64 fp32 per wave, LSE then Delta
+    // row terms of the tile: 64 fp32 per wave, LSE then -Delta
 #pragma unroll
     for (int c = wave; c < 2 * (BM / 64); c += NW) {
       const int part = c % (BM / 64);
@@ -136,38 +148,67 @@ __global__ __launch_bounds__(64 * NW, (D == 128 ? 4 : 8) / NW) void bwd_dkdv_ker
     const bf16_t* dOt = dOs[buf];
 #pragma unroll
     for (int qb = 0; qb < BM / 32; ++qb) {
-      f32x16 s = zero16(), dp = zero16();
+      // -Delta of the tile's rows in accumulator layout (register i: row
+      // 8(i/4) + 4(l/32) + i%4): the dP products accumulate onto it
+      f32x16 ndl;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dlt_s[buf][qb * 32 + 8 * g + 4 * (lane >> 5)]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) ndl[4 * g + j] = d4[j];
+      }
+      f32x16 s[KBW], dp[KBW];
+#pragma unroll
+      for (int kb = 0; kb < KBW; ++kb) {
+        s[kb] = zero16();
+        dp[kb] = ndl;
+      }
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        s = mfma32(lds_row8<D>(Qt, qb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), kf[kk], s);
-        dp = mfma32(lds_row8<D>(dOt, qb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5)), vf[kk], dp);
+        const bf16x8 qa = lds_row8<D>(Qt, qb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5));
+        const bf16x8 da = lds_row8<D>(dOt, qb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5));
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb) {
+          s[kb] = mfma32(qa, kf[kb][kk], s[kb]);
+          dp[kb] = mfma32(da, vf[kb][kk], dp[kb]);
+        }
       }
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int rr = qb * 32 + 8 * g + 4 * (lane >> 5);
         const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lse_s[buf][rr]);
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dlt_s[buf][rr]);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int i = 4 * g + j;
-          float pv = fast_exp2(fmaf(s[i], c, -l4[j]));
-          if constexpr (decltype(masked)::value) {
-            const int q = q0 + rr + j;
-            const bool ok = (q < T) & (q >= qvis);  // q in mykey's chunk or a later one
-            pv = ok ? pv : 0.f;
+#pragma unroll
+          for (int kb = 0; kb < KBW; ++kb) {
+            float pv = fast_exp2(fmaf(s[kb][i], c, -l4[j]));
+            if constexpr (decltype(masked)::value) {
+              const int q = q0 + rr + j;
+              const bool ok = (q < T) & (q >= qvis[kb]);  // q in the key's chunk or a later one
+              pv = ok ? pv : 0.f;
+            }
+            s[kb][i] = pv;
+            dp[kb][i] = pv * dp[kb][i];  // P (dP - Delta)
           }
-          s[i] = pv;
-          dp[i] = pv * (dp[i] - d4[j]);
         }
       }
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        const bf16x8 pb = pack8(s, t);
-        const bf16x8 dsb = pack8(dp, t);
+        bf16x8 pb[KBW], dsb[KBW];
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb) {
+          pb[kb] = pack8(s[kb], t);
+          dsb[kb] = pack8(dp[kb], t);
+        }
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          dv[db] = mfma32(lds_tr8<D>(dOt, qb * 32, t, db * 32, lane), pb, dv[db]);
-          dk[db] = mfma32(lds_tr8<D>(Qt, qb * 32, t, db * 32, lane), dsb, dk[db]);
+          const bf16x8 dot = lds_tr8<D>(dOt, qb * 32, t, db * 32, lane);
+#pragma unroll
+          for (int kb = 0; kb < KBW; ++kb) dv[kb][db] = mfma32(dot, pb[kb], dv[kb][db]);
+          const bf16x8 qt = lds_tr8<D>(Qt, qb * 32, t, db * 32, lane);
+#pragma unroll
+          for (int kb = 0; kb < KBW; ++kb) dk[kb][db] = mfma32(qt, dsb[kb], dk[kb][db]);
         }
       }
     }
@@ -195,9 +236,11 @@ __global__ __launch_bounds__(64 * NW, (D == 128 ? 4 : 8) / NW) void bwd_dkdv_ker
   run(std::false_type{}, min(qfe, T));
   run(std::true_type{}, T);
 
-  if (mykey < T) {
-    bf16_t* dkrow = p.dk + bi * p.sdk.b + hi * p.sdk.h + mykey * p.sdk.t;
-    bf16_t* dvrow = p.dv + bi * p.sdv.b + hi * p.sdv.h + mykey * p.sdv.t;
+#pragma unroll
+  for (int kb = 0; kb < KBW; ++kb) {
+    if (mykey[kb] >= T) continue;
+    bf16_t* dkrow = p.dk + bi * p.sdk.b + hi * p.sdk.h + mykey[kb] * p.sdk.t;
+    bf16_t* dvrow = p.dv + bi * p.sdv.b + hi * p.sdv.h + mykey[kb] * p.sdv.t;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
@@ -205,8 +248,8 @@ __global__ __launch_bounds__(64 * NW, (D == 128 ? 4 : 8) / NW) void bwd_dkdv_ker
         bf16x4 wk, wv;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          wk[j] = to_bf16(dk[db][4 * g + j] * p.scale);
-          wv[j] = to_bf16(dv[db][4 * g + j]);
+          wk[j] = to_bf16(dk[kb][db][4 * g + j] * p.scale);
+          wv[j] = to_bf16(dv[kb][db][4 * g + j]);
         }
         const int col = db * 32 + 8 * g + 4 * (lane >> 5);
         if (D % 32 != 0 && col >= D) continue;  // (D = 72)
@@ -237,7 +280,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
   const long long kb_ = bi * p.sk.b + hi * p.sk.h, vb_ = bi * p.sv.b + hi * p.sv.h;
 
   int qrow[RB], e1[RB];
-  float lse2[RB], dlt[RB];
+  float lse2[RB], ndlt[RB];  // LSE * log2 e and -Delta of this lane's query
   bf16x8 qf[RB][KK], df[RB][KK];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
@@ -256,7 +299,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
       }
     }
     lse2[rb] = p.lse2[(long long)bh * T + qc];
-    dlt[rb] = p.delta[(long long)bh * T + qc];
+    ndlt[rb] = p.delta[(long long)bh * T + qc];
     e1[rb] = min(T, (qc / L + 1) * L);
   }
   const int e1f = min(T, (q0 / L + 1) * L);
@@ -309,7 +352,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
             const int key = k0 + kb * 32 + acc_row(i, lane);
             pv = key < e1[rb] ? pv : 0.f;
           }
-          dp[rb][i] = pv * (dp[rb][i] - dlt[rb]);
+          dp[rb][i] = pv * (dp[rb][i] + ndlt[rb]);  // P (dP - Delta)
         }
       }
 #pragma unroll
@@ -370,6 +413,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
 template <int D>
 struct BwdCfg {
   static constexpr int NW_DKV = 4;
+  static constexpr int KBW_DKV = 1;  // 32-key blocks per wave of the dK/dV kernel (2 measured slower at D = 64)
   static constexpr int NW_DQ = 4;
   // 32-row query blocks per wave in the dQ kernel (two measured no faster at
   // D = 64 and spill at D = 128)
@@ -381,15 +425,15 @@ struct BwdCfg {
 template <int D>
 static hipError_t launch_bwd_d(const BwdParams& p, hipStream_t stream) {
   constexpr int NK = BwdCfg<D>::NW_DKV, NQ = BwdCfg<D>::NW_DQ, RQ = BwdCfg<D>::RB_DQ;
-  constexpr int BMK = BwdCfg<D>::BM_DKV, BNQ = BwdCfg<D>::BN_DQ;
+  constexpr int BMK = BwdCfg<D>::BM_DKV, BNQ = BwdCfg<D>::BN_DQ, KBW = BwdCfg<D>::KBW_DKV;
   const long long rows = (long long)p.BH * p.T;
   const long long threads = rows * (D == 64 ? 8 : 16);
   hipLaunchKernelGGL(bwd_rowterms_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p,
                      rows);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int nkt = (p.T + 32 * NK - 1) / (32 * NK);
-  hipLaunchKernelGGL((bwd_dkdv_kernel<D, NK, BMK>), dim3(nkt * p.BH), dim3(64 * NK), 0, stream, p, nkt);
+  const int nkt = (p.T + 32 * NK * KBW - 1) / (32 * NK * KBW);
+  hipLaunchKernelGGL((bwd_dkdv_kernel<D, NK, BMK, KBW>), dim3(nkt * p.BH), dim3(64 * NK), 0, stream, p, nkt);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int nqt = (p.T + 32 * RQ * NQ - 1) / (32 * RQ * NQ);

@@ -118,7 +118,7 @@ template <int ROWS, int NT>
 __device__ __forceinline__ void stage8_s(fp8_t* lds_tile, const fp8_t* tile, const RowOffsets8<ROWS, NT>& ro, int tid) {
 #pragma unroll
   for (int it = 0; it < RowOffsets8<ROWS, NT>::ROUNDS; ++it)
-    dma_lds_16_s(tile, ro.off[it], (MW_LDS void*)(lds_tile + (it * NT + (tid & ~63)) * 16));
+    dma_lds_16_s(tile, ro.off[it], lds_addr(lds_tile) + it * NT * 16 + wave_stage_off(tid));
 }
 
 struct RowPair8 {
@@ -133,9 +133,9 @@ __device__ __forceinline__ void stage8_rows(fp8_t* k_tile, fp8_t* v_tile, RowSrc
     const int row = ci >> 3;
     const int ls = (ci & 7) ^ Tile8::swz(row);
     const RowPair8 src = row_src(row);
-    const int dst = (it * NT + (tid & ~63)) * 16;  // wave-uniform base
-    dma_lds_16(src.k + 16 * ls, (MW_LDS void*)(k_tile + dst));
-    dma_lds_16(src.v + 16 * ls, (MW_LDS void*)(v_tile + dst));
+    const unsigned dst = it * NT * 16 + wave_stage_off(tid);  // wave-uniform
+    dma_lds_16(src.k + 16 * ls, lds_addr(k_tile) + dst);
+    dma_lds_16(src.v + 16 * ls, lds_addr(v_tile) + dst);
   }
 }
 

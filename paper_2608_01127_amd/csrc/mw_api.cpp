@@ -164,7 +164,7 @@ size_t mw_block_causal_attn_bwd_workspace_size(int B, int H, int T, int D) {
   (void)D;
   if (B < 1 || H < 1 || T < 1) return 0;
   const size_t bytes = (size_t)B * H * T * sizeof(float);
-  return 2 * ((bytes + 255) & ~(size_t)255);  // Delta and base-2 LSE, one fp32 per row each
+  return 2 * ((bytes + 255) & ~(size_t)255);  // -Delta and base-2 LSE, one fp32 per row each
 }
 
 int mw_block_causal_attn_bwd_strided(const void* q, const void* k, const void* v, const void* o, const void* d_o,

@@ -145,13 +145,23 @@ __device__ __forceinline__ bf16x8 lds_tr8(const bf16_t* tile, int rbase, int t, 
 // `row_ptr(r)` returns the global address of tile row r; it must always be a
 // valid address (callers clamp rows past the end of the data).
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void dma_lds_16(const void* src, MW_LDS void* wave_dst) {
-  const unsigned base = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)wave_dst);
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(base) : "m0", "memory");
+// LDS byte address of a pointer into LDS: the low 32 bits of its generic
+// address (the aperture base is the high half), without the null check of an
+// address-space cast.
+__device__ __forceinline__ unsigned lds_addr(const void* p) { return (unsigned)(uintptr_t)p; }
+
+// This wave's byte offset in a staging round (64 lanes x 16 bytes per wave),
+// as a wave-uniform (scalar) value.
+__device__ __forceinline__ unsigned wave_stage_off(int tid) {
+  return __builtin_amdgcn_readfirstlane((unsigned)(tid & ~63) * 16u);
 }
-__device__ __forceinline__ void dma_lds_4(const void* src, MW_LDS void* wave_dst) {
-  const unsigned base = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)wave_dst);
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(base) : "m0", "memory");
+
+// `lds_dst` is the wave-uniform LDS byte address of the wave's 64 x 16 bytes.
+__device__ __forceinline__ void dma_lds_16(const void* src, unsigned lds_dst) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_dst) : "m0", "memory");
+}
+__device__ __forceinline__ void dma_lds_4(const void* src, unsigned lds_dst) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(lds_dst) : "m0", "memory");
 }
 
 // Pieces of a ROWS x D tile staged by NT threads: whole rounds of NT, the last
@@ -185,17 +195,15 @@ __device__ __forceinline__ void stage_rows_direct(bf16_t* lds_tile, RowPtr row_p
     const int row = ci / SLOTS, ps = ci % SLOTS;
     const int ls = ps ^ Tile<D>::swz(row);
     const bf16_t* src = row_ptr(row) + ls * 8;
-    bf16_t* dst = lds_tile + (it * NT + (tid & ~63)) * 8;  // wave-uniform base
-    dma_lds_16(src, (MW_LDS void*)dst);
+    dma_lds_16(src, lds_addr(lds_tile) + it * NT * 16 + wave_stage_off(tid));
   }
 }
 
 // The same load with a wave-uniform 64-bit base held in SGPRs and a per-lane
 // 32-bit byte offset (the saddr form): a tile whose rows are equally spaced is
 // staged from one scalar base per tile and offsets computed once per kernel.
-__device__ __forceinline__ void dma_lds_16_s(const void* sbase, unsigned voff, MW_LDS void* wave_dst) {
-  const unsigned base = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)wave_dst);
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(base)
+__device__ __forceinline__ void dma_lds_16_s(const void* sbase, unsigned voff, unsigned lds_dst) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(lds_dst)
                : "m0", "memory");
 }
 
@@ -227,8 +235,7 @@ __device__ __forceinline__ void stage_rows_s(bf16_t* lds_tile, const bf16_t* til
                                              int tid) {
 #pragma unroll
   for (int it = 0; it < RowOffsets<D, ROWS, NT>::ROUNDS; ++it) {
-    bf16_t* dst = lds_tile + (it * NT + (tid & ~63)) * 8;  // wave-uniform base
-    dma_lds_16_s(tile, ro.off[it], (MW_LDS void*)dst);
+    dma_lds_16_s(tile, ro.off[it], lds_addr(lds_tile) + it * NT * 16 + wave_stage_off(tid));
   }
 }
 
@@ -250,16 +257,16 @@ __device__ __forceinline__ void stage_kv_rows_direct(bf16_t* k_tile, bf16_t* v_t
     const int row = ci / SLOTS, ps = ci % SLOTS;
     const int ls = ps ^ Tile<D>::swz(row);
     const RowPair src = row_src(row);
-    const int dst = (it * NT + (tid & ~63)) * 8;  // wave-uniform base
-    dma_lds_16(src.k + ls * 8, (MW_LDS void*)(k_tile + dst));
-    dma_lds_16(src.v + ls * 8, (MW_LDS void*)(v_tile + dst));
+    const unsigned dst = it * NT * 16 + wave_stage_off(tid);
+    dma_lds_16(src.k + ls * 8, lds_addr(k_tile) + dst);
+    dma_lds_16(src.v + ls * 8, lds_addr(v_tile) + dst);
   }
 }
 
 // 64 consecutive fp32 values (rows r0..r0+63, clamped to n-1) into LDS by one wave.
 __device__ __forceinline__ void stage_f32x64_direct(float* lds, const float* g, int r0, int n, int lane) {
   const float* src = g + min(r0 + lane, n - 1);
-  dma_lds_4(src, (MW_LDS void*)lds);
+  dma_lds_4(src, lds_addr(lds));
 }
 
 // Wait until this wave's outstanding memory operations (global loads, including

@@ -62,7 +62,7 @@ struct BwdParams {
   const uint16_t* o;
   const uint16_t* d_o;
   const float* lse;
-  float* delta;  // workspace [BH, T]: rowsum(dO * O)
+  float* delta;  // workspace [BH, T]: -rowsum(dO * O)
   float* lse2;   // workspace [BH, T]: LSE * log2(e)
   uint16_t* dq;
   uint16_t* dk;
