@@ -56,25 +56,34 @@ __global__ __launch_bounds__(256) void bwd_rowterms_kernel(BwdParams p, long lon
   }
 }
 
+// LDS of the dK/dV work: Q and dO tiles (two stages each), then LSE and -Delta
+// of the tile's rows (two stages each).
+template <int D, int NW, int BM>
+struct DkdvLds {
+  static constexpr int TE = stage_elems<D, BM, 64 * NW>();
+  static constexpr int BYTES = 2 * 2 * TE * 2 + 2 * 2 * BM * 4;
+};
+
 // NW waves, each owning KBW blocks of 32 keys (K and V fragments and the dK,
 // dV accumulators in registers).  With KBW = 2 every Q and dO fragment read
 // from LDS feeds two MFMAs (one per key block), halving the LDS reads per
-// MFMA, which otherwise bound this kernel (one 16-byte row read or two
-// transposing reads per MFMA); the register state then needs the full
-// register file of one wave per SIMD, as D = 128 does with one key block.
+// MFMA; the register state then needs the full register file of one wave per
+// SIMD (measured slower than one key block at two waves per SIMD at D = 64,
+// where the in-order issue of a lone wave cannot overlap its MFMAs and its
+// softmax work).  Work item `logical`: key tile logical % n_ktiles of
+// (batch, head) logical / n_ktiles.
 template <int D, int NW, int BM, int KBW>
-__global__ __launch_bounds__(64 * NW, (D == 128 || KBW > 1 ? 4 : 8) / NW) void bwd_dkdv_kernel(BwdParams p,
-                                                                                            int n_ktiles) {
+__device__ __forceinline__ void dkdv_body(const BwdParams& p, const int logical, const int n_ktiles,
+                                          unsigned char* lds) {
   constexpr int BN = 32 * NW * KBW, NT = 64 * NW;
   static_assert(BM % 64 == 0, "row terms are staged 64 at a time");
   constexpr int KK = (D + 15) / 16, DB = (D + 31) / 32;  // D = 72: 80 and 96 columns
-  constexpr int TE = stage_elems<D, BM, NT>();
-  __shared__ __attribute__((aligned(16))) bf16_t Qs[2][TE];
-  __shared__ __attribute__((aligned(16))) bf16_t dOs[2][TE];
-  __shared__ __attribute__((aligned(16))) float lse_s[2][BM];
-  __shared__ __attribute__((aligned(16))) float dlt_s[2][BM];
+  constexpr int TE = DkdvLds<D, NW, BM>::TE;
+  bf16_t(*Qs)[TE] = reinterpret_cast<bf16_t(*)[TE]>(lds);
+  bf16_t(*dOs)[TE] = reinterpret_cast<bf16_t(*)[TE]>(lds + 2 * TE * 2);
+  float(*lse_s)[BM] = reinterpret_cast<float(*)[BM]>(lds + 4 * TE * 2);
+  float(*dlt_s)[BM] = reinterpret_cast<float(*)[BM]>(lds + 4 * TE * 2 + 2 * BM * 4);
 
-  const int logical = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = logical / n_ktiles;
   const int kt = logical % n_ktiles;  // early keys are seen by the most queries: heaviest first
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -260,17 +269,32 @@ __global__ __launch_bounds__(64 * NW, (D == 128 || KBW > 1 ? 4 : 8) / NW) void b
   }
 }
 
+template <int D, int NW, int BM, int KBW>
+__global__ __launch_bounds__(64 * NW, (D == 128 || KBW > 1 ? 4 : 8) / NW) void bwd_dkdv_kernel(BwdParams p,
+                                                                                            int n_ktiles) {
+  __shared__ __attribute__((aligned(16))) unsigned char lds[DkdvLds<D, NW, BM>::BYTES];
+  dkdv_body<D, NW, BM, KBW>(p, xcd_remap(blockIdx.x, gridDim.x), n_ktiles, lds);
+}
+
+// LDS of the dQ work: K and V tiles, two stages each.
+template <int D, int NW, int BN>
+struct DqLds {
+  static constexpr int TE = stage_elems<D, BN, 64 * NW>();
+  static constexpr int BYTES = 2 * 2 * TE * 2;
+};
+
 // NW waves, each owning RB blocks of 32 query rows: with RB = 2 every K and V
-// fragment read from LDS feeds two MFMAs (one per row block).
+// fragment read from LDS feeds two MFMAs (one per row block).  Work item
+// `logical`: query tile n_qtiles - 1 - logical % n_qtiles (heaviest first) of
+// (batch, head) logical / n_qtiles.
 template <int D, int NW, int RB, int BN>
-__global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, int n_qtiles) {
+__device__ __forceinline__ void dq_body(const BwdParams& p, const int logical, const int n_qtiles, unsigned char* lds) {
   constexpr int BM = 32 * RB * NW, NT = 64 * NW;
   constexpr int KK = (D + 15) / 16, DB = (D + 31) / 32;  // D = 72: 80 and 96 columns
-  constexpr int TE = stage_elems<D, BN, NT>();
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][TE];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][TE];
+  constexpr int TE = DqLds<D, NW, BN>::TE;
+  bf16_t(*Ks)[TE] = reinterpret_cast<bf16_t(*)[TE]>(lds);
+  bf16_t(*Vs)[TE] = reinterpret_cast<bf16_t(*)[TE]>(lds + 2 * TE * 2);
 
-  const int logical = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = logical / n_qtiles;
   const int qt = n_qtiles - 1 - logical % n_qtiles;  // late queries see the most keys: heaviest first
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -408,18 +432,45 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, in
   }
 }
 
+template <int D, int NW, int RB, int BN>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, int n_qtiles) {
+  __shared__ __attribute__((aligned(16))) unsigned char lds[DqLds<D, NW, BN>::BYTES];
+  dq_body<D, NW, RB, BN>(p, xcd_remap(blockIdx.x, gridDim.x), n_qtiles, lds);
+}
+
+// dK/dV and dQ work in one grid (both run two waves per SIMD with four-wave
+// workgroups): the first n_dkdv workgroups take key tiles, the rest query
+// tiles, so the query tiles fill the CUs that the key tiles' tail leaves idle
+// and no kernel boundary separates them.  Each part keeps its own XCD-aware
+// order (exact when n_dkdv is a multiple of the XCD count).
+template <int D, int NK, int BMK, int NQ, int RQ, int BNQ>
+__global__ __launch_bounds__(256, 2) void bwd_grad_kernel(BwdParams p, int n_dkdv, int n_ktiles, int n_qtiles) {
+  static_assert(NK == 4 && NQ == 4, "four-wave workgroups");
+  constexpr int B1 = DkdvLds<D, NK, BMK>::BYTES, B2 = DqLds<D, NQ, BNQ>::BYTES;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[B1 > B2 ? B1 : B2];
+  const int id = blockIdx.x;
+  if (id < n_dkdv) {
+    dkdv_body<D, NK, BMK, 1>(p, xcd_remap(id, n_dkdv), n_ktiles, lds);
+  } else {
+    dq_body<D, NQ, RQ, BNQ>(p, xcd_remap(id - n_dkdv, (int)gridDim.x - n_dkdv), n_qtiles, lds);
+  }
+}
+
 // Waves per workgroup of the dK/dV kernel (32 keys each) and of the dQ kernel
 // (32 queries each).
 template <int D>
 struct BwdCfg {
   static constexpr int NW_DKV = 4;
-  static constexpr int KBW_DKV = 1;  // 32-key blocks per wave of the dK/dV kernel (2 measured slower at D = 64)
+  static constexpr int KBW_DKV = 1;  // 32-key blocks per wave of the dK/dV kernel
   static constexpr int NW_DQ = 4;
   // 32-row query blocks per wave in the dQ kernel (two measured no faster at
   // D = 64 and spill at D = 128)
   static constexpr int RB_DQ = 1;
   static constexpr int BM_DKV = 64;  // queries per step of the dK/dV kernel
   static constexpr int BN_DQ = D == 64 ? 128 : 64;  // keys per step of the dQ kernel
+  // dK/dV and dQ work in one grid where both run two waves per SIMD (at
+  // D = 128 the dK/dV work needs one wave per SIMD)
+  static constexpr bool ONE_GRID = D != 128;
 };
 
 template <int D>
@@ -433,10 +484,15 @@ static hipError_t launch_bwd_d(const BwdParams& p, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int nkt = (p.T + 32 * NK * KBW - 1) / (32 * NK * KBW);
+  const int nqt = (p.T + 32 * RQ * NQ - 1) / (32 * RQ * NQ);
+  if constexpr (BwdCfg<D>::ONE_GRID) {
+    hipLaunchKernelGGL((bwd_grad_kernel<D, NK, BMK, NQ, RQ, BNQ>), dim3(nkt * p.BH + nqt * p.BH), dim3(256), 0,
+                       stream, p, nkt * p.BH, nkt, nqt);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL((bwd_dkdv_kernel<D, NK, BMK, KBW>), dim3(nkt * p.BH), dim3(64 * NK), 0, stream, p, nkt);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int nqt = (p.T + 32 * RQ * NQ - 1) / (32 * RQ * NQ);
   hipLaunchKernelGGL((bwd_dq_kernel<D, NQ, RQ, BNQ>), dim3(nqt * p.BH), dim3(64 * NQ), 0, stream, p, nqt);
   return hipGetLastError();
 }
