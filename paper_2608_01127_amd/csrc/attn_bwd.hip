@@ -70,11 +70,9 @@ struct DkdvLds {
 // MFMA; the register state then needs the full register file of one wave per
 // SIMD (measured slower than one key block at two waves per SIMD at D = 64,
 // where the in-order issue of a lone wave cannot overlap its MFMAs and its
-// softmax work).  Work item `logical`: key tile logical % n_ktiles of
-// (batch, head) logical / n_ktiles.
+// softmax work).  Work item: key tile kt of (batch, head) bh.
 template <int D, int NW, int BM, int KBW>
-__device__ __forceinline__ void dkdv_body(const BwdParams& p, const int logical, const int n_ktiles,
-                                          unsigned char* lds) {
+__device__ __forceinline__ void dkdv_body(const BwdParams& p, const int bh, const int kt, unsigned char* lds) {
   constexpr int BN = 32 * NW * KBW, NT = 64 * NW;
   static_assert(BM % 64 == 0, "row terms are staged 64 at a time");
   constexpr int KK = (D + 15) / 16, DB = (D + 31) / 32;  // D = 72: 80 and 96 columns
@@ -84,8 +82,6 @@ __device__ __forceinline__ void dkdv_body(const BwdParams& p, const int logical,
   float(*lse_s)[BM] = reinterpret_cast<float(*)[BM]>(lds + 4 * TE * 2);
   float(*dlt_s)[BM] = reinterpret_cast<float(*)[BM]>(lds + 4 * TE * 2 + 2 * BM * 4);
 
-  const int bh = logical / n_ktiles;
-  const int kt = logical % n_ktiles;  // early keys are seen by the most queries: heaviest first
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int T = p.T, L = p.L;
   const int k0 = kt * BN;
@@ -273,7 +269,9 @@ template <int D, int NW, int BM, int KBW>
 __global__ __launch_bounds__(64 * NW, (D == 128 || KBW > 1 ? 4 : 8) / NW) void bwd_dkdv_kernel(BwdParams p,
                                                                                             int n_ktiles) {
   __shared__ __attribute__((aligned(16))) unsigned char lds[DkdvLds<D, NW, BM>::BYTES];
-  dkdv_body<D, NW, BM, KBW>(p, xcd_remap(blockIdx.x, gridDim.x), n_ktiles, lds);
+  int bh, kt, split;  // early keys are seen by the most queries: heaviest first
+  tile_item(blockIdx.x, gridDim.x, p.BH, n_ktiles, 1, bh, kt, split);
+  dkdv_body<D, NW, BM, KBW>(p, bh, kt, lds);
 }
 
 // LDS of the dQ work: K and V tiles, two stages each.
@@ -284,19 +282,16 @@ struct DqLds {
 };
 
 // NW waves, each owning RB blocks of 32 query rows: with RB = 2 every K and V
-// fragment read from LDS feeds two MFMAs (one per row block).  Work item
-// `logical`: query tile n_qtiles - 1 - logical % n_qtiles (heaviest first) of
-// (batch, head) logical / n_qtiles.
+// fragment read from LDS feeds two MFMAs (one per row block).  Work item:
+// query tile qt of (batch, head) bh.
 template <int D, int NW, int RB, int BN>
-__device__ __forceinline__ void dq_body(const BwdParams& p, const int logical, const int n_qtiles, unsigned char* lds) {
+__device__ __forceinline__ void dq_body(const BwdParams& p, const int bh, const int qt, unsigned char* lds) {
   constexpr int BM = 32 * RB * NW, NT = 64 * NW;
   constexpr int KK = (D + 15) / 16, DB = (D + 31) / 32;  // D = 72: 80 and 96 columns
   constexpr int TE = DqLds<D, NW, BN>::TE;
   bf16_t(*Ks)[TE] = reinterpret_cast<bf16_t(*)[TE]>(lds);
   bf16_t(*Vs)[TE] = reinterpret_cast<bf16_t(*)[TE]>(lds + 2 * TE * 2);
 
-  const int bh = logical / n_qtiles;
-  const int qt = n_qtiles - 1 - logical % n_qtiles;  // late queries see the most keys: heaviest first
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int T = p.T, L = p.L;
   const int q0 = qt * BM;
@@ -435,24 +430,30 @@ __device__ __forceinline__ void dq_body(const BwdParams& p, const int logical, c
 template <int D, int NW, int RB, int BN>
 __global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, int n_qtiles) {
   __shared__ __attribute__((aligned(16))) unsigned char lds[DqLds<D, NW, BN>::BYTES];
-  dq_body<D, NW, RB, BN>(p, xcd_remap(blockIdx.x, gridDim.x), n_qtiles, lds);
+  int bh, r, split;  // late queries see the most keys: heaviest first
+  tile_item(blockIdx.x, gridDim.x, p.BH, n_qtiles, 1, bh, r, split);
+  dq_body<D, NW, RB, BN>(p, bh, n_qtiles - 1 - r, lds);
 }
 
 // dK/dV and dQ work in one grid (both run two waves per SIMD with four-wave
 // workgroups): the first n_dkdv workgroups take key tiles, the rest query
 // tiles, so the query tiles fill the CUs that the key tiles' tail leaves idle
-// and no kernel boundary separates them.  Each part keeps its own XCD-aware
-// order (exact when n_dkdv is a multiple of the XCD count).
+// and no kernel boundary separates them.  Each part keeps its own XCD-aware,
+// heaviest-first order (tile_item; exact when n_dkdv is a multiple of the XCD
+// count).
 template <int D, int NK, int BMK, int NQ, int RQ, int BNQ>
 __global__ __launch_bounds__(256, 2) void bwd_grad_kernel(BwdParams p, int n_dkdv, int n_ktiles, int n_qtiles) {
   static_assert(NK == 4 && NQ == 4, "four-wave workgroups");
   constexpr int B1 = DkdvLds<D, NK, BMK>::BYTES, B2 = DqLds<D, NQ, BNQ>::BYTES;
   __shared__ __attribute__((aligned(16))) unsigned char lds[B1 > B2 ? B1 : B2];
   const int id = blockIdx.x;
+  int bh, r, split;
   if (id < n_dkdv) {
-    dkdv_body<D, NK, BMK, 1>(p, xcd_remap(id, n_dkdv), n_ktiles, lds);
+    tile_item(id, n_dkdv, p.BH, n_ktiles, 1, bh, r, split);
+    dkdv_body<D, NK, BMK, 1>(p, bh, r, lds);
   } else {
-    dq_body<D, NQ, RQ, BNQ>(p, xcd_remap(id - n_dkdv, (int)gridDim.x - n_dkdv), n_qtiles, lds);
+    tile_item(id - n_dkdv, (int)gridDim.x - n_dkdv, p.BH, n_qtiles, 1, bh, r, split);
+    dq_body<D, NQ, RQ, BNQ>(p, bh, n_qtiles - 1 - r, lds);
   }
 }
 

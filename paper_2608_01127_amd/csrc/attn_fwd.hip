@@ -133,11 +133,9 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   bf16_t(*Ks)[TE] = lds[0];
   bf16_t(*Vs)[TE] = lds[1];
 
-  const int logical = xcd_remap(blockIdx.x, gridDim.x);
   const int NS = p.n_splits;
-  const int split = logical % NS;
-  const int bh = (logical / NS) / p.n_qtiles;
-  const int qt = p.n_qtiles - 1 - (logical / NS) % p.n_qtiles;  // heaviest (last) query tile first
+  int bh, qt, split;
+  fwd_item(blockIdx.x, gridDim.x, p.BH, p.n_qtiles, NS, bh, qt, split);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int rw = wave % NWR, kg = wave / NWR;  // row wave, key group
   const int q0 = qt * BM;
