@@ -135,7 +135,11 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
 
   const int NS = p.n_splits;
   int bh, qt, split;
-  fwd_item(blockIdx.x, gridDim.x, p.BH, p.n_qtiles, NS, bh, qt, split);
+  if constexpr (CACHED) {
+    cached_item(blockIdx.x, gridDim.x, p.n_qtiles, NS, bh, qt, split);
+  } else {
+    fwd_item(blockIdx.x, gridDim.x, p.BH, p.n_qtiles, NS, bh, qt, split);
+  }
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int rw = wave % NWR, kg = wave / NWR;  // row wave, key group
   const int q0 = qt * BM;

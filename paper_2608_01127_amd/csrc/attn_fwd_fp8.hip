@@ -203,11 +203,9 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   fp8_t(*Ks)[BN * DH] = lds[0];
   fp8_t(*Vs)[BN * DH] = lds[1];
 
-  const int logical = xcd_remap(blockIdx.x, gridDim.x);
   const int NS = p.n_splits;
-  const int split = logical % NS;
-  const int bh = (logical / NS) / p.n_qtiles;
-  const int qt = p.n_qtiles - 1 - (logical / NS) % p.n_qtiles;  // heaviest (last) query tile first
+  int bh, qt, split;  // split-major within a head, heaviest (last) query tile first
+  cached_item(blockIdx.x, gridDim.x, p.n_qtiles, NS, bh, qt, split);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q0 = qt * BM;
   const int b_ = bh / p.H, h_ = bh - b_ * p.H;

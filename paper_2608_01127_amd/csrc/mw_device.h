@@ -329,6 +329,20 @@ __device__ __forceinline__ void fwd_item(int bid, int n, int BH, int nqt, int NS
   tile_item(bid, n, BH, nqt, NS, bh, rank, split);
   qt = nqt - 1 - rank;
 }
+// Cached attention: the heads one after another on each XCD (xcd_remap) and,
+// within a head, split-major: every query tile's first key range (query tiles
+// heaviest first), then every query tile's second range, and so on, so that
+// the workgroups an XCD runs at once read the same key range and a window
+// larger than the L2 is streamed once per range.  Measured 1-4% faster than
+// keeping a query tile's splits adjacent or interleaving the heads.
+__device__ __forceinline__ void cached_item(int bid, int n, int nqt, int NS, int& bh, int& qt, int& split) {
+  const int logical = xcd_remap(bid, n);
+  const int per_head = nqt * NS;
+  bh = logical / per_head;
+  const int r = logical - bh * per_head;
+  split = r / nqt;
+  qt = nqt - 1 - r % nqt;
+}
 
 // Row (within a 32-row accumulator block) of accumulator register i in lane l.
 __device__ __forceinline__ int acc_row(int i, int lane) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
