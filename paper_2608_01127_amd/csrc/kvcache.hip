@@ -38,41 +38,55 @@ __global__ __launch_bounds__(256) void kv_gather_kernel(const uint16_t* __restri
 
 // RoPE re-shift of cached keys (paper Sec. 3.5): every key row of the live
 // chunks gets its rope band rotated by the angles whose cos/sin the host put in
-// `tab`.  One thread per (row, pair): a 4-byte load of the pair, an fp32
-// rotation, a 4-byte store rounded to bf16.  HBM-bound.
+// `tab`.  Grid: (pieces of one slot / 256, live chunks), so the ring slot of a
+// block is one scalar; one thread per 16-byte piece (4 pairs) of a row's band,
+// read and written whole when the band starts on a 16-byte boundary, pair by
+// pair otherwise and for a last piece of fewer than 4 pairs.  The cos/sin
+// table is staged in LDS.  fp32 rotation, bf16 (RNE) stores.  HBM-bound.
 __global__ __launch_bounds__(256) void rope_shift_kernel(uint16_t* __restrict__ k_slots, long long slot_stride, int S,
-                                                         int first_slot, long long rows_per_slot, int D, int dim_offset,
-                                                         int n_pairs, long long total, RopeTable tab) {
-  const long long stride = (long long)gridDim.x * blockDim.x;
-  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
-    const int pair = (int)(i % n_pairs);
-    const long long row = i / n_pairs;
-    const long long ch = row / rows_per_slot, r = row % rows_per_slot;
-    const int slot = (int)((first_slot + ch) % S);
-    unsigned* w = reinterpret_cast<unsigned*>(k_slots + slot * slot_stride + r * D + dim_offset + 2 * pair);
-    const unsigned u = *w;
+                                                         int first_slot, int rows_per_slot, int D, int dim_offset,
+                                                         int n_pairs, RopeTable tab) {
+  __shared__ float cs[2][64];
+  if (threadIdx.x < 64) {
+    cs[0][threadIdx.x] = tab.c[threadIdx.x];
+    cs[1][threadIdx.x] = tab.s[threadIdx.x];
+  }
+  __syncthreads();
+  const int ppr = (n_pairs + 3) >> 2;  // 16-byte pieces per row
+  const int j = (int)blockIdx.x * 256 + (int)threadIdx.x;
+  if (j >= rows_per_slot * ppr) return;
+  const int slot = (first_slot + (int)blockIdx.y) % S;  // live chunk blockIdx.y, oldest first
+  const int r = j / ppr, p0 = (j - r * ppr) * 4;
+  uint16_t* w = k_slots + slot * slot_stride + (long long)r * D + dim_offset + 2 * p0;
+  auto rot = [&](const unsigned u, const int pr) {
     const float x0 = __uint_as_float(u << 16), x1 = __uint_as_float(u & 0xffff0000u);
-    const float c = tab.c[pair], s = tab.s[pair];
-    const float y0 = fmaf(x0, c, -x1 * s);
-    const float y1 = fmaf(x0, s, x1 * c);
+    const float c = cs[0][pr], sn = cs[1][pr];
+    const float y0 = fmaf(x0, c, -x1 * sn);
+    const float y1 = fmaf(x0, sn, x1 * c);
     const unsigned b0 = __builtin_bit_cast(unsigned short, to_bf16(y0));
     const unsigned b1 = __builtin_bit_cast(unsigned short, to_bf16(y1));
-    *w = b0 | (b1 << 16);
+    return b0 | (b1 << 16);
+  };
+  if ((dim_offset & 7) == 0 && p0 + 4 <= n_pairs) {
+    u32x4 v = *reinterpret_cast<const u32x4*>(w);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = rot(v[q], p0 + q);
+    *reinterpret_cast<u32x4*>(w) = v;
+  } else {
+    unsigned* wp = reinterpret_cast<unsigned*>(w);
+    for (int q = 0; q < 4 && p0 + q < n_pairs; ++q) wp[q] = rot(wp[q], p0 + q);
   }
 }
-
 hipError_t launch_rope_shift(uint16_t* k_slots, long long slot_stride, int S, int first_slot, int n_live,
                              long long rows_per_slot, int D, int dim_offset, int n_pairs, const RopeTable& tab,
                              hipStream_t stream) {
-  const long long total = (long long)n_live * rows_per_slot * n_pairs;
-  long long blocks = (total + 255) / 256;
-  if (blocks > 256 * 32) blocks = 256 * 32;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(rope_shift_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, k_slots, slot_stride, S,
-                     first_slot, rows_per_slot, D, dim_offset, n_pairs, total, tab);
+  const long long pieces = rows_per_slot * ((n_pairs + 3) / 4);
+  if (n_live < 1 || pieces < 1) return hipSuccess;
+  if (pieces > 0x7fffffffLL - 256 || n_live > 65535) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rope_shift_kernel, dim3((unsigned)((pieces + 255) / 256), (unsigned)n_live), dim3(256), 0, stream,
+                     k_slots, slot_stride, S, first_slot, (int)rows_per_slot, D, dim_offset, n_pairs, tab);
   return hipGetLastError();
 }
-
 hipError_t launch_kv_copy(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_dst, uint16_t* v_dst,
                           long long n_elems, hipStream_t stream) {
   const long long n16 = n_elems / 8;  // n_elems is a multiple of 8 (D is 64 or 128)
