@@ -31,6 +31,8 @@ def queued(B, H, nq, qlen, D, seed):
     (1, 2, 64, 100, 3, 2, 0, 2, 70),     # empty window, queued chunks of another length
     (1, 1, 128, 64, 8, 9, 7, 4, 33),     # short queued chunks
     (1, 2, 72, 150, 4, 6, 3, 3, 150),    # D=72 (the 0.5B model's head width)
+    (2, 4, 64, 96, 4, 6, 3, 2, 96),      # B*H = 8: the split-major work order with XCD-aware heads
+    (1, 8, 128, 160, 5, 5, -1, 3, 160),
 ])
 def test_cached_attention_vs_oracle(mw, split, mode, B, H, D, L, S, n_commit, window, nq, qlen):
     print(f"[case] cached split={split} mode={mode} B={B} H={H} D={D} L={L} S={S} commits={n_commit} w={window} "

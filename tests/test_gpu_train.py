@@ -39,6 +39,12 @@ SMALL = [
     (1, 2, 700, 72, 96),     # D=72 (the 0.5B model's head width): padded MFMA steps, ragged tail
     (2, 1, 300, 72, 300),    # D=72, one chunk
     (1, 1, 45, 72, 7),       # D=72, smaller than one tile
+    # B*H a multiple of 8: the XCD work order that runs an XCD's heads' tiles
+    # heaviest first across those heads, and (D = 64, 72) the one backward grid
+    # whose dK/dV part is a multiple of 8 workgroups
+    (2, 4, 700, 64, 96),     # chunk edges inside tiles, ragged last chunk
+    (1, 8, 520, 72, 130),
+    (2, 4, 300, 128, 100),
 ]
 
 
