@@ -81,6 +81,7 @@ __device__ __forceinline__ void dkdv_body(const BwdParams& p, const int bh, cons
   bf16_t(*dOs)[TE] = reinterpret_cast<bf16_t(*)[TE]>(lds + 2 * TE * 2);
   float(*lse_s)[BM] = reinterpret_cast<float(*)[BM]>(lds + 4 * TE * 2);
   float(*dlt_s)[BM] = reinterpret_cast<float(*)[BM]>(lds + 4 * TE * 2 + 2 * BM * 4);
+  const FragOffsets<D> fo(threadIdx.x & 63, 0);  // Q and dO tiles share the layout
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int T = p.T, L = p.L;
@@ -170,8 +171,8 @@ __device__ __forceinline__ void dkdv_body(const BwdParams& p, const int bh, cons
       }
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        const bf16x8 qa = lds_row8<D>(Qt, qb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5));
-        const bf16x8 da = lds_row8<D>(dOt, qb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5));
+        const bf16x8 qa = fo.row8(Qt, qb * 32, kk);
+        const bf16x8 da = fo.row8(dOt, qb * 32, kk);
 #pragma unroll
         for (int kb = 0; kb < KBW; ++kb) {
           s[kb] = mfma32(qa, kf[kb][kk], s[kb]);
@@ -208,10 +209,10 @@ __device__ __forceinline__ void dkdv_body(const BwdParams& p, const int bh, cons
         }
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const bf16x8 dot = lds_tr8<D>(dOt, qb * 32, t, db * 32, lane);
+          const bf16x8 dot = fo.tr8(dOt, qb * 32, t, db);
 #pragma unroll
           for (int kb = 0; kb < KBW; ++kb) dv[kb][db] = mfma32(dot, pb[kb], dv[kb][db]);
-          const bf16x8 qt = lds_tr8<D>(Qt, qb * 32, t, db * 32, lane);
+          const bf16x8 qt = fo.tr8(Qt, qb * 32, t, db);
 #pragma unroll
           for (int kb = 0; kb < KBW; ++kb) dk[kb][db] = mfma32(qt, dsb[kb], dk[kb][db]);
         }
@@ -291,6 +292,7 @@ __device__ __forceinline__ void dq_body(const BwdParams& p, const int bh, const 
   constexpr int TE = DqLds<D, NW, BN>::TE;
   bf16_t(*Ks)[TE] = reinterpret_cast<bf16_t(*)[TE]>(lds);
   bf16_t(*Vs)[TE] = reinterpret_cast<bf16_t(*)[TE]>(lds + 2 * TE * 2);
+  const FragOffsets<D> fo(threadIdx.x & 63, 0);  // K and V tiles share the layout
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int T = p.T, L = p.L;
@@ -354,8 +356,8 @@ __device__ __forceinline__ void dq_body(const BwdParams& p, const int bh, const 
       }
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        const bf16x8 kfrag = lds_row8<D>(Kt, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5));
-        const bf16x8 vfrag = lds_row8<D>(Vt, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5));
+        const bf16x8 kfrag = fo.row8(Kt, kb * 32, kk);
+        const bf16x8 vfrag = fo.row8(Vt, kb * 32, kk);
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
           s[rb] = mfma32(kfrag, qf[rb][kk], s[rb]);
@@ -381,7 +383,7 @@ __device__ __forceinline__ void dq_body(const BwdParams& p, const int bh, const 
         for (int rb = 0; rb < RB; ++rb) dsb[rb] = pack8(dp[rb], t);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const bf16x8 ktr = lds_tr8<D>(Kt, kb * 32, t, db * 32, lane);
+          const bf16x8 ktr = fo.tr8(Kt, kb * 32, t, db);
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb) dq[rb][db] = mfma32(ktr, dsb[rb], dq[rb][db]);
         }

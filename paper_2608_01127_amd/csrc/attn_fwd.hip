@@ -200,6 +200,15 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   // fast loop free of the mask and of register copies between the two bodies.
   const int kfull = max(0, (e1f / BK) * BK);
 
+  // Per-lane element offsets, within a staged tile, of this wave's fragment
+  // reads: the K rows of S^T = K Q^T (one per 16-column contraction step) and
+  // the two transposing reads of each 32-column block of V.  The tile swizzle
+  // repeats every 16 rows, so a 32-key block or a 16-key contraction step only
+  // adds a constant: a fragment address is the stage buffer plus one of these
+  // registers (one add, shared by the key blocks) plus an immediate.  A key
+  // group's slice of the staged keys is folded in here.
+  const FragOffsets<D> fo(lane, kg * BN * D);
+
   auto step = [&](auto masked, const int k0, const bf16_t* Kt, const bf16_t* Vt) {
     // S^T for KB 32-key blocks x RB row blocks; each K fragment is read once
     f32x16 s[RB][KB];
@@ -211,7 +220,7 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
     for (int kk = 0; kk < KK; ++kk) {
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
-        const bf16x8 kfrag = lds_row8<D>(Kt, kb * 32 + (lane & 31), 16 * kk + 8 * (lane >> 5));
+        const bf16x8 kfrag = fo.row8(Kt, kb * 32, kk);
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) s[rb][kb] = mfma32(kfrag, qf[rb][kk], s[rb][kb]);
       }
@@ -290,7 +299,7 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
         for (int rb = 0; rb < RB; ++rb) pb[rb] = pack8(s[rb][kb], t);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const bf16x8 vfrag = lds_tr8<D>(Vt, kb * 32, t, db * 32, lane);
+          const bf16x8 vfrag = fo.tr8(Vt, kb * 32, t, db);
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb) o[rb][db] = mfma32(vfrag, pb[rb], o[rb][db]);
         }
@@ -299,9 +308,7 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   };
 
   // this wave's slice of a staged step: keys [kg * BN, (kg + 1) * BN)
-  auto slice = [&](auto masked, const int k0, const int st) {
-    step(masked, k0 + kg * BN, Ks[st] + kg * BN * D, Vs[st] + kg * BN * D);
-  };
+  auto slice = [&](auto masked, const int k0, const int st) { step(masked, k0 + kg * BN, Ks[st], Vs[st]); };
   const KVOffsets<D, CACHED, BK, NT> kvo(p, tid);
   int kc = advance(kbeg - BK);  // next tile to use
   {

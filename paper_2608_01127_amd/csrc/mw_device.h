@@ -126,6 +126,57 @@ __device__ __forceinline__ bf16x8 lds_tr8(const bf16_t* tile, int rbase, int t, 
   return r;
 }
 
+// Per-lane element offsets of a wave's fragment reads from an LDS tile, for
+// kernels that compute them once: the row read of lds_row8 (row l % 32,
+// columns 16 kk + 8 (l / 32)) per 16-column step kk, and the two transposing
+// reads of lds_tr8 (rows rr and rr + 8, column block db).  The slot swizzle
+// repeats every 16 rows, so a read of rows further down the tile (a later
+// 32-row block, the second 16-row contraction step) is the same register plus
+// a constant offset that the compiler folds into the instruction.
+template <int D>
+struct FragOffsets {
+  static constexpr int KK = (D + 15) / 16, DB = (D + 31) / 32;
+  int row[KK], tr[DB][2];
+  __device__ __forceinline__ FragOffsets(int lane, int extra) {
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) row[kk] = Tile<D>::off(lane & 31, 16 * kk + 8 * (lane >> 5)) + extra;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int rr = 4 * (lane >> 5) + ((lane & 15) >> 2);
+      const int cc = db * 32 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+      tr[db][0] = Tile<D>::off(rr, cc) + extra;
+      tr[db][1] = Tile<D>::off(rr + 8, cc) + extra;
+    }
+  }
+  // lds_row8(tile, rbase + l % 32, 16 kk + 8 (l / 32)), rbase a multiple of 16
+  __device__ __forceinline__ bf16x8 row8(const bf16_t* tile, int rbase, int kk) const {
+    return *reinterpret_cast<const bf16x8*>(tile + row[kk] + rbase * D);
+  }
+  // lds_tr8(tile, rbase, t, 32 db, l), rbase a multiple of 16
+  __device__ __forceinline__ bf16x8 tr8(const bf16_t* tile, int rbase, int t, int db) const;
+};
+
+// The same A operand from the two addresses lds_tr8 computes (rows rr and
+// rr + 8 of the tile at column cc), for callers that precompute them.
+__device__ __forceinline__ bf16x8 lds_tr8_at(const bf16_t* p0, const bf16_t* p1) {
+  i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((MW_LDS i16x4*)(p0));
+  i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((MW_LDS i16x4*)(p1));
+  bf16x8 r;
+  bf16x4 lo4 = __builtin_bit_cast(bf16x4, lo);
+  bf16x4 hi4 = __builtin_bit_cast(bf16x4, hi);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    r[j] = lo4[j];
+    r[4 + j] = hi4[j];
+  }
+  return r;
+}
+
+template <int D>
+__device__ __forceinline__ bf16x8 FragOffsets<D>::tr8(const bf16_t* tile, int rbase, int t, int db) const {
+  return lds_tr8_at(tile + tr[db][0] + (rbase + 16 * t) * D, tile + tr[db][1] + (rbase + 16 * t) * D);
+}
+
 // ---------------------------------------------------------------------------
 // Direct global -> LDS staging (global_load_lds_dwordx4): each lane's 16 bytes
 // land at wave_base + 16 * lane (wave_base in M0), so the tile swizzle is
