@@ -446,8 +446,8 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
 // Tile configuration per head dimension: waves per workgroup (32 query rows
 // each), keys per step, row blocks per wave and LDS stages.  With D = 128 a
 // workgroup of 8 waves shares each staged K/V tile among 256 queries, halving
-// L2 -> LDS traffic per MFMA; with D = 64 four waves of two row blocks and a
-// third workgroup per CU measured faster.
+// L2 -> LDS traffic per MFMA; with D = 64 four waves of two row blocks (two
+// workgroups per CU) measured faster.
 template <int D>
 struct FwdCfg {
   static constexpr int NW = D == 64 ? 4 : 8;
@@ -554,15 +554,32 @@ static hipError_t launch_fwd_cfg(const FwdParams& p, hipStream_t stream) {
 // kernel and the split heuristic live in the D = 128 unit.  The key-group
 // configurations for few queued rows are compiled in a unit of their own
 // (MW_FWD_DECODE) with the default scheduler.
+template <int D, bool CACHED, int NW, int BN, int RB, int KG>
+static int resident_tpl(int fallback) {
+  static const int n = resident_workgroups(attn_fwd_kernel<D, CACHED, NW, BN, RB, KG>, 64 * NW, fallback);
+  return n;
+}
+
+template <int D, bool CACHED>
+static int resident_cfg(int fallback) {
+  using C = FwdCfg<D>;
+  return resident_tpl<D, CACHED, C::NW, C::BN, C::RB, C::KG>(fallback);
+}
+
+// (fallbacks: D = 64 runs 4 waves of about 235 registers, two workgroups per
+// CU; D = 72 and 128 run 8 waves of 160-240 registers, one per CU)
 #if MW_FWD_HEAD_DIM == 64 && !defined(MW_FWD_DECODE)
 hipError_t launch_fwd_64(const FwdParams& p, bool cached, hipStream_t stream) {
   return cached ? launch_fwd_cfg<64, true>(p, stream) : launch_fwd_cfg<64, false>(p, stream);
 }
+int fwd_resident_wgs_64(bool cached) { return cached ? resident_cfg<64, true>(2) : resident_cfg<64, false>(2); }
 #elif MW_FWD_HEAD_DIM == 72 && !defined(MW_FWD_DECODE)
 hipError_t launch_fwd_72(const FwdParams& p, bool cached, hipStream_t stream) {
   return cached ? launch_fwd_cfg<72, true>(p, stream) : launch_fwd_cfg<72, false>(p, stream);
 }
+int fwd_resident_wgs_72(bool cached) { return cached ? resident_cfg<72, true>(1) : resident_cfg<72, false>(1); }
 #elif MW_FWD_HEAD_DIM == 128 && !defined(MW_FWD_DECODE)
+int fwd_resident_wgs_128(bool cached) { return cached ? resident_cfg<128, true>(1) : resident_cfg<128, false>(1); }
 hipError_t launch_fwd_128(const FwdParams& p, bool cached, hipStream_t stream) {
   if (!cached) return launch_fwd_cfg<128, false>(p, stream);
   const int bm = fwd_choice(128, true, p.Tq).bm;
@@ -578,6 +595,13 @@ hipError_t launch_fwd_decode_128(const FwdParams& p, int bm, hipStream_t stream)
   using C = FwdDecodeCfg<128, 4>;
   return launch_fwd_tpl<128, true, C::NW, C::BN, C::RB, C::KG>(p, stream);
 }
+// (fallback: 8 waves of 190-235 registers and 128 KB of LDS, one per CU)
+int fwd_resident_wgs_decode_128(int bm) {
+  using C2 = FwdDecodeCfg<128, 2>;
+  using C4 = FwdDecodeCfg<128, 4>;
+  return bm == 64 ? resident_tpl<128, true, C2::NW, C2::BN, C2::RB, C2::KG>(1)
+                  : resident_tpl<128, true, C4::NW, C4::BN, C4::RB, C4::KG>(1);
+}
 #else
 #error "compile with -DMW_FWD_HEAD_DIM=64, 72 or 128 (128 optionally with -DMW_FWD_DECODE)"
 #endif
@@ -585,11 +609,11 @@ hipError_t launch_fwd_decode_128(const FwdParams& p, int bm, hipStream_t stream)
 #if MW_FWD_HEAD_DIM == 128 && !defined(MW_FWD_DECODE)
 // Must agree with the dispatch in launch_fwd_128.
 FwdChoice fwd_choice(int D, bool cached, int Tq) {
-  if (cached && D == 128 && Tq <= 64) return {64, 1};
-  if (cached && D == 128 && Tq <= 512) return {128, 1};  // several 128-row tiles up to 512 rows
-  if (D == 64) return {32 * FwdCfg<64>::RB * FwdCfg<64>::NW, 3};
-  if (D == 72) return {32 * FwdCfg<72>::RB * FwdCfg<72>::NW, 2};
-  return {32 * FwdCfg<128>::RB * FwdCfg<128>::NW, 2};
+  if (cached && D == 128 && Tq <= 64) return {64, fwd_resident_wgs_decode_128(64)};
+  if (cached && D == 128 && Tq <= 512) return {128, fwd_resident_wgs_decode_128(128)};  // 128-row tiles up to 512 rows
+  if (D == 64) return {32 * FwdCfg<64>::RB * FwdCfg<64>::NW, fwd_resident_wgs_64(cached)};
+  if (D == 72) return {32 * FwdCfg<72>::RB * FwdCfg<72>::NW, fwd_resident_wgs_72(cached)};
+  return {32 * FwdCfg<128>::RB * FwdCfg<128>::NW, fwd_resident_wgs_128(cached)};
 }
 
 hipError_t launch_combine(const FwdParams& p, int D, hipStream_t stream) {
@@ -606,30 +630,40 @@ size_t fwd_split_bytes(int D, int BH, int Tq, int n_splits) {
   return (size_t)n_splits * BH * Tq * (D + 2) * sizeof(float);
 }
 
-// Split count from a small cost model: the unsplit work runs in
-// max(MFMA time, K/V streaming time); a grid of `base * ns` workgroups fills
-// its last round of the GPU's workgroup slots only partly (efficiency =
-// grid / (rounds * slots)); each split adds fp32 partials written and read
-// back.  The count with the lowest estimate wins (each split keeps at least
-// two key tiles; at most 64 splits; bounded by the workspace).
+// Split count from a small cost model.  A call is bound by its MFMA time or
+// by streaming its K/V window, whichever is larger at full occupancy.  A grid
+// of `base * ns` workgroups runs an MFMA-bound call at the efficiency with
+// which it fills the GPU's resident workgroup slots (grid / (rounds * slots)),
+// and a streaming-bound one at the fraction of the 256 CUs it covers (one
+// workgroup per CU keeps a CU's loads in flight).  Each split adds fp32
+// partials written and read back.  The count with the lowest estimate wins
+// (each split keeps at least two key tiles; at most 64 splits; bounded by the
+// workspace).  Measured on one queued chunk of 64-512 tokens over a 6 x 2640
+// window it picks the fastest of 4-32 splits, and on 1024-10560 queued rows
+// the fastest or one within 1%.
 int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes) {
-  return fwd_choose_splits_for(fwd_choice(D, true, Tq), 0.8e15, D, BH, Tq, Tk, ws_bytes);
+  return fwd_choose_splits_for(fwd_choice(D, true, Tq), 0.8e15, 2, D, BH, Tq, Tk, ws_bytes);
 }
 
-int fwd_choose_splits_for(const FwdChoice& ch, double flops, int D, int BH, int Tq, int Tk, size_t ws_bytes) {
+int fwd_choose_splits_for(const FwdChoice& ch, double flops, int kv_bytes, int D, int BH, int Tq, int Tk,
+                          size_t ws_bytes) {
   const int BN = 128;  // keys staged per step (at most)
-  const double slots = 256.0 * ch.wg_per_cu;  // resident workgroups (registers / LDS)
+  const double cus = 256.0;
+  const double slots = cus * ch.wg_per_cu;
   const double base = (double)((Tq + ch.bm - 1) / ch.bm) * BH;
   const double pairs = (double)BH * Tq * std::max(1.0, (double)Tk - 0.5 * Tq);
-  const double t_work = std::max(4.0 * pairs * D / flops, 2.0 * BH * (double)Tk * D * 2 / 4.0e12);
+  const double t_mfma = 4.0 * pairs * D / flops;
+  const double t_stream = 2.0 * BH * (double)Tk * D * kv_bytes / 4.0e12;
+  const bool mfma_bound = t_mfma >= t_stream;
   const int ns_max = (int)std::min<long long>(64, std::max(1, (Tk / BN) / 2));
   int best = 1;
   double best_t = 1e30;
   for (int ns = 1; ns <= ns_max; ++ns) {
     if (ns > 1 && fwd_split_bytes(D, BH, Tq, ns) > ws_bytes) break;
     const double grid = base * ns;
-    const double eff = grid / (std::ceil(grid / slots) * slots);
-    const double t = t_work / eff + (ns > 1 ? 2.0 * fwd_split_bytes(D, BH, Tq, ns) / 4.0e12 : 0.0);
+    const double t = (mfma_bound ? t_mfma / (grid / (std::ceil(grid / slots) * slots))
+                                 : t_stream / std::min(1.0, grid / cus)) +
+                     (ns > 1 ? 2.0 * fwd_split_bytes(D, BH, Tq, ns) / 4.0e12 : 0.0);
     if (t < best_t * 0.98) {  // prefer fewer splits unless clearly better
       best_t = t;
       best = ns;

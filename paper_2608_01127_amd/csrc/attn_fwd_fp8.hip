@@ -471,11 +471,16 @@ hipError_t launch_fp8_tpl(FwdParams p, hipStream_t stream) {
 
 }  // namespace
 
-// Must agree with the dispatch in launch_fwd_fp8.
+// Must agree with the dispatch in launch_fwd_fp8.  Resident workgroups per CU
+// from the runtime (fallbacks as built: two 2-wave workgroups of 64 KB LDS,
+// three 4-wave ones of about 170 registers, one 8-wave one).
 FwdChoice fwd8_choice(int Tq) {
-  if (Tq <= 64) return {64, 2};
-  if (Tq <= 128) return {128, 1};
-  return {32 * Fwd8Cfg::RB * Fwd8Cfg::NW, 1};
+  static const int r64 = resident_workgroups(attn_fwd_fp8_kernel<2, Fwd8FewRows<2>::RB, Fwd8FewRows<2>::BN>, 128, 2);
+  static const int r128 = resident_workgroups(attn_fwd_fp8_kernel<4, Fwd8FewRows<4>::RB, Fwd8FewRows<4>::BN>, 256, 3);
+  static const int r256 = resident_workgroups(attn_fwd_fp8_kernel<Fwd8Cfg::NW, Fwd8Cfg::RB, Fwd8Cfg::BN>, 512, 1);
+  if (Tq <= 64) return {64, r64};
+  if (Tq <= 128) return {128, r128};
+  return {32 * Fwd8Cfg::RB * Fwd8Cfg::NW, r256};
 }
 
 hipError_t launch_fwd_fp8(FwdParams p, hipStream_t stream) {

@@ -423,7 +423,7 @@ size_t mw_chunk_attn_cached_workspace_size(const mw_kvcache* c, int n_queued, in
   const long long tk = c->sink_len + w * c->L + tq;
   if (tq > kMaxT || tk > kMaxT) return 0;
   const int bh = c->B * c->H;
-  const int ns = c->elem_bytes == 1 ? mw::fwd_choose_splits_for(mw::fwd8_choice((int)tq), kFp8Flops, c->D, bh, (int)tq,
+  const int ns = c->elem_bytes == 1 ? mw::fwd_choose_splits_for(mw::fwd8_choice((int)tq), kFp8Flops, 1, c->D, bh, (int)tq,
                                                                 (int)tk, (size_t)-1)
                                     : mw::fwd_choose_splits(c->D, bh, (int)tq, (int)tk, (size_t)-1);
   return mw::fwd_split_bytes(c->D, bh, (int)tq, ns);
@@ -583,7 +583,7 @@ int mw_chunk_attn_cached_fp8(const void* q8, const void* k8_new, const void* v8_
   p.slot_stride = (long long)c->B * c->H * c->L * c->D;  // bytes = elements
   p.S = c->S;
   p.first_slot = (int)((c->head - w) % c->S);
-  p.n_splits = mw::fwd_choose_splits_for(mw::fwd8_choice(p.Tq), kFp8Flops, c->D, p.BH, p.Tq, p.Tk,
+  p.n_splits = mw::fwd_choose_splits_for(mw::fwd8_choice(p.Tq), kFp8Flops, 1, c->D, p.BH, p.Tq, p.Tk,
                                          workspace != nullptr ? workspace_bytes : 0);
   p.part = static_cast<float*>(workspace);
   p.so = so;

@@ -435,4 +435,18 @@ struct Vis {
   }
 };
 
+// Workgroups of `threads` threads running `kernel` that one CU holds at once,
+// from the runtime's occupancy calculator (the kernel's registers and LDS as
+// built), or `fallback` where the runtime cannot answer (no device present:
+// the figure then only sizes a workspace).
+template <typename Kernel>
+inline int resident_workgroups(Kernel kernel, int threads, int fallback) {
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) != hipSuccess || n < 1) {
+    (void)hipGetLastError();
+    return fallback;
+  }
+  return n;
+}
+
 }  // namespace mw

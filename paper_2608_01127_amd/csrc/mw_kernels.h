@@ -87,6 +87,14 @@ inline hipError_t launch_fwd(const FwdParams& p, int D, bool cached, hipStream_t
   return D == 64 ? launch_fwd_64(p, cached, stream)
                  : (D == 72 ? launch_fwd_72(p, cached, stream) : launch_fwd_128(p, cached, stream));
 }
+// Workgroups per CU that the forward kernel of each unit holds at once
+// (runtime occupancy; the value the kernels' register and LDS use gives as
+// built where no device is present): the training or cached kernel of
+// launch_fwd_64 / _72 / _128, and the few-rows kernel of `bm` rows.
+int fwd_resident_wgs_64(bool cached);
+int fwd_resident_wgs_72(bool cached);
+int fwd_resident_wgs_128(bool cached);
+int fwd_resident_wgs_decode_128(int bm);
 // Query rows per workgroup and resident workgroups per CU of the tile
 // configuration the forward launcher picks for a shape.
 struct FwdChoice {
@@ -112,8 +120,9 @@ struct QuantJobs {
 };
 hipError_t launch_quantize_fp8(const QuantJobs& jobs, int n_jobs, int B, int H, int T, int D, hipStream_t stream);
 // Split count for a cached call run by the configuration `ch` at `flops`
-// FLOP/s of sustained MFMA throughput.
-int fwd_choose_splits_for(const FwdChoice& ch, double flops, int D, int BH, int Tq, int Tk, size_t ws_bytes);
+// FLOP/s of sustained MFMA throughput, over K/V elements of `kv_bytes` bytes.
+int fwd_choose_splits_for(const FwdChoice& ch, double flops, int kv_bytes, int D, int BH, int Tq, int Tk,
+                          size_t ws_bytes);
 // Split count the cached launcher uses for this shape given `ws_bytes` of
 // workspace (1 = no split), and the workspace bytes a split count needs.
 int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes);

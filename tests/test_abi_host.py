@@ -196,6 +196,25 @@ def test_cached_workspace_size_policy():
     assert lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 0, 128, 6) == 0
 
 
+# Split counts over a 6 x 2640-token window (B1 H16 D128): the fastest of 1-8
+# splits measured on MI355X for 1024-10560 queued rows (four 2640-token chunks:
+# 3 splits within 1% of none), and of 4-32 splits for one chunk of 64-512 rows.
+@pytest.mark.parametrize("e4m3, n_queued, q_len, splits", [
+    (False, 4, 2640, 3), (False, 1, 2640, 4), (False, 1, 1024, 4), (False, 1, 64, 16), (False, 1, 128, 16),
+    (False, 1, 256, 8), (False, 1, 512, 4), (True, 1, 64, 16), (True, 1, 128, 16), (True, 1, 256, 16)])
+def test_cached_split_choice(e4m3, n_queued, q_len, splits):
+    lib = mw.load()
+    if e4m3:
+        c = _lib.mw_kvcache()
+        assert lib.mw_kvcache_init_fp8(ctypes.byref(c), A, A, 8, 1, 16, 2640, 128, 0.02, 0.02) == mw.MW_OK
+    else:
+        c = new_cache(S=8, B=1, H=16, L=2640, D=128)
+    c.head = 6
+    ws = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), n_queued, q_len, 6)
+    per_split = 16 * n_queued * q_len * 130 * 4  # fp32 O and (m, l) per query row
+    assert ws % per_split == 0 and ws // per_split == splits
+
+
 def test_sink_and_rope_validation():
     lib = mw.load()
     c = new_cache(S=4, D=128)
