@@ -470,17 +470,18 @@ def main():
     # split it is the split kernel followed by the small combine kernel; the
     # events bracket both, so the duration is the call's.
     cached_tflops = F_st / (ph["cached"] * 1e-3) / 1e12
-    n_splits = max(1, ws_c.numel() // (st.B * st.H * st.n_queued * st.q_len * (st.D + 2) * 4))
+    n_splits, n_whole = mw.mw_chunk_attn_cached_plan(cache, st.n_queued, st.q_len, st.window, 0, ws_c.numel())
     digest = source_digest(["paper_2608_01127_amd/csrc/attn_fwd.hip", "paper_2608_01127_amd/csrc/mw_device.h"])
     traffic = read_traffic("attn_fwd_cached", digest)
     kname = "attn_fwd_kernel<128, true, 8, 64, 1, 1>"
     if n_splits > 1:
-        kname += f" over {n_splits} key ranges + attn_combine_kernel<128>"
+        kname += (f" ({n_whole} whole query tiles per head, the others over {n_splits} key ranges)"
+                  " + attn_combine_kernel<128>")
     roofline = {"kernel": kname + " (cached chunk attention call)", "bound": "mfma",
                 "achieved": round(cached_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(cached_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
                 "algorithmic_flops_per_launch": F_st, "avg_launch_ms": round(ph["cached"], 4),
-                "n_splits": n_splits}
+                "n_splits": n_splits, "n_whole": n_whole}
 
     res = {
         "metric": "block-causal attn fwd+bwd TFLOP/s (% bf16 MFMA peak); cached-chunk attn GB/s",

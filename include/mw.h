@@ -242,9 +242,11 @@ int mw_kvcache_slot_of(const mw_kvcache* c, int64_t chunk);
  *                      range of each query tile is split over several
  *                      workgroups (fp32 partial results in the workspace, then a
  *                      merge), which keeps the GPU busy when there are few query
- *                      tiles (few or short queued chunks).  NULL or a smaller
- *                      buffer: as many splits as fit (possibly none).  The
- *                      result does not depend on the split count beyond fp32
+ *                      tiles (few or short queued chunks); the heaviest query
+ *                      tiles may run unsplit while the lighter ones, which run
+ *                      last, are split (mw_chunk_attn_cached_plan).  NULL or a
+ *                      smaller buffer: a plan that fits (possibly no split).
+ *                      The result does not depend on the plan beyond fp32
  *                      rounding.
  * Keys are visited in logical order whatever the ring offset, so the result
  * for a given window content does not depend on where the ring wrapped.
@@ -254,9 +256,22 @@ int mw_kvcache_slot_of(const mw_kvcache* c, int64_t chunk);
  * ---------------------------------------------------------------------- */
 enum { MW_QUEUED_CAUSAL = 0, MW_QUEUED_ISOLATED = 1 };
 
-/* Workspace bytes that let mw_chunk_attn_cached use its preferred split count
- * for this shape (0 when it would not split).  Negative window: all live. */
+/* Workspace bytes that let mw_chunk_attn_cached use its preferred split plan
+ * for this shape under either visibility rule (0 when neither would split).
+ * Negative window: all live. */
 size_t mw_chunk_attn_cached_workspace_size(const mw_kvcache* c, int n_queued, int q_len, int window);
+
+/* The key-range split plan that mw_chunk_attn_cached (mw_chunk_attn_cached_fp8
+ * for an e4m3 cache) uses for this shape, visibility rule (flags) and
+ * workspace size (0: no workspace): *n_splits key ranges for the lighter
+ * query tiles of each head, of which the *n_whole heaviest (the last) run
+ * unsplit; *n_splits = 1 means no split and then *n_whole = 0.  The plan comes
+ * from a cost model of the kernel's dispatch and does not change the result
+ * beyond fp32 rounding.  Host-only: no device work.
+ * Errors: MW_EINVAL (null pointers, n_queued/q_len < 1, window < -1 or above
+ * the live chunks, unknown flags), MW_EUNSUPPORTED (as mw_chunk_attn_cached). */
+int mw_chunk_attn_cached_plan(const mw_kvcache* c, int n_queued, int q_len, int window, int flags,
+                              size_t workspace_bytes, int* n_splits, int* n_whole);
 
 int mw_chunk_attn_cached(const void* q, const void* k_new, const void* v_new,
                          int n_queued, int q_len, const mw_kvcache* c, int window, int flags,

@@ -28,6 +28,7 @@ from ._lib import (  # noqa: F401
     mw_block_causal_attn_fwd,
     mw_chunk_attn_cached,
     mw_chunk_attn_cached_fp8,
+    mw_chunk_attn_cached_plan,
     mw_chunk_attn_cached_workspace_size,
     mw_kvcache,
     mw_kvcache_append,

@@ -68,6 +68,7 @@ class mw_sched_tick(ctypes.Structure):
 
 # Exported symbols and their signatures (mirrors include/mw.h).
 _vp, _i, _f, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+_ip = ctypes.POINTER(ctypes.c_int)
 _cache_p = ctypes.POINTER(mw_kvcache)
 _str_p = ctypes.POINTER(mw_strides)
 SIGNATURES = {
@@ -84,6 +85,7 @@ SIGNATURES = {
     "mw_kvcache_live": ([_cache_p], _i),
     "mw_kvcache_slot_of": ([_cache_p, ctypes.c_int64], _i),
     "mw_chunk_attn_cached_workspace_size": ([_cache_p, _i, _i, _i], _sz),
+    "mw_chunk_attn_cached_plan": ([_cache_p, _i, _i, _i, _i, _sz, _ip, _ip], _i),
     "mw_chunk_attn_cached": ([_vp, _vp, _vp, _i, _i, _cache_p, _i, _i, _vp, _vp, _f, _vp, _sz, _vp], _i),
     "mw_block_causal_attn_fwd_strided": ([_vp, _vp, _vp, _vp, _vp, _str_p, _i, _i, _i, _i, _i, _f, _vp], _i),
     "mw_block_causal_attn_bwd_strided": ([_vp] * 9 + [_vp, _sz, _str_p, _i, _i, _i, _i, _i, _f, _vp], _i),
@@ -346,6 +348,18 @@ def mw_kvcache_slot_of(cache: KVCache, chunk: int) -> int:
 def mw_chunk_attn_cached_workspace_size(cache: KVCache, n_queued: int, q_len: int, window: int = -1) -> int:
     return int(load().mw_chunk_attn_cached_workspace_size(ctypes.byref(cache.desc), int(n_queued), int(q_len),
                                                           int(window)))
+
+
+def mw_chunk_attn_cached_plan(cache: KVCache, n_queued: int, q_len: int, window: int = -1,
+                              flags: int = MW_QUEUED_CAUSAL, workspace_bytes: int = -1):
+    """(n_splits, n_whole) the cached call uses with `workspace_bytes` of workspace
+    (-1: the size mw_chunk_attn_cached_workspace_size gives)."""
+    if workspace_bytes < 0:
+        workspace_bytes = mw_chunk_attn_cached_workspace_size(cache, n_queued, q_len, window)
+    ns, nw = ctypes.c_int(0), ctypes.c_int(0)
+    _check(load().mw_chunk_attn_cached_plan(ctypes.byref(cache.desc), int(n_queued), int(q_len), int(window),
+                                            int(flags), int(workspace_bytes), ctypes.byref(ns), ctypes.byref(nw)))
+    return ns.value, nw.value
 
 
 def mw_chunk_attn_cached(q, k_new, v_new, n_queued: int, q_len: int, cache: KVCache, window: int = -1,

@@ -21,6 +21,11 @@
 // variant; see Vis in mw_device.h.
 #include <algorithm>
 #include <cmath>
+#include <map>
+#include <mutex>
+#include <queue>
+#include <tuple>
+#include <vector>
 #include <type_traits>
 
 #include "mw_device.h"
@@ -133,12 +138,13 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   bf16_t(*Ks)[TE] = lds[0];
   bf16_t(*Vs)[TE] = lds[1];
 
-  const int NS = p.n_splits;
-  int bh, qt, split;
+  const int NS = p.n_splits;  // key ranges of a split tile (partials layout)
+  int bh, qt, split, nst;      // nst: key ranges of this workgroup's tile
   if constexpr (CACHED) {
-    cached_item(blockIdx.x, gridDim.x, p.n_qtiles, NS, bh, qt, split);
+    cached_item(blockIdx.x, gridDim.x, p.n_qtiles, NS, p.n_whole, bh, qt, split, nst);
   } else {
     fwd_item(blockIdx.x, gridDim.x, p.BH, p.n_qtiles, NS, bh, qt, split);
+    nst = NS;
   }
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int rw = wave % NWR, kg = wave / NWR;  // row wave, key group
@@ -172,10 +178,10 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   vis.range(q0, e1f, s2f, e2f);
   vis.range(min(q0 + BM, p.Tq) - 1, e1l, s2l, e2l);
   const int kend_all = max(e1l, e2l);
-  // this workgroup's share of the key tiles [0, kend_all): split `split` of NS
+  // this workgroup's share of the key tiles [0, kend_all): split `split` of nst
   const int ntiles = (kend_all + BK - 1) / BK;
-  const int kbeg = (int)((long long)ntiles * split / NS) * BK;
-  const int kend = min(kend_all, (int)((long long)ntiles * (split + 1) / NS) * BK);
+  const int kbeg = (int)((long long)ntiles * split / nst) * BK;
+  const int kend = min(kend_all, (int)((long long)ntiles * (split + 1) / nst) * BK);
   // next visited key tile after k: tiles no row of this workgroup can see are skipped
   auto advance = [&](int k) {
     int n = k + BK;
@@ -398,11 +404,12 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   for (int rb = 0; rb < RB; ++rb) {
     lsum[rb] = sum_halves(lsum[rb]);
     if (qrow[rb] >= p.Tq) continue;
-    if (NS > 1) {
+    if (nst > 1) {
       // partial result of this key range: unnormalised O, the reference max m
       // (log2 units, possibly stale by up to the rescale threshold) and the sum
-      // l of 2^(s - m); rows past Tq are not written
-      const long long row = ((long long)split * p.BH + bh) * p.Tq + qrow[rb];
+      // l of 2^(s - m); rows past Tq are not written (a split tile's rows are
+      // below split_rows)
+      const long long row = ((long long)split * p.BH + bh) * p.split_rows + qrow[rb];
       float* po = p.part + row * D;
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
@@ -417,7 +424,7 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
         }
       }
       if (lane < 32) {
-        float* ml = p.part + (long long)NS * p.BH * p.Tq * D + 2 * row;
+        float* ml = p.part + (long long)NS * p.BH * p.split_rows * D + 2 * row;
         ml[0] = m[rb];
         ml[1] = lsum[rb];
       }
@@ -475,17 +482,19 @@ struct FwdDecodeCfg {
 
 // Merge of the per-split partials: with M = max_s m_s and w_s = 2^(m_s - M),
 //   O = sum_s w_s O_s / sum_s w_s l_s,   LSE = (M + log2 sum_s w_s l_s) ln 2.
+// The split rows are rows [0, split_rows) of each head (rows = BH * split_rows).
 // One thread per 4 output columns of a row.
 template <int D>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part, uint16_t* __restrict__ o,
-                                                           Strides so, int H, int Tq, float* __restrict__ lse,
-                                                           int NS, long long rows) {
+                                                           Strides so, int H, int Tq, int split_rows,
+                                                           float* __restrict__ lse, int NS, long long rows) {
   constexpr int TPR = D / 4;  // threads per row
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long row = gid / TPR;
   if (row >= rows) return;
-  const long long bh = row / Tq;
-  const long long orow = (bh / H) * so.b + (bh % H) * so.h + (row - bh * Tq) * so.t;
+  const long long bh = row / split_rows;
+  const long long t = row - bh * split_rows;
+  const long long orow = (bh / H) * so.b + (bh % H) * so.h + t * so.t;
   const int c = (int)(gid % TPR) * 4;
   const float* ml = part + (long long)NS * rows * D;
   // splits are read in groups of G so that G loads are in flight at once
@@ -524,22 +533,20 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
 #pragma unroll
   for (int j = 0; j < 4; ++j) out[j] = to_bf16(acc[j] * inv);
   *reinterpret_cast<bf16x4*>(o + orow + c) = out;
-  if (lse != nullptr && c == 0) lse[row] = (M + __log2f(L)) * 0.69314718055994530942f;
+  if (lse != nullptr && c == 0) lse[bh * Tq + t] = (M + __log2f(L)) * 0.69314718055994530942f;
 }
 
 template <int D, bool CACHED, int NW, int BN, int RB, int KG>
 static hipError_t launch_fwd_tpl(FwdParams p, hipStream_t stream) {
   constexpr int BM = 32 * RB * (NW / KG);
-  p.n_qtiles = (p.Tq + BM - 1) / BM;
-  if (p.n_splits < 1) p.n_splits = 1;
-  hipLaunchKernelGGL((attn_fwd_kernel<D, CACHED, NW, BN, RB, KG>), dim3(p.n_qtiles * p.BH * p.n_splits),
-                     dim3(64 * NW), 0, stream, p);
+  const long long grid = fwd_prepare(p, BM, CACHED);
+  hipLaunchKernelGGL((attn_fwd_kernel<D, CACHED, NW, BN, RB, KG>), dim3((unsigned)grid), dim3(64 * NW), 0, stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_splits == 1) return e;
-  const long long rows = (long long)p.BH * p.Tq;
+  const long long rows = (long long)p.BH * p.split_rows;
   const long long threads = rows * (D / 4);
   hipLaunchKernelGGL(attn_combine_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p.part,
-                     p.o, p.so, p.H, p.Tq, p.lse, p.n_splits, rows);
+                     p.o, p.so, p.H, p.Tq, p.split_rows, p.lse, p.n_splits, rows);
   return hipGetLastError();
 }
 
@@ -609,67 +616,184 @@ int fwd_resident_wgs_decode_128(int bm) {
 #if MW_FWD_HEAD_DIM == 128 && !defined(MW_FWD_DECODE)
 // Must agree with the dispatch in launch_fwd_128.
 FwdChoice fwd_choice(int D, bool cached, int Tq) {
-  if (cached && D == 128 && Tq <= 64) return {64, fwd_resident_wgs_decode_128(64)};
-  if (cached && D == 128 && Tq <= 512) return {128, fwd_resident_wgs_decode_128(128)};  // 128-row tiles up to 512 rows
-  if (D == 64) return {32 * FwdCfg<64>::RB * FwdCfg<64>::NW, fwd_resident_wgs_64(cached)};
-  if (D == 72) return {32 * FwdCfg<72>::RB * FwdCfg<72>::NW, fwd_resident_wgs_72(cached)};
-  return {32 * FwdCfg<128>::RB * FwdCfg<128>::NW, fwd_resident_wgs_128(cached)};
+  using C2 = FwdDecodeCfg<128, 2>;
+  using C4 = FwdDecodeCfg<128, 4>;
+  if (cached && D == 128 && Tq <= 64) return {64, C2::BN * C2::KG, fwd_resident_wgs_decode_128(64)};
+  if (cached && D == 128 && Tq <= 512)  // 128-row tiles up to 512 rows
+    return {128, C4::BN * C4::KG, fwd_resident_wgs_decode_128(128)};
+  if (D == 64) return {32 * FwdCfg<64>::RB * FwdCfg<64>::NW, FwdCfg<64>::BN, fwd_resident_wgs_64(cached)};
+  if (D == 72) return {32 * FwdCfg<72>::RB * FwdCfg<72>::NW, FwdCfg<72>::BN, fwd_resident_wgs_72(cached)};
+  return {32 * FwdCfg<128>::RB * FwdCfg<128>::NW, FwdCfg<128>::BN, fwd_resident_wgs_128(cached)};
 }
 
 hipError_t launch_combine(const FwdParams& p, int D, hipStream_t stream) {
   if (D != 128) return hipErrorInvalidValue;
-  const long long rows = (long long)p.BH * p.Tq;
+  const long long rows = (long long)p.BH * p.split_rows;
   const long long threads = rows * (128 / 4);
   hipLaunchKernelGGL(attn_combine_kernel<128>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p.part,
-                     p.o, p.so, p.H, p.Tq, p.lse, p.n_splits, rows);
+                     p.o, p.so, p.H, p.Tq, p.split_rows, p.lse, p.n_splits, rows);
   return hipGetLastError();
 }
 
-size_t fwd_split_bytes(int D, int BH, int Tq, int n_splits) {
+size_t fwd_split_bytes(int D, int BH, int split_rows, int n_splits) {
   if (n_splits <= 1) return 0;
-  return (size_t)n_splits * BH * Tq * (D + 2) * sizeof(float);
+  return (size_t)n_splits * BH * split_rows * (D + 2) * sizeof(float);
 }
 
-// Split count from a small cost model.  A call is bound by its MFMA time or
-// by streaming its K/V window, whichever is larger at full occupancy.  A grid
-// of `base * ns` workgroups runs an MFMA-bound call at the efficiency with
-// which it fills the GPU's resident workgroup slots (grid / (rounds * slots)),
-// and a streaming-bound one at the fraction of the 256 CUs it covers (one
-// workgroup per CU keeps a CU's loads in flight).  Each split adds fp32
-// partials written and read back.  The count with the lowest estimate wins
-// (each split keeps at least two key tiles; at most 64 splits; bounded by the
-// workspace).  Measured on one queued chunk of 64-512 tokens over a 6 x 2640
-// window it picks the fastest of 4-32 splits, and on 1024-10560 queued rows
-// the fastest or one within 1%.
-int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes) {
-  return fwd_choose_splits_for(fwd_choice(D, true, Tq), 0.8e15, 2, D, BH, Tq, Tk, ws_bytes);
+int fwd_split_rows(int bm, int Tq, const SplitPlan& sp) {
+  if (sp.n_splits <= 1) return 0;
+  const int nqt = (Tq + bm - 1) / bm;
+  return std::min(Tq, (nqt - std::min(std::max(sp.n_whole, 0), nqt)) * bm);
 }
 
-int fwd_choose_splits_for(const FwdChoice& ch, double flops, int kv_bytes, int D, int BH, int Tq, int Tk,
-                          size_t ws_bytes) {
-  const int BN = 128;  // keys staged per step (at most)
+// Sustained MFMA rate of the bf16 cached kernel assumed by the split planner.
+constexpr double kBf16Flops = 1.1e15;
+
+SplitPlan fwd_plan_cached(int D, int BH, int Tq, int Tk, int qlen, bool isolated, size_t ws_bytes) {
+  return fwd_plan_splits(fwd_choice(D, true, Tq), kBf16Flops, 2, D, BH, Tq, Tk, qlen, isolated, ws_bytes);
+}
+
+namespace {
+
+// Makespan, in key steps, of the cached grid's workgroups on `slots` resident
+// workgroup slots, taken in dispatch order (cached_item) each as soon as a
+// slot frees: `heads` heads of query tiles with steps[qt] key steps each, the
+// n_whole heaviest unsplit, the rest over ns key ranges.  A workgroup costs
+// its key steps plus `o_wg`, plus `o_part` when it writes a partial.
+double split_makespan(const std::vector<int>& steps, int heads, int slots, int ns, int n_whole, double o_wg,
+                      double o_part) {
+  std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
+  for (int i = 0; i < slots; ++i) free_at.push(0.0);
+  auto take = [&](double t) {
+    const double s = free_at.top();
+    free_at.pop();
+    free_at.push(s + t);
+  };
+  const int nqt = (int)steps.size();
+  for (int h = 0; h < heads; ++h) {
+    for (int r = 0; r < n_whole; ++r) take(steps[nqt - 1 - r] + o_wg);
+    for (int s = 0; s < ns; ++s) {
+      for (int r = n_whole; r < nqt; ++r) {
+        const long long c = steps[nqt - 1 - r];
+        take((double)(c * (s + 1) / ns - c * s / ns) + o_wg + o_part);
+      }
+    }
+  }
+  double mk = 0.0;
+  while (!free_at.empty()) {
+    mk = std::max(mk, free_at.top());
+    free_at.pop();
+  }
+  return mk;
+}
+
+struct PlanKey {
+  int bm, bk, wg, kv_bytes, D, BH, Tq, Tk, qlen, isolated;
+  double flops;
+  size_t ws;
+  bool operator<(const PlanKey& o) const {
+    return std::tie(bm, bk, wg, kv_bytes, D, BH, Tq, Tk, qlen, isolated, flops, ws) <
+           std::tie(o.bm, o.bk, o.wg, o.kv_bytes, o.D, o.BH, o.Tq, o.Tk, o.qlen, o.isolated, o.flops, o.ws);
+  }
+};
+
+SplitPlan plan_splits(const FwdChoice& ch, double flops, int kv_bytes, int D, int BH, int Tq, int Tk, int qlen,
+                      bool isolated, size_t ws_bytes) {
   const double cus = 256.0;
   const double slots = cus * ch.wg_per_cu;
-  const double base = (double)((Tq + ch.bm - 1) / ch.bm) * BH;
+  const int nqt = (Tq + ch.bm - 1) / ch.bm;
+  const double base = (double)nqt * BH;
   const double pairs = (double)BH * Tq * std::max(1.0, (double)Tk - 0.5 * Tq);
   const double t_mfma = 4.0 * pairs * D / flops;
   const double t_stream = 2.0 * BH * (double)Tk * D * kv_bytes / 4.0e12;
-  const bool mfma_bound = t_mfma >= t_stream;
-  const int ns_max = (int)std::min<long long>(64, std::max(1, (Tk / BN) / 2));
-  int best = 1;
-  double best_t = 1e30;
-  for (int ns = 1; ns <= ns_max; ++ns) {
-    if (ns > 1 && fwd_split_bytes(D, BH, Tq, ns) > ws_bytes) break;
-    const double grid = base * ns;
-    const double t = (mfma_bound ? t_mfma / (grid / (std::ceil(grid / slots) * slots))
-                                 : t_stream / std::min(1.0, grid / cus)) +
-                     (ns > 1 ? 2.0 * fwd_split_bytes(D, BH, Tq, ns) / 4.0e12 : 0.0);
-    if (t < best_t * 0.98) {  // prefer fewer splits unless clearly better
-      best_t = t;
-      best = ns;
+  const int ns_max = (int)std::min<long long>(64, std::max(1, (Tk / 128) / 2));
+  auto part_time = [&](int rows, int ns) { return ns > 1 ? 2.0 * fwd_split_bytes(D, BH, rows, ns) / 4.0e12 : 0.0; };
+  struct Cand {
+    double t;
+    SplitPlan sp;
+  };
+  std::vector<Cand> cands;
+  if (t_mfma < t_stream) {
+    // streaming-bound (few query rows): every tile split, priced by CU coverage
+    for (int ns = 1; ns <= ns_max; ++ns) {
+      if (ns > 1 && fwd_split_bytes(D, BH, Tq, ns) > ws_bytes) break;
+      cands.push_back({t_stream / std::min(1.0, base * ns / cus) + part_time(Tq, ns), {ns, 0}});
+    }
+  } else {
+    // MFMA-bound: simulate the dispatch of one XCD (BH / 8 whole heads when
+    // the heads divide over the 8 XCDs, else the whole GPU).  Key steps per
+    // query tile: the keys its last row sees (queued-causal), or the history
+    // plus the queued chunks its rows span (isolated).
+    const int wL = Tk - Tq;
+    std::vector<int> steps(nqt);
+    for (int qt = 0; qt < nqt; ++qt) {
+      const int r0 = qt * ch.bm, r1 = std::min(Tq, r0 + ch.bm) - 1;
+      const long long keys = isolated ? (long long)wL + (long long)(r1 / qlen + 1 - r0 / qlen) * qlen
+                                      : (long long)wL + (long long)(r1 / qlen + 1) * qlen;
+      steps[qt] = (int)((keys + ch.bk - 1) / ch.bk);
+    }
+    const double t_step = 4.0 * ch.bm * ch.bk * D / (flops / slots);  // one key step of one workgroup
+    const double o_wg = 1.0;                                           // prologue and epilogue, in steps
+    // a partial written at the CU's share of HBM bandwidth, in steps
+    const double o_part = ch.bm * (D + 2) * 4.0 / (4.0e12 / cus) / t_step;
+    const bool per_xcd = BH % 8 == 0;
+    const int heads = per_xcd ? BH / 8 : BH;
+    const int sl = (int)slots / (per_xcd ? 8 : 1);
+    // more than four rounds of workgroups gain nothing
+    const int ns_cap = std::min(ns_max, std::max(8, (int)std::ceil(4.0 * slots / base)));
+    for (int ns = 1; ns <= ns_cap; ++ns) {
+      for (int whole = ns == 1 ? nqt : 0; whole <= (ns == 1 ? nqt : nqt - 1); ++whole) {
+        const int rows = fwd_split_rows(ch.bm, Tq, SplitPlan{ns, whole});
+        if (ns > 1 && fwd_split_bytes(D, BH, rows, ns) > ws_bytes) continue;
+        const double t = split_makespan(steps, heads, sl, ns, whole, o_wg, o_part) * t_step +
+                         (ns > 1 ? part_time(rows, ns) + 5e-6 : 0.0);  // merge traffic and its launch
+        cands.push_back({t, {ns, ns > 1 ? whole : 0}});
+      }
     }
   }
-  return best;
+  // the simplest plan within 2% of the fastest: fewest splits, then most whole tiles
+  double t_min = 1e300;
+  for (const Cand& c : cands) t_min = std::min(t_min, c.t);
+  SplitPlan best{1 << 30, 0};
+  for (const Cand& c : cands) {
+    if (c.t > t_min * 1.02) continue;
+    if (c.sp.n_splits < best.n_splits || (c.sp.n_splits == best.n_splits && c.sp.n_whole > best.n_whole)) best = c.sp;
+  }
+  return best.n_splits == (1 << 30) ? SplitPlan{1, 0} : best;
+}
+
+}  // namespace
+
+// Split plan from a cost model, memoised per shape (a streaming loop repeats
+// its shape every step).  A call is bound by its MFMA time or by streaming
+// its K/V window, whichever is larger at full occupancy.  A streaming-bound
+// call splits every query tile and runs at the fraction of the 256 CUs its
+// grid covers (one workgroup per CU keeps a CU's loads in flight).  For an
+// MFMA-bound call a list-scheduling simulation of the dispatch order prices
+// every split count and whole-tile count: keeping the heaviest tiles whole and
+// splitting only the light ones that run last evens out the CUs' finish
+// without the partials of a full split.  Each split adds fp32 partials, written
+// and read back by the merge.  The plan taken is the simplest (fewest splits,
+// then most whole tiles) within 2% of the fastest; each split keeps at least
+// two key tiles; at most 64 splits; bounded by the workspace.  Measured
+// on one queued chunk of 64-2640 tokens over a 6 x 2640 window it picks the
+// fastest of 1-32 uniform splits.
+SplitPlan fwd_plan_splits(const FwdChoice& ch, double flops, int kv_bytes, int D, int BH, int Tq, int Tk, int qlen,
+                          bool isolated, size_t ws_bytes) {
+  if (BH < 1 || Tq < 1 || Tk < 1 || qlen < 1 || ch.bm < 1 || ch.bk < 1) return {1, 0};
+  static std::mutex mu;
+  static std::map<PlanKey, SplitPlan> memo;
+  const PlanKey key{ch.bm, ch.bk, ch.wg_per_cu, kv_bytes, D, BH, Tq, Tk, qlen, isolated ? 1 : 0, flops, ws_bytes};
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = memo.find(key);
+    if (it != memo.end()) return it->second;
+  }
+  const SplitPlan sp = plan_splits(ch, flops, kv_bytes, D, BH, Tq, Tk, qlen, isolated, ws_bytes);
+  std::lock_guard<std::mutex> lock(mu);
+  if (memo.size() > 4096) memo.clear();
+  memo[key] = sp;
+  return sp;
 }
 #endif  // MW_FWD_HEAD_DIM == 128
 

@@ -203,9 +203,9 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   fp8_t(*Ks)[BN * DH] = lds[0];
   fp8_t(*Vs)[BN * DH] = lds[1];
 
-  const int NS = p.n_splits;
-  int bh, qt, split;  // split-major within a head, heaviest (last) query tile first
-  cached_item(blockIdx.x, gridDim.x, p.n_qtiles, NS, bh, qt, split);
+  const int NS = p.n_splits;  // key ranges of a split tile (partials layout)
+  int bh, qt, split, nst;      // nst: key ranges of this workgroup's tile
+  cached_item(blockIdx.x, gridDim.x, p.n_qtiles, NS, p.n_whole, bh, qt, split, nst);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q0 = qt * BM;
   const int b_ = bh / p.H, h_ = bh - b_ * p.H;
@@ -236,8 +236,8 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   vis.range(min(q0 + BM, p.Tq) - 1, e1l, s2l, e2l);
   const int kend_all = max(e1l, e2l);
   const int ntiles = (kend_all + BN - 1) / BN;
-  const int kbeg = (int)((long long)ntiles * split / NS) * BN;
-  const int kend = min(kend_all, (int)((long long)ntiles * (split + 1) / NS) * BN);
+  const int kbeg = (int)((long long)ntiles * split / nst) * BN;
+  const int kend = min(kend_all, (int)((long long)ntiles * (split + 1) / nst) * BN);
   auto advance = [&](int k) {
     int n = k + BN;
     if (n >= e1l && n + BN <= s2f) n = (s2f / BN) * BN;
@@ -368,9 +368,10 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   for (int rb = 0; rb < RB; ++rb) {
     lsum[rb] = sum_halves(lsum[rb]);
     if (qrow[rb] >= p.Tq) continue;
-    if (NS > 1) {
-      // partial of this key range (O already carries the V scale)
-      const long long row = ((long long)split * p.BH + bh) * p.Tq + qrow[rb];
+    if (nst > 1) {
+      // partial of this key range (O already carries the V scale); a split
+      // tile's rows are below split_rows
+      const long long row = ((long long)split * p.BH + bh) * p.split_rows + qrow[rb];
       float* po = p.part + row * DH;
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
@@ -384,7 +385,7 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
         }
       }
       if (lane < 32) {
-        float* ml = p.part + (long long)NS * p.BH * p.Tq * DH + 2 * row;
+        float* ml = p.part + (long long)NS * p.BH * p.split_rows * DH + 2 * row;
         ml[0] = m[rb];
         ml[1] = lsum[rb];
       }
@@ -460,10 +461,8 @@ struct Fwd8FewRows {
 template <int NW, int RB, int BN>
 hipError_t launch_fp8_tpl(FwdParams p, hipStream_t stream) {
   constexpr int BM = 32 * RB * NW;
-  p.n_qtiles = (p.Tq + BM - 1) / BM;
-  if (p.n_splits < 1) p.n_splits = 1;
-  hipLaunchKernelGGL((attn_fwd_fp8_kernel<NW, RB, BN>), dim3(p.n_qtiles * p.BH * p.n_splits), dim3(64 * NW), 0,
-                     stream, p);
+  const long long grid = fwd_prepare(p, BM, true);
+  hipLaunchKernelGGL((attn_fwd_fp8_kernel<NW, RB, BN>), dim3((unsigned)grid), dim3(64 * NW), 0, stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_splits == 1) return e;
   return launch_combine(p, DH, stream);
@@ -478,9 +477,9 @@ FwdChoice fwd8_choice(int Tq) {
   static const int r64 = resident_workgroups(attn_fwd_fp8_kernel<2, Fwd8FewRows<2>::RB, Fwd8FewRows<2>::BN>, 128, 2);
   static const int r128 = resident_workgroups(attn_fwd_fp8_kernel<4, Fwd8FewRows<4>::RB, Fwd8FewRows<4>::BN>, 256, 3);
   static const int r256 = resident_workgroups(attn_fwd_fp8_kernel<Fwd8Cfg::NW, Fwd8Cfg::RB, Fwd8Cfg::BN>, 512, 1);
-  if (Tq <= 64) return {64, r64};
-  if (Tq <= 128) return {128, r128};
-  return {32 * Fwd8Cfg::RB * Fwd8Cfg::NW, r256};
+  if (Tq <= 64) return {64, Fwd8FewRows<2>::BN, r64};
+  if (Tq <= 128) return {128, Fwd8FewRows<4>::BN, r128};
+  return {32 * Fwd8Cfg::RB * Fwd8Cfg::NW, Fwd8Cfg::BN, r256};
 }
 
 hipError_t launch_fwd_fp8(FwdParams p, hipStream_t stream) {

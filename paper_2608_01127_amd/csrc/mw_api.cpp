@@ -2,6 +2,7 @@
 // bookkeeping and kernel launches.  No device memory is allocated here.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdint>
@@ -409,7 +410,7 @@ int mw_kvcache_slot_of(const mw_kvcache* c, int64_t chunk) {
 }
 
 // sustained MFMA rate assumed by the split model of the e4m3 kernel
-constexpr double kFp8Flops = 1.4e15;
+constexpr double kFp8Flops = 1.6e15;
 
 static long long window_chunks(const mw_kvcache* c, int window) {
   const long long live = c->head - c->tail;
@@ -423,10 +424,47 @@ size_t mw_chunk_attn_cached_workspace_size(const mw_kvcache* c, int n_queued, in
   const long long tk = c->sink_len + w * c->L + tq;
   if (tq > kMaxT || tk > kMaxT) return 0;
   const int bh = c->B * c->H;
-  const int ns = c->elem_bytes == 1 ? mw::fwd_choose_splits_for(mw::fwd8_choice((int)tq), kFp8Flops, 1, c->D, bh, (int)tq,
-                                                                (int)tk, (size_t)-1)
-                                    : mw::fwd_choose_splits(c->D, bh, (int)tq, (int)tk, (size_t)-1);
-  return mw::fwd_split_bytes(c->D, bh, (int)tq, ns);
+  // the larger of the two visibility rules' plans (a call given less workspace
+  // plans within it)
+  const mw::FwdChoice ch = c->elem_bytes == 1 ? mw::fwd8_choice((int)tq) : mw::fwd_choice(c->D, true, (int)tq);
+  size_t bytes = 0;
+  for (const bool isolated : {false, true}) {
+    const mw::SplitPlan sp =
+        c->elem_bytes == 1
+            ? mw::fwd_plan_splits(ch, kFp8Flops, 1, c->D, bh, (int)tq, (int)tk, q_len, isolated, (size_t)-1)
+            : mw::fwd_plan_cached(c->D, bh, (int)tq, (int)tk, q_len, isolated, (size_t)-1);
+    bytes = std::max(bytes, mw::fwd_split_bytes(c->D, bh, mw::fwd_split_rows(ch.bm, (int)tq, sp), sp.n_splits));
+  }
+  return bytes;
+}
+
+int mw_chunk_attn_cached_plan(const mw_kvcache* c, int n_queued, int q_len, int window, int flags,
+                              size_t workspace_bytes, int* n_splits, int* n_whole) {
+  const char* fn = "mw_chunk_attn_cached_plan";
+  int st = check_cache(fn, c);
+  if (st) return st;
+  if (n_splits == nullptr || n_whole == nullptr) return fail(MW_EINVAL, "%s: null output pointer", fn);
+  if (n_queued < 1 || q_len < 1) return fail(MW_EINVAL, "%s: n_queued and q_len must be >= 1", fn);
+  if (flags != MW_QUEUED_CAUSAL && flags != MW_QUEUED_ISOLATED) return fail(MW_EINVAL, "%s: unknown flags %d", fn, flags);
+  const long long live = c->head - c->tail;
+  if (window < -1) return fail(MW_EINVAL, "%s: window must be >= -1", fn);
+  const long long w = window_chunks(c, window);
+  if (w > live) return fail(MW_EINVAL, "%s: window %d exceeds the %lld live chunks", fn, window, live);
+  if (w > MW_MAX_WINDOW) return fail(MW_EUNSUPPORTED, "%s: window %lld exceeds %d", fn, w, MW_MAX_WINDOW);
+  if (n_queued > MW_MAX_QUEUED) return fail(MW_EUNSUPPORTED, "%s: n_queued %d exceeds %d", fn, n_queued, MW_MAX_QUEUED);
+  const long long tq = (long long)n_queued * q_len;
+  const long long tk = c->sink_len + w * c->L + tq;
+  if (tk > kMaxT) return fail(MW_EUNSUPPORTED, "%s: too many tokens", fn);
+  const int bh = c->B * c->H;
+  const bool isolated = flags == MW_QUEUED_ISOLATED;
+  const mw::SplitPlan sp =
+      c->elem_bytes == 1
+          ? mw::fwd_plan_splits(mw::fwd8_choice((int)tq), kFp8Flops, 1, c->D, bh, (int)tq, (int)tk, q_len, isolated,
+                                workspace_bytes)
+          : mw::fwd_plan_cached(c->D, bh, (int)tq, (int)tk, q_len, isolated, workspace_bytes);
+  *n_splits = sp.n_splits;
+  *n_whole = sp.n_whole;
+  return MW_OK;
 }
 
 int mw_chunk_attn_cached_strided(const void* q, const void* k_new, const void* v_new, int n_queued, int q_len,
@@ -487,7 +525,10 @@ int mw_chunk_attn_cached_strided(const void* q, const void* k_new, const void* v
   p.slot_stride = (long long)c->B * c->H * c->L * c->D;
   p.S = c->S;
   p.first_slot = (int)((c->head - w) % c->S);
-  p.n_splits = mw::fwd_choose_splits(c->D, p.BH, p.Tq, p.Tk, workspace != nullptr ? workspace_bytes : 0);
+  const mw::SplitPlan sp = mw::fwd_plan_cached(c->D, p.BH, p.Tq, p.Tk, q_len, flags == MW_QUEUED_ISOLATED,
+                                               workspace != nullptr ? workspace_bytes : 0);
+  p.n_splits = sp.n_splits;
+  p.n_whole = sp.n_whole;
   p.part = static_cast<float*>(workspace);
   p.sq = sv[0];
   p.sk = sv[1];
@@ -583,8 +624,10 @@ int mw_chunk_attn_cached_fp8(const void* q8, const void* k8_new, const void* v8_
   p.slot_stride = (long long)c->B * c->H * c->L * c->D;  // bytes = elements
   p.S = c->S;
   p.first_slot = (int)((c->head - w) % c->S);
-  p.n_splits = mw::fwd_choose_splits_for(mw::fwd8_choice(p.Tq), kFp8Flops, 1, c->D, p.BH, p.Tq, p.Tk,
-                                         workspace != nullptr ? workspace_bytes : 0);
+  const mw::SplitPlan sp = mw::fwd_plan_splits(mw::fwd8_choice(p.Tq), kFp8Flops, 1, c->D, p.BH, p.Tq, p.Tk, q_len,
+                                               flags == MW_QUEUED_ISOLATED, workspace != nullptr ? workspace_bytes : 0);
+  p.n_splits = sp.n_splits;
+  p.n_whole = sp.n_whole;
   p.part = static_cast<float*>(workspace);
   p.so = so;
   p.o_scale = c->v_scale;

@@ -42,10 +42,15 @@ struct FwdParams {
   long long slot_stride;  // elements per slot (B*H*L*D)
   int S;                  // ring capacity in slots
   int first_slot;         // slot of the oldest window chunk; chunk i of the window is in slot (first_slot+i)%S
-  // key-range splitting (n_splits > 1): each workgroup covers 1/n_splits of its
-  // query tile's key tiles and writes fp32 partials (see attn_fwd.hip)
+  // key-range splitting (cached attention, n_splits > 1): the n_whole heaviest
+  // (last) query tiles of each head run unsplit; each of the others is covered
+  // by n_splits workgroups, one per 1/n_splits of its key tiles, which write
+  // fp32 partials for a merge kernel (see attn_fwd.hip).  The split tiles are a
+  // head's first ones: rows [0, split_rows), set by the launcher.
   int n_splits;
-  float* part;  // [n_splits][BH][Tq][D] unnormalised O, then [n_splits][BH][Tq][2] (m, l)
+  int n_whole;
+  int split_rows;
+  float* part;  // [n_splits][BH][split_rows][D] unnormalised O, then [n_splits][BH][split_rows][2] (m, l)
   // views of q, k (training keys / queued keys), v and o; lse and the ring
   // are always contiguous
   Strides sq, sk, sv, so;
@@ -95,10 +100,11 @@ int fwd_resident_wgs_64(bool cached);
 int fwd_resident_wgs_72(bool cached);
 int fwd_resident_wgs_128(bool cached);
 int fwd_resident_wgs_decode_128(int bm);
-// Query rows per workgroup and resident workgroups per CU of the tile
-// configuration the forward launcher picks for a shape.
+// Query rows per workgroup, keys per main-loop step and resident workgroups
+// per CU of the tile configuration the forward launcher picks for a shape.
 struct FwdChoice {
   int bm;
+  int bk;
   int wg_per_cu;
 };
 FwdChoice fwd_choice(int D, bool cached, int Tq);
@@ -119,14 +125,37 @@ struct QuantJobs {
   QuantJob j[2];
 };
 hipError_t launch_quantize_fp8(const QuantJobs& jobs, int n_jobs, int B, int H, int T, int D, hipStream_t stream);
-// Split count for a cached call run by the configuration `ch` at `flops`
-// FLOP/s of sustained MFMA throughput, over K/V elements of `kv_bytes` bytes.
-int fwd_choose_splits_for(const FwdChoice& ch, double flops, int kv_bytes, int D, int BH, int Tq, int Tk,
-                          size_t ws_bytes);
-// Split count the cached launcher uses for this shape given `ws_bytes` of
-// workspace (1 = no split), and the workspace bytes a split count needs.
-int fwd_choose_splits(int D, int BH, int Tq, int Tk, size_t ws_bytes);
-size_t fwd_split_bytes(int D, int BH, int Tq, int n_splits);
+// Key-range split plan of a cached call: the n_whole heaviest query tiles of
+// each head run unsplit, the others over n_splits key ranges (n_splits = 1:
+// no split, n_whole = 0).
+struct SplitPlan {
+  int n_splits;
+  int n_whole;
+};
+// Plan for a call run by the configuration `ch` at `flops` FLOP/s of
+// sustained MFMA throughput, over K/V elements of `kv_bytes` bytes, with
+// queued chunks of `qlen` rows (`isolated`: each sees only the history and
+// itself), within `ws_bytes` of workspace.
+SplitPlan fwd_plan_splits(const FwdChoice& ch, double flops, int kv_bytes, int D, int BH, int Tq, int Tk, int qlen,
+                          bool isolated, size_t ws_bytes);
+// The plan of the bf16 cached launcher (its configuration and sustained rate).
+SplitPlan fwd_plan_cached(int D, int BH, int Tq, int Tk, int qlen, bool isolated, size_t ws_bytes);
+// Rows per head covered by the split tiles (0 without a split), and the
+// workspace bytes of their partials.
+int fwd_split_rows(int bm, int Tq, const SplitPlan& sp);
+size_t fwd_split_bytes(int D, int BH, int split_rows, int n_splits);
+// Grid of a forward launch with `bm`-row tiles, after setting the split fields
+// of p: n_qtiles, and for a split (cached attention only) the whole-tile count
+// clamped to the tiles and the rows of the split tiles.
+inline long long fwd_prepare(FwdParams& p, int bm, bool cached) {
+  p.n_qtiles = (p.Tq + bm - 1) / bm;
+  if (p.n_splits < 1 || !cached) p.n_splits = 1;
+  p.n_whole = p.n_whole < 0 ? 0 : (p.n_whole > p.n_qtiles ? p.n_qtiles : p.n_whole);
+  if (p.n_whole == p.n_qtiles) p.n_splits = 1;
+  if (p.n_splits == 1) p.n_whole = 0;
+  p.split_rows = fwd_split_rows(bm, p.Tq, SplitPlan{p.n_splits, p.n_whole});
+  return (long long)p.BH * (p.n_whole + (long long)(p.n_qtiles - p.n_whole) * p.n_splits);
+}
 hipError_t launch_bwd_64(const BwdParams& p, hipStream_t stream);
 hipError_t launch_bwd_72(const BwdParams& p, hipStream_t stream);
 hipError_t launch_bwd_128(const BwdParams& p, hipStream_t stream);

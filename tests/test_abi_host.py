@@ -190,19 +190,22 @@ def test_cached_workspace_size_policy():
     assert lib.mw_chunk_attn_cached_workspace_size(None, 1, 64, -1) == 0
     big = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 4, 2640, 6)   # 42 tiles x 16 heads
     small = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 1, 128, 6)  # one tile per head
-    # per split: fp32 O (D floats) plus (m, l) per query row
-    assert big % (16 * 4 * 2640 * 130 * 4) == 0
+    # per split and split query row: fp32 O (D floats) plus (m, l)
+    assert big % (16 * 130 * 4) == 0 and 0 < big < 8 * 16 * 4 * 2640 * 130 * 4
     assert small % (16 * 128 * 130 * 4) == 0 and small // (16 * 128 * 130 * 4) >= 8
     assert lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 0, 128, 6) == 0
 
 
-# Split counts over a 6 x 2640-token window (B1 H16 D128): the fastest of 1-8
-# splits measured on MI355X for 1024-10560 queued rows (four 2640-token chunks:
-# 3 splits within 1% of none), and of 4-32 splits for one chunk of 64-512 rows.
-@pytest.mark.parametrize("e4m3, n_queued, q_len, splits", [
-    (False, 4, 2640, 3), (False, 1, 2640, 4), (False, 1, 1024, 4), (False, 1, 64, 16), (False, 1, 128, 16),
-    (False, 1, 256, 8), (False, 1, 512, 4), (True, 1, 64, 16), (True, 1, 128, 16), (True, 1, 256, 16)])
-def test_cached_split_choice(e4m3, n_queued, q_len, splits):
+# Split plans over a 6 x 2640-token window (B1 H16 D128), queued-causal, as
+# (key ranges, whole tiles per head).  Measured on MI355X: the uniform counts
+# are the fastest of 1-8 splits (1024-2640 queued rows) and of 4-32 (one chunk
+# of 64-512 rows); four 2640-token chunks (42 query tiles per head) run their
+# 32 heaviest tiles unsplit and the first chunk's 10 tiles over 3 key ranges.
+@pytest.mark.parametrize("e4m3, n_queued, q_len, plan", [
+    (False, 4, 2640, (3, 32)), (False, 1, 2640, (4, 0)), (False, 1, 1024, (4, 0)), (False, 1, 64, (16, 0)),
+    (False, 1, 128, (16, 0)), (False, 1, 256, (8, 0)), (False, 1, 512, (4, 0)), (True, 1, 64, (16, 0)),
+    (True, 1, 128, (16, 0))])
+def test_cached_split_plan(e4m3, n_queued, q_len, plan):
     lib = mw.load()
     if e4m3:
         c = _lib.mw_kvcache()
@@ -211,8 +214,51 @@ def test_cached_split_choice(e4m3, n_queued, q_len, splits):
         c = new_cache(S=8, B=1, H=16, L=2640, D=128)
     c.head = 6
     ws = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), n_queued, q_len, 6)
-    per_split = 16 * n_queued * q_len * 130 * 4  # fp32 O and (m, l) per query row
-    assert ws % per_split == 0 and ws // per_split == splits
+    ns, nw = ctypes.c_int(-1), ctypes.c_int(-1)
+    assert lib.mw_chunk_attn_cached_plan(ctypes.byref(c), n_queued, q_len, 6, mw.MW_QUEUED_CAUSAL, ws,
+                                         ctypes.byref(ns), ctypes.byref(nw)) == mw.MW_OK
+    assert (ns.value, nw.value) == plan
+    # the plan fits the workspace the library asks for; without one nothing is split
+    bm = 64 if (q_len <= 64) else (128 if q_len <= (128 if e4m3 else 512) and n_queued * q_len <= 512 else 256)
+    nqt = -(-n_queued * q_len // bm)
+    rows = min(n_queued * q_len, (nqt - nw.value) * bm) if ns.value > 1 else 0
+    assert ns.value * 16 * rows * 130 * 4 <= ws
+    assert lib.mw_chunk_attn_cached_plan(ctypes.byref(c), n_queued, q_len, 6, mw.MW_QUEUED_CAUSAL, 0,
+                                         ctypes.byref(ns), ctypes.byref(nw)) == mw.MW_OK
+    assert (ns.value, nw.value) == (1, 0)
+
+
+def test_small_hybrid_split_plans():
+    """The small shapes the GPU parity tests use for plans with whole and split query tiles."""
+    lib = mw.load()
+    ns, nw = ctypes.c_int(), ctypes.c_int()
+    c = new_cache(S=4, B=1, H=8, L=1500, D=128)
+    c.head = 2
+    for mode, plan in ((mw.MW_QUEUED_ISOLATED, (2, 6)), (mw.MW_QUEUED_CAUSAL, (2, 0))):
+        ws = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 3, 1500, 2)
+        assert lib.mw_chunk_attn_cached_plan(ctypes.byref(c), 3, 1500, 2, mode, ws, ctypes.byref(ns),
+                                             ctypes.byref(nw)) == mw.MW_OK
+        assert (ns.value, nw.value) == plan
+    c8 = _lib.mw_kvcache()
+    assert lib.mw_kvcache_init_fp8(ctypes.byref(c8), A, A, 3, 1, 1, 300, 128, 0.02, 0.02) == mw.MW_OK
+    c8.head = 1
+    ws = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c8), 3, 300, 1)
+    assert lib.mw_chunk_attn_cached_plan(ctypes.byref(c8), 3, 300, 1, mw.MW_QUEUED_ISOLATED, ws, ctypes.byref(ns),
+                                         ctypes.byref(nw)) == mw.MW_OK
+    assert (ns.value, nw.value) == (4, 1)
+
+
+def test_cached_split_plan_validation():
+    lib = mw.load()
+    c = new_cache(S=8, B=1, H=16, L=2640, D=128)
+    c.head = 6
+    ns, nw = ctypes.c_int(), ctypes.c_int()
+    plan = lib.mw_chunk_attn_cached_plan
+    assert plan(ctypes.byref(c), 1, 64, 6, 0, 0, None, ctypes.byref(nw)) == mw.MW_EINVAL
+    assert plan(ctypes.byref(c), 0, 64, 6, 0, 0, ctypes.byref(ns), ctypes.byref(nw)) == mw.MW_EINVAL
+    assert plan(ctypes.byref(c), 1, 64, 7, 0, 0, ctypes.byref(ns), ctypes.byref(nw)) == mw.MW_EINVAL
+    assert plan(ctypes.byref(c), 1, 64, 6, 5, 0, ctypes.byref(ns), ctypes.byref(nw)) == mw.MW_EINVAL
+    assert plan(None, 1, 64, 6, 0, 0, ctypes.byref(ns), ctypes.byref(nw)) == mw.MW_EINVAL
 
 
 def test_sink_and_rope_validation():

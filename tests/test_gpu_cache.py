@@ -234,6 +234,35 @@ def test_few_rows_key_groups_vs_oracle(mw, split, mode, B, H, L, S, n_commit, wi
     assert_close("lse", to_f64(lse), rl, max_abs=2e-3, mean_abs=2e-4)
 
 
+@pytest.mark.parametrize("mode", [0, 1])
+def test_hybrid_split_plan_vs_oracle(mw, mode):
+    """Three 1500-token chunks over a 2-chunk window (B1 H8 D128).  Isolated, the split plan keeps
+    the 6 heaviest of each head's 18 query tiles whole and splits the others over 2 key ranges
+    (whole tiles write O directly, the merge covers only the split rows); queued-causal splits
+    every tile.  Both against the oracle and against the unsplit pass."""
+    B, H, D, L, S, nq = 1, 8, 128, 1500, 4, 3
+    print(f"[case] hybrid split plan mode={mode} B={B} H={H} D={D} L={L} nq={nq} w=2", flush=True)
+    cache = mw.KVCache(S, B, H, L, D)
+    chunks = make_chunks(2, B, H, L, D, seed=5100)
+    for kc, vc in chunks:
+        mw.mw_kvcache_append(cache, to_gpu(kc), to_gpu(vc))
+    ns, nw = mw.mw_chunk_attn_cached_plan(cache, nq, L, 2, mode)
+    assert (ns, nw) == ((2, 6) if mode == 1 else (2, 0))
+    inp = queued(B, H, nq, L, D, seed=5200)
+    args = (to_gpu(inp["q"]), to_gpu(inp["k_new"]), to_gpu(inp["v_new"]), nq, L, cache)
+    o, lse = mw.mw_chunk_attn_cached(*args, window=2, flags=mode, want_lse=True)
+    o1, lse1 = mw.mw_chunk_attn_cached(*args, window=2, flags=mode, want_lse=True, split=False)
+    sync()
+    ro, rl = oracle.cached_chunk_attn(f64(inp["q"]), f64(inp["k_new"]), f64(inp["v_new"]),
+                                      [f64(c[0]) for c in chunks], [f64(c[1]) for c in chunks], nq, L, mode=mode)
+    assert_close("o", to_f64(o), ro)
+    assert_close("lse", to_f64(lse), rl, max_abs=2e-3, mean_abs=2e-4)
+    # the whole tiles (rows past the split rows) run the unsplit pass's arithmetic
+    rows = (18 - nw) * 256 if ns > 1 else 0
+    assert np.array_equal(to_f64(o)[:, :, rows:], to_f64(o1)[:, :, rows:])
+    assert np.array_equal(to_f64(lse)[:, :, rows:], to_f64(lse1)[:, :, rows:])
+
+
 @pytest.fixture(scope="module")
 def stream_run(mw):
     s = synth.STREAM

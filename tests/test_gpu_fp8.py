@@ -125,6 +125,7 @@ def run_fp8_case(mw, B, H, L, S, n_commit, window, nq, qlen, mode, split, sink_l
     (1, 2, 120, 4, 4, 3, 3, 120, 40),    # with a sink
     (1, 2, 128, 6, 6, 5, 1, 64, 0),      # one short queued chunk (64-row configuration)
     (1, 2, 128, 6, 6, 5, 1, 100, 32),    # 128-row configuration, ragged
+    (1, 1, 300, 3, 1, 1, 3, 300, 0),     # isolated: one whole query tile, the others over 4 key ranges
 ])
 def test_fp8_cached_attention_vs_oracle(mw, split, mode, B, H, L, S, n_commit, window, nq, qlen, sink_len):
     print(f"[case] fp8 cached split={split} mode={mode} B={B} H={H} L={L} S={S} commits={n_commit} w={window} "
