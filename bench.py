@@ -471,7 +471,8 @@ def main():
     # events bracket both, so the duration is the call's.
     cached_tflops = F_st / (ph["cached"] * 1e-3) / 1e12
     n_splits, n_whole = mw.mw_chunk_attn_cached_plan(cache, st.n_queued, st.q_len, st.window, 0, ws_c.numel())
-    digest = source_digest(["paper_2608_01127_amd/csrc/attn_fwd.hip", "paper_2608_01127_amd/csrc/mw_device.h"])
+    digest = source_digest(["paper_2608_01127_amd/csrc/attn_fwd.hip", "paper_2608_01127_amd/csrc/mw_device.h",
+                            "paper_2608_01127_amd/csrc/mw_kernels.h", "paper_2608_01127_amd/build.py"])
     traffic = read_traffic("attn_fwd_cached", digest)
     kname = "attn_fwd_kernel<128, true, 8, 64, 1, 1>"
     if n_splits > 1:

@@ -86,7 +86,9 @@ struct BwdParams {
 hipError_t launch_fwd_64(const FwdParams& p, bool cached, hipStream_t stream);
 hipError_t launch_fwd_72(const FwdParams& p, bool cached, hipStream_t stream);
 hipError_t launch_fwd_128(const FwdParams& p, bool cached, hipStream_t stream);
-// cached attention at D = 128 with `bm` (64 or 128) query rows per workgroup
+// cached attention at D = 128: the 256-row configuration, and the ones with
+// `bm` (64 or 128) query rows per workgroup
+hipError_t launch_fwd_cached_128(const FwdParams& p, hipStream_t stream);
 hipError_t launch_fwd_decode_128(const FwdParams& p, int bm, hipStream_t stream);
 inline hipError_t launch_fwd(const FwdParams& p, int D, bool cached, hipStream_t stream) {
   return D == 64 ? launch_fwd_64(p, cached, stream)
@@ -99,6 +101,7 @@ inline hipError_t launch_fwd(const FwdParams& p, int D, bool cached, hipStream_t
 int fwd_resident_wgs_64(bool cached);
 int fwd_resident_wgs_72(bool cached);
 int fwd_resident_wgs_128(bool cached);
+int fwd_resident_wgs_cached_128();
 int fwd_resident_wgs_decode_128(int bm);
 // Query rows per workgroup, keys per main-loop step and resident workgroups
 // per CU of the tile configuration the forward launcher picks for a shape.
