@@ -248,6 +248,49 @@ def test_small_hybrid_split_plans():
     assert (ns.value, nw.value) == (4, 1)
 
 
+@pytest.mark.parametrize("e4m3", [False, True])
+def test_cached_split_plan_fits_the_workspace(e4m3):
+    """Over a sweep of shapes and workspace budgets, the plan's partials fit the budget, a plan
+    with whole tiles leaves at least one tile split, and the workspace-size query covers the plan
+    of either visibility rule."""
+    lib = mw.load()
+    ns, nw = ctypes.c_int(), ctypes.c_int()
+    for (B, H, L, D, live, nq, ql) in [(1, 16, 2640, 128, 6, 4, 2640), (2, 12, 600, 128, 12, 8, 600),
+                                       (1, 8, 1500, 128, 2, 3, 1500), (1, 16, 2640, 128, 6, 1, 200),
+                                       (1, 3, 500, 128, 4, 2, 333), (2, 6, 96, 64, 3, 3, 96)]:
+        if e4m3 and D != 128:
+            continue
+        c = _lib.mw_kvcache()
+        if e4m3:
+            assert lib.mw_kvcache_init_fp8(ctypes.byref(c), A, A, live + 1, B, H, L, D, 0.02, 0.02) == mw.MW_OK
+        else:
+            assert lib.mw_kvcache_init(ctypes.byref(c), A, A, live + 1, B, H, L, D) == mw.MW_OK
+        c.head = live
+        need = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), nq, ql, live)
+        tq = nq * ql
+        for mode in (mw.MW_QUEUED_CAUSAL, mw.MW_QUEUED_ISOLATED):
+            for ws in (need, need // 2, need // 5, 1 << 20, 0):
+                assert lib.mw_chunk_attn_cached_plan(ctypes.byref(c), nq, ql, live, mode, ws, ctypes.byref(ns),
+                                                     ctypes.byref(nw)) == mw.MW_OK
+                n_splits, n_whole = ns.value, nw.value
+                assert n_splits >= 1 and n_whole >= 0
+                if n_splits == 1:
+                    assert n_whole == 0
+                    continue
+                # rows per tile of the configuration the launcher picks: 256, or for D = 128 cached
+                # attention with few rows 64 (<= 64) / 128 (bf16 <= 512, e4m3 <= 128)
+                if D != 128 or tq > (128 if e4m3 else 512):
+                    bm = 256
+                else:
+                    bm = 64 if tq <= 64 else (128 if (tq <= 128 or not e4m3) else 256)
+                nqt = -(-tq // bm)
+                assert n_whole < nqt
+                rows = min(tq, (nqt - n_whole) * bm)
+                assert n_splits * B * H * rows * (D + 2) * 4 <= ws
+                if ws == need:
+                    assert n_splits * B * H * rows * (D + 2) * 4 <= need
+
+
 def test_cached_split_plan_validation():
     lib = mw.load()
     c = new_cache(S=8, B=1, H=16, L=2640, D=128)
