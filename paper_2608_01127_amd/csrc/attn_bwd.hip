@@ -326,14 +326,12 @@ __device__ __forceinline__ void dq_body(const BwdParams& p, const int bh, const 
   const int e1f = min(T, (q0 / L + 1) * L);
   const int kend = min(T, ((min(q0 + BM, T) - 1) / L + 1) * L);
   const float c = p.scale_log2;
-  // -Delta depends only on the query (the lane's accumulator column): where
-  // registers allow (D < 128), a tile of it is the accumulator input of every
-  // dP product, so dS = P (dP - Delta) is one multiply per element; at D = 128
-  // the tile does not fit and -Delta is added per element.
-  constexpr bool NDL_TILE = D < 128;
-  f32x16 ndl[NDL_TILE ? RB : 1];
+  // -Delta depends only on the query (the lane's accumulator column): a tile
+  // of it is the accumulator input of every dP product, so dS = P (dP - Delta)
+  // is one multiply per element
+  f32x16 ndl[RB];
 #pragma unroll
-  for (int rb = 0; rb < (NDL_TILE ? RB : 1); ++rb)
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int i = 0; i < 16; ++i) ndl[rb][i] = ndlt[rb];
 
@@ -362,7 +360,7 @@ __device__ __forceinline__ void dq_body(const BwdParams& p, const int bh, const 
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
         s[rb] = zero16();
-        dp[rb] = NDL_TILE ? ndl[NDL_TILE ? rb : 0] : zero16();
+        dp[rb] = ndl[rb];
       }
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
@@ -383,7 +381,7 @@ __device__ __forceinline__ void dq_body(const BwdParams& p, const int bh, const 
             const int key = k0 + kb * 32 + acc_row(i, lane);
             pv = key < e1[rb] ? pv : 0.f;
           }
-          dp[rb][i] = pv * (NDL_TILE ? dp[rb][i] : dp[rb][i] + ndlt[rb]);  // P (dP - Delta)
+          dp[rb][i] = pv * dp[rb][i];  // P (dP - Delta)
         }
       }
 #pragma unroll
