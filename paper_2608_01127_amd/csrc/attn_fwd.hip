@@ -727,6 +727,10 @@ SplitPlan plan_splits(const FwdChoice& ch, double flops, int kv_bytes, int D, in
       if (ns > 1 && fwd_split_bytes(D, BH, Tq, ns) > ws_bytes) break;
       cands.push_back({t_stream / std::min(1.0, base * ns / cus) + part_time(Tq, ns), {ns, 0}});
     }
+  } else if (base >= 8.0 * slots) {
+    // eight or more rounds of workgroups: the last round is a small fraction
+    // of the call, so nothing is split
+    cands.push_back({t_mfma, {1, 0}});
   } else {
     // MFMA-bound: simulate the dispatch of one XCD (BH / 8 whole heads when
     // the heads divide over the 8 XCDs, else the whole GPU).  Key steps per
@@ -747,10 +751,12 @@ SplitPlan plan_splits(const FwdChoice& ch, double flops, int kv_bytes, int D, in
     const bool per_xcd = BH % 8 == 0;
     const int heads = per_xcd ? BH / 8 : BH;
     const int sl = (int)slots / (per_xcd ? 8 : 1);
-    // more than four rounds of workgroups gain nothing
+    // more than four rounds of workgroups gain nothing; at most 48 whole-tile
+    // counts per split count are priced (every one up to 48 query tiles)
     const int ns_cap = std::min(ns_max, std::max(8, (int)std::ceil(4.0 * slots / base)));
+    const int stride = (nqt + 47) / 48;
     for (int ns = 1; ns <= ns_cap; ++ns) {
-      for (int whole = ns == 1 ? nqt : 0; whole <= (ns == 1 ? nqt : nqt - 1); ++whole) {
+      for (int whole = ns == 1 ? nqt : 0; whole <= (ns == 1 ? nqt : nqt - 1); whole += (ns == 1 ? 1 : stride)) {
         const int rows = fwd_split_rows(ch.bm, Tq, SplitPlan{ns, whole});
         if (ns > 1 && fwd_split_bytes(D, BH, rows, ns) > ws_bytes) continue;
         const double t = split_makespan(steps, heads, sl, ns, whole, o_wg, o_part) * t_step +
