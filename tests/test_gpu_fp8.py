@@ -192,3 +192,40 @@ def test_fp8_paper_1b_streaming(mw, window):
     go = to_f64(o.contiguous())
     for b, h in heads:
         assert_close(f"o b{b} h{h}", go[b, h], ro[b, h], FP8_MAX_ABS, FP8_MEAN_ABS)
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_fp8_stream_config_sampled_heads(mw, mode):
+    """The streaming shape the bench times, in e4m3 (4 in-flight 2640-token chunks over a 6-chunk
+    window of an 8-slot ring, B1 H16 D128), with the call's own split plan (queued-causal: 32 whole
+    query tiles per head, the first chunk's 10 over 3 key ranges); heads 0 and 15 vs the oracle on
+    the dequantized codes."""
+    s = synth.STREAM
+    print(f"[case] fp8 {s.name} mode={mode}", flush=True)
+    ks, vs, qs = 0.011, 0.012, 0.0105
+    cache = mw.KVCache(s.slots, s.B, s.H, s.chunk_len, s.D, fp8=True, k_scale=ks, v_scale=vs)
+    hist = [(synth.normal_bf16((s.B, s.H, s.chunk_len, s.D), 9600 + 2 * i),
+             synth.normal_bf16((s.B, s.H, s.chunk_len, s.D), 9601 + 2 * i)) for i in range(s.slots)]
+    for kc, vc in hist:  # 8 commits, then keep the newest 6
+        mw.mw_kvcache_append(cache, to_gpu(kc), to_gpu(vc))
+    mw.mw_kvcache_evict(cache, s.slots - s.window)
+    ns, nw = mw.mw_chunk_attn_cached_plan(cache, s.n_queued, s.q_len, s.window, mode)
+    if mode == 0:
+        assert (ns, nw) == (3, 32)
+    inp = {n: synth.normal_bf16((s.B, s.H, s.n_queued * s.q_len, s.D), 9590 + i) for i, n in enumerate("qkv")}
+    q8 = mw.mw_quantize_fp8(to_gpu(inp["q"]), qs)
+    k8 = mw.mw_quantize_fp8(to_gpu(inp["k"]), ks)
+    v8 = mw.mw_quantize_fp8(to_gpu(inp["v"]), vs)
+    o, lse = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, s.n_queued, s.q_len, cache, qs, window=s.window, flags=mode,
+                                         want_lse=True)
+    sync()
+    dq = lambda b, sc: oracle.dequantize_fp8(codes(b, sc), sc)
+    win = hist[-s.window:]
+    heads = [(0, 0), (0, s.H - 1)]
+    ro, rl = oracle.cached_chunk_attn(dq(inp["q"], qs), dq(inp["k"], ks), dq(inp["v"], vs),
+                                      [dq(c[0], ks) for c in win], [dq(c[1], vs) for c in win], s.n_queued, s.q_len,
+                                      mode=mode, heads=heads)
+    go, gl = to_f64(o), to_f64(lse)
+    for b, h in heads:
+        assert_close(f"o b{b} h{h} plan {(ns, nw)}", go[b, h], ro[b, h], FP8_MAX_ABS, FP8_MEAN_ABS)
+        assert_close(f"lse b{b} h{h}", gl[b, h], rl[b, h], max_abs=2e-3, mean_abs=2e-4)
