@@ -232,13 +232,14 @@ def test_small_hybrid_split_plans():
     """The small shapes the GPU parity tests use for plans with whole and split query tiles."""
     lib = mw.load()
     ns, nw = ctypes.c_int(), ctypes.c_int()
-    c = new_cache(S=4, B=1, H=8, L=1500, D=128)
-    c.head = 2
-    for mode, plan in ((mw.MW_QUEUED_ISOLATED, (2, 6)), (mw.MW_QUEUED_CAUSAL, (2, 0))):
-        ws = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 3, 1500, 2)
-        assert lib.mw_chunk_attn_cached_plan(ctypes.byref(c), 3, 1500, 2, mode, ws, ctypes.byref(ns),
-                                             ctypes.byref(nw)) == mw.MW_OK
-        assert (ns.value, nw.value) == plan
+    for (H, D, window) in ((8, 128, 2), (16, 64, 1)):
+        c = new_cache(S=window + 2, B=1, H=H, L=1500, D=D)
+        c.head = window
+        for mode, plan in ((mw.MW_QUEUED_ISOLATED, (2, 6)), (mw.MW_QUEUED_CAUSAL, (2, 0))):
+            ws = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 3, 1500, window)
+            assert lib.mw_chunk_attn_cached_plan(ctypes.byref(c), 3, 1500, window, mode, ws, ctypes.byref(ns),
+                                                 ctypes.byref(nw)) == mw.MW_OK
+            assert (ns.value, nw.value) == plan
     c8 = _lib.mw_kvcache()
     assert lib.mw_kvcache_init_fp8(ctypes.byref(c8), A, A, 3, 1, 1, 300, 128, 0.02, 0.02) == mw.MW_OK
     c8.head = 1

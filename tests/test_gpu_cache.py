@@ -235,23 +235,26 @@ def test_few_rows_key_groups_vs_oracle(mw, split, mode, B, H, L, S, n_commit, wi
 
 
 @pytest.mark.parametrize("mode", [0, 1])
-def test_hybrid_split_plan_vs_oracle(mw, mode):
-    """Three 1500-token chunks over a 2-chunk window (B1 H8 D128).  Isolated, the split plan keeps
-    the 6 heaviest of each head's 18 query tiles whole and splits the others over 2 key ranges
-    (whole tiles write O directly, the merge covers only the split rows); queued-causal splits
-    every tile.  Both against the oracle and against the unsplit pass."""
-    B, H, D, L, S, nq = 1, 8, 128, 1500, 4, 3
-    print(f"[case] hybrid split plan mode={mode} B={B} H={H} D={D} L={L} nq={nq} w=2", flush=True)
+@pytest.mark.parametrize("H,D,window", [(8, 128, 2), (16, 64, 1)])
+def test_hybrid_split_plan_vs_oracle(mw, mode, H, D, window):
+    """Three 1500-token chunks over a 2-chunk (B1 H8 D128) or 1-chunk (B1 H16 D64, two row blocks
+    per wave) window.  Isolated, the split plan keeps the 6 heaviest of each head's 18 query tiles
+    whole and splits the others over 2 key ranges (whole tiles write O directly, the merge covers
+    only the split rows); queued-causal splits every tile.  Both against the oracle and against
+    the unsplit pass."""
+    B, L, nq = 1, 1500, 3
+    S = window + 2
+    print(f"[case] hybrid split plan mode={mode} B={B} H={H} D={D} L={L} nq={nq} w={window}", flush=True)
     cache = mw.KVCache(S, B, H, L, D)
-    chunks = make_chunks(2, B, H, L, D, seed=5100)
+    chunks = make_chunks(window, B, H, L, D, seed=5100 + D)
     for kc, vc in chunks:
         mw.mw_kvcache_append(cache, to_gpu(kc), to_gpu(vc))
-    ns, nw = mw.mw_chunk_attn_cached_plan(cache, nq, L, 2, mode)
+    ns, nw = mw.mw_chunk_attn_cached_plan(cache, nq, L, window, mode)
     assert (ns, nw) == ((2, 6) if mode == 1 else (2, 0))
-    inp = queued(B, H, nq, L, D, seed=5200)
+    inp = queued(B, H, nq, L, D, seed=5200 + D)
     args = (to_gpu(inp["q"]), to_gpu(inp["k_new"]), to_gpu(inp["v_new"]), nq, L, cache)
-    o, lse = mw.mw_chunk_attn_cached(*args, window=2, flags=mode, want_lse=True)
-    o1, lse1 = mw.mw_chunk_attn_cached(*args, window=2, flags=mode, want_lse=True, split=False)
+    o, lse = mw.mw_chunk_attn_cached(*args, window=window, flags=mode, want_lse=True)
+    o1, lse1 = mw.mw_chunk_attn_cached(*args, window=window, flags=mode, want_lse=True, split=False)
     sync()
     ro, rl = oracle.cached_chunk_attn(f64(inp["q"]), f64(inp["k_new"]), f64(inp["v_new"]),
                                       [f64(c[0]) for c in chunks], [f64(c[1]) for c in chunks], nq, L, mode=mode)
