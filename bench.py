@@ -2,8 +2,10 @@
 """Benchmark of the block-causal attention hot path on one MI355X.
 
 One step runs every row of the hot path once:
-  training   : block-causal attention forward + backward, B=2 H=12 T=10560 D=64,
-               8 chunks of 1320 tokens (3 latent frames x 440 tokens);
+  training   : block-causal attention forward + backward at B=1 H=16 T=42240
+               D=128, 16 chunks of 2640 tokens (3 latent frames x 880 tokens),
+               the largest training configuration, whose throughput is `value`;
+               and the same at B=2 H=12 T=10560 D=64, 8 chunks of 1320 tokens;
   streaming  : commit one 2640-token chunk to the 8-slot KV ring, evict down to a
                6-chunk window, re-shift the retained keys' temporal RoPE band by
                the evicted chunk's 3 latent-frame positions, and cached attention
@@ -11,9 +13,11 @@ One step runs every row of the hot path once:
                over that window.
 Inputs are seeded synthetic N(0,1) bf16 tensors resident in HBM before timing.
 
-Prints one JSON line.  `value` is the training forward+backward throughput in
-useful TFLOP/s (4 P D forward + 10 P D backward, P = visible query-key pairs),
-timed with HIP events on the launch stream over the K timed steps.
+Prints one JSON line.  `value` is the D=128 training forward+backward
+throughput in useful TFLOP/s (4 P D forward + 10 P D backward, P = visible
+query-key pairs), timed with HIP events on the launch stream over the K timed
+steps.  Outside the timed steps: the cache-bound decode shapes, a 200-step
+rollout, the paper's own shapes, the e4m3 variant and the CPU oracle baseline.
 """
 from __future__ import annotations
 
@@ -87,39 +91,107 @@ def read_traffic(kernel: str, digest: str):
         return None
 
 
-def cpu_baseline(target_s: float):
-    """The fp64 oracle, as it stands, on a bounded sample of the training workload:
-    forward + backward of whole heads of the D=64 shape, as many heads as fit in
-    about target_s seconds (at least one)."""
+def _oracle_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        return int(max([i.get("num_threads", 1) for i in threadpool_info()] or [1]))
+    except Exception:  # pragma: no cover
+        return len(os.sched_getaffinity(0))
+
+
+def cpu_baseline(target_s: float, d128_bits=None):
+    """The fp64 oracle, as it stands, timed on bounded samples of the three
+    headline workloads (about target_s seconds in all), each rate counted
+    with the same useful-FLOP rule as the GPU (14 P D for forward+backward,
+    4 P D for the cached call, P = visible pairs of the rows done):
+      - B1 H16 T42240 D128 L2640 training: evenly spaced 512-row query blocks of
+        head 0, each through the oracle's one-head forward and backward (the
+        work the whole-sequence functions do per row block); extrapolated from
+        those rows of one head;
+      - B2 H12 T10560 D64 L1320 training: whole heads;
+      - the cached call (4 queued 2640-token chunks over 6 committed chunks,
+        H16 D128): whole heads.
+    `value` is the D128 training sample's rate."""
     import numpy as np
     import oracle
     import synth
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        threads = len(os.sched_getaffinity(0))
-    s = synth.TRAIN_D64
-    bits = synth.training_inputs(s)
-    t = {n: synth.bf16_bits_to_f64(bits[n]) for n in bits}
-    heads_done = 0
+    threads = _oracle_threads()
+    budget = {"d128": 0.45 * target_s, "d64": 0.3 * target_s, "cached": 0.25 * target_s}
+    out = []
+
+    # --- B1 H16 T42240 D128: 512-row blocks of head 0, evenly spaced
+    s3 = synth.TRAIN_D128
+    bits = d128_bits if d128_bits is not None else synth.training_inputs(s3)
+    hq, hk, hv, hdo = (synth.bf16_bits_to_f64(bits[n][0, 0]) for n in ("q", "k", "v", "do"))
+    sc = 1.0 / math.sqrt(s3.D)
+    nblk = -(-s3.T // 512)
+    order = []
+    for stride in (16, 8, 4, 2, 1):  # coarse-to-fine sweep: every prefix is spread over the sequence
+        order += [b for b in range(0, nblk, stride) if b not in order]
+    pairs = blocks = 0
     t0 = time.perf_counter()
-    for b in range(s.B):
-        for h in range(s.H):
-            sl = (slice(b, b + 1), slice(h, h + 1))
-            q, k, v, do = (t[n][sl] for n in ("q", "k", "v", "do"))
-            oracle.block_causal_attn_fwd(q, k, v, s.chunk_len)
-            oracle.block_causal_attn_bwd(q, k, v, do, s.chunk_len)
-            heads_done += 1
-            if time.perf_counter() - t0 >= target_s:
-                break
-        if time.perf_counter() - t0 >= target_s:
+    for blk in order:
+        rows = np.arange(blk * 512, min(s3.T, blk * 512 + 512))
+        vis = oracle.block_causal_visible(rows, s3.T, s3.chunk_len)
+        oracle.attention_fwd(hq[rows], hk, hv, vis, sc)
+        oracle.attention_bwd(hq[rows], hk, hv, hdo[rows], vis, sc)
+        pairs += int(vis.sum())
+        blocks += 1
+        if time.perf_counter() - t0 >= budget["d128"]:
             break
     dt = time.perf_counter() - t0
-    flops = 14.0 * pairs_block_causal(1, heads_done, s.T, s.chunk_len) * s.D
-    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"fp64 numpy oracle fwd+bwd of {heads_done} of {s.B * s.H} heads of {s.name} "
-                      f"({dt:.1f} s), useful-FLOP count as the GPU"}
+    out.append({"workload": s3.name, "value": round(14.0 * pairs * s3.D / dt / 1e12, 6), "unit": "TFLOP/s",
+                "seconds": round(dt, 2),
+                "sample": f"{blocks} of {nblk} evenly spaced 512-row query blocks of head 0 of 16, fwd+bwd, "
+                          f"extrapolated from one head"})
+
+    # --- B2 H12 T10560 D64: whole heads
+    s2 = synth.TRAIN_D64
+    b2 = synth.training_inputs(s2)
+    t2 = {n: synth.bf16_bits_to_f64(b2[n]) for n in b2}
+    heads = 0
+    t0 = time.perf_counter()
+    for b in range(s2.B):
+        for h in range(s2.H):
+            sl = (slice(b, b + 1), slice(h, h + 1))
+            q, k, v, do = (t2[n][sl] for n in ("q", "k", "v", "do"))
+            oracle.block_causal_attn_fwd(q, k, v, s2.chunk_len)
+            oracle.block_causal_attn_bwd(q, k, v, do, s2.chunk_len)
+            heads += 1
+            if time.perf_counter() - t0 >= budget["d64"]:
+                break
+        if time.perf_counter() - t0 >= budget["d64"]:
+            break
+    dt = time.perf_counter() - t0
+    flops = 14.0 * pairs_block_causal(1, heads, s2.T, s2.chunk_len) * s2.D
+    out.append({"workload": s2.name, "value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "seconds": round(dt, 2),
+                "sample": f"fwd+bwd of {heads} of {s2.B * s2.H} whole heads"})
+
+    # --- cached call: whole heads of the streaming step
+    st = synth.STREAM
+    sb = synth.stream_step_inputs(st, 0, which=("q", "k_new", "v_new"))
+    win = [synth.stream_step_inputs(st, i % 4, which=("k_commit", "v_commit")) for i in range(st.window)]
+    heads = 0
+    t0 = time.perf_counter()
+    for h in range(st.H):
+        sl = (slice(0, 1), slice(h, h + 1))
+        q, kn, vn = (synth.bf16_bits_to_f64(sb[n][sl]) for n in ("q", "k_new", "v_new"))
+        wk = [synth.bf16_bits_to_f64(w["k_commit"][sl]) for w in win]
+        wv = [synth.bf16_bits_to_f64(w["v_commit"][sl]) for w in win]
+        oracle.cached_chunk_attn(q, kn, vn, wk, wv, st.n_queued, st.q_len)
+        heads += 1
+        if time.perf_counter() - t0 >= budget["cached"]:
+            break
+    dt = time.perf_counter() - t0
+    flops = 4.0 * pairs_cached(1, heads, st.window, st.chunk_len, st.n_queued, st.q_len) * st.D
+    out.append({"workload": st.name + " cached call", "value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s",
+                "seconds": round(dt, 2), "sample": f"{heads} of {st.B * st.H} whole heads"})
+
+    head = out[0]
+    return {"value": head["value"], "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"fp64 numpy oracle on {s3.name}: {head['sample']} ({head['seconds']} s), useful-FLOP "
+                      f"count as the GPU; the other headline workloads in by_config",
+            "by_config": out}
 
 
 def decode_shapes(mw, torch, cache, st, dev, reps=20):
@@ -359,10 +431,56 @@ def fp8_stream(mw, torch, dev, st, reps=10):
     return out
 
 
+def rollout(mw, torch, dev, st, steps=200):
+    """The long-horizon rollout: 200 chunk steps from an empty ring, each one
+    commit (append), eviction down to the 6-chunk window, and cached attention
+    of the 4 queued chunks over the live window (1, 2, ... 6 committed chunks,
+    then 6 with the ring wrapping every 8 commits).  Timed as a whole with HIP
+    events on the launch stream; useful TFLOP/s counts each step's visible
+    pairs with its actual window."""
+    g = torch.Generator(device=dev).manual_seed(5)
+    B, H, D, L, nq, ql, W = st.B, st.H, st.D, st.chunk_len, st.n_queued, st.q_len, st.window
+    cache = mw.KVCache(st.slots, B, H, L, D, device=dev)
+    srcs = [tuple(torch.randn(B, H, L, D, device=dev, generator=g).to(torch.bfloat16) for _ in range(2))
+            for _ in range(4)]
+    q, kn, vn = (torch.randn(B, H, nq * ql, D, device=dev, generator=g).to(torch.bfloat16) for _ in range(3))
+    o = torch.empty_like(q)
+    ws = torch.empty(max(16, mw.mw_chunk_attn_cached_workspace_size(cache, nq, ql, W)), dtype=torch.uint8,
+                     device=dev)
+    windows = []
+
+    def run(n, record):
+        for t in range(n):
+            mw.mw_kvcache_append(cache, *srcs[t % 4])
+            mw.mw_kvcache_evict(cache, max(0, cache.live - W))
+            mw.mw_chunk_attn_cached(q, kn, vn, nq, ql, cache, window=cache.live, out=o, workspace=ws)
+            if record:
+                windows.append(cache.live)
+
+    run(8, False)  # warm-up on a scratch ring (plans memoised, code loaded)
+    cache = mw.KVCache(st.slots, B, H, L, D, device=dev)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    run(steps, True)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    F = sum(4.0 * pairs_cached(B, H, w, L, nq, ql) * D for w in windows)
+    return {"workload": synth_name(st, steps), "steps": steps, "total_ms": round(ms, 3),
+            "ms_per_step": round(ms / steps, 4), "tflops": round(F / (ms * 1e-3) / 1e12, 2),
+            "append_bytes_per_step": 4 * B * H * L * D * 2}
+
+
+def synth_name(st, steps):
+    return f"rollout_B{st.B}H{st.H}D{st.D}L{st.chunk_len}_nq{st.n_queued}_W{st.window}_S{st.slots}_{steps}steps"
+
+
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1"}))
+        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1 (the hot path is "
+                                   "measured on one GPU's share; sharding is a design note only)"}))
         sys.exit(2)
     import numpy as np
     import torch
@@ -380,14 +498,31 @@ def main():
         return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
 
     # ------------------------------------------------------------------ inputs (resident in HBM)
-    tr = synth.TRAIN_D64
-    tb = synth.training_inputs(tr)
-    q, k, v, do = (up(tb[n]) for n in ("q", "k", "v", "do"))
-    B, H, T, D, L = tr.B, tr.H, tr.T, tr.D, tr.chunk_len
-    o = torch.empty_like(q)
-    lse = torch.empty((B, H, T), dtype=torch.float32, device=dev)
-    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
-    ws = torch.empty(mw.mw_block_causal_attn_bwd_workspace_size(B, H, T, D), dtype=torch.uint8, device=dev)
+    class Train:
+        """One training workload's tensors and useful FLOPs."""
+
+        def __init__(self, shape, bits):
+            self.s = shape
+            self.q, self.k, self.v, self.do = (up(bits[n]) for n in ("q", "k", "v", "do"))
+            B, H, T, D = shape.B, shape.H, shape.T, shape.D
+            self.o = torch.empty_like(self.q)
+            self.lse = torch.empty((B, H, T), dtype=torch.float32, device=dev)
+            self.dq, self.dk, self.dv = (torch.empty_like(self.q) for _ in range(3))
+            self.ws = torch.empty(mw.mw_block_causal_attn_bwd_workspace_size(B, H, T, D), dtype=torch.uint8,
+                                  device=dev)
+            P = pairs_block_causal(B, H, T, shape.chunk_len)
+            self.F_fwd, self.F_bwd = 4.0 * P * D, 10.0 * P * D
+
+        def fwd(self):
+            mw.mw_block_causal_attn_fwd(self.q, self.k, self.v, self.s.chunk_len, out=self.o, lse=self.lse)
+
+        def bwd(self):
+            mw.mw_block_causal_attn_bwd(self.q, self.k, self.v, self.o, self.do, self.lse, self.s.chunk_len,
+                                        workspace=self.ws, dq=self.dq, dk=self.dk, dv=self.dv)
+
+    bits128 = synth.training_inputs(synth.TRAIN_D128)
+    t128 = Train(synth.TRAIN_D128, bits128)   # the largest training configuration: the headline
+    t64 = Train(synth.TRAIN_D64, synth.training_inputs(synth.TRAIN_D64))
 
     st = synth.STREAM
     cache = mw.KVCache(st.slots, st.B, st.H, st.chunk_len, st.D, device=dev)
@@ -405,8 +540,6 @@ def main():
         mw.mw_kvcache_append(cache, *commits[i % n_src])
     torch.cuda.synchronize()
 
-    P_train = pairs_block_causal(B, H, T, L)
-    F_fwd, F_bwd = 4.0 * P_train * D, 10.0 * P_train * D
     P_st = pairs_cached(st.B, st.H, st.window, st.chunk_len, st.n_queued, st.q_len, causal=True)
     F_st = 4.0 * P_st * st.D
     chunk_bytes = st.B * st.H * st.chunk_len * st.D * 2
@@ -421,23 +554,30 @@ def main():
     frames_per_chunk = 3
     bytes_rope = 2 * st.window * st.B * st.H * st.chunk_len * rope_cnt * 2  # band read + written
 
+    PH = ["fwd_d128", "bwd_d128", "fwd_d64", "bwd_d64", "append", "rope_shift", "cached"]
+
     def step(rec=None):
-        e = [ev() for _ in range(6)] if rec is not None else None
-        if e: e[0].record()
-        mw.mw_block_causal_attn_fwd(q, k, v, L, out=o, lse=lse)
-        if e: e[1].record()
-        mw.mw_block_causal_attn_bwd(q, k, v, o, do, lse, L, workspace=ws, dq=dq, dk=dk, dv=dv)
-        if e: e[2].record()
+        e = [ev() for _ in range(len(PH) + 1)] if rec is not None else None
+        mark = (lambda i: e[i].record()) if e else (lambda i: None)
+        mark(0)
+        t128.fwd()
+        mark(1)
+        t128.bwd()
+        mark(2)
+        t64.fwd()
+        mark(3)
+        t64.bwd()
+        mark(4)
         mw.mw_kvcache_append(cache, *commits[step_i[0] % n_src])
         step_i[0] += 1
-        if e: e[3].record()
+        mark(5)
         n_ev = cache.live - st.window
         mw.mw_kvcache_evict(cache, n_ev)
         mw.mw_kvcache_rope_shift(cache, n_ev * frames_per_chunk, rope_off, rope_cnt)
-        if e: e[4].record()
+        mark(6)
         mw.mw_chunk_attn_cached(sq, skn, svn, st.n_queued, st.q_len, cache, window=st.window,
                                 flags=mw.MW_QUEUED_CAUSAL, out=so, workspace=ws_c)
-        if e: e[5].record()
+        mark(7)
         if rec is not None:
             rec.append(e)
 
@@ -454,36 +594,49 @@ def main():
     torch.cuda.synchronize()
     K = args.steps
     total_ms = t_start.elapsed_time(t_end)
-    ph = {"fwd": 0.0, "bwd": 0.0, "append": 0.0, "rope_shift": 0.0, "cached": 0.0}
-    for e in recs:
-        ph["fwd"] += e[0].elapsed_time(e[1])
-        ph["bwd"] += e[1].elapsed_time(e[2])
-        ph["append"] += e[2].elapsed_time(e[3])
-        ph["rope_shift"] += e[3].elapsed_time(e[4])
-        ph["cached"] += e[4].elapsed_time(e[5])
-    ph = {n: t / K for n, t in ph.items()}
+    ph = {n: sum(e[i].elapsed_time(e[i + 1]) for e in recs) / K for i, n in enumerate(PH)}
     ms_step = total_ms / K
-    train_ms = ph["fwd"] + ph["bwd"]
-    value = (F_fwd + F_bwd) / (train_ms * 1e-3) / 1e12
-
-    # dominant launch of the step: the cached-attention call.  With a key-range
-    # split it is the split kernel followed by the small combine kernel; the
-    # events bracket both, so the duration is the call's.
-    cached_tflops = F_st / (ph["cached"] * 1e-3) / 1e12
+    tfl = lambda F, ms: F / (ms * 1e-3) / 1e12
+    gbs = lambda nb, ms: nb / (ms * 1e-3) / 1e9
+    value = tfl(t128.F_fwd + t128.F_bwd, ph["fwd_d128"] + ph["bwd_d128"])
+    value64 = tfl(t64.F_fwd + t64.F_bwd, ph["fwd_d64"] + ph["bwd_d64"])
+    cached_tflops = tfl(F_st, ph["cached"])
     n_splits, n_whole = mw.mw_chunk_attn_cached_plan(cache, st.n_queued, st.q_len, st.window, 0, ws_c.numel())
-    digest = source_digest(["paper_2608_01127_amd/csrc/attn_fwd.hip", "paper_2608_01127_amd/csrc/mw_device.h",
-                            "paper_2608_01127_amd/csrc/mw_kernels.h", "paper_2608_01127_amd/build.py"])
-    traffic = read_traffic("attn_fwd_cached", digest)
-    kname = "attn_fwd_kernel<128, true, 8, 64, 1, 1>"
-    if n_splits > 1:
-        kname += (f" ({n_whole} whole query tiles per head, the others over {n_splits} key ranges)"
-                  " + attn_combine_kernel<128>")
-    roofline = {"kernel": kname + " (cached chunk attention call)", "bound": "mfma",
-                "achieved": round(cached_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(cached_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
-                "algorithmic_flops_per_launch": F_st, "avg_launch_ms": round(ph["cached"], 4),
-                "n_splits": n_splits, "n_whole": n_whole}
 
+    # Dominant launch of the step: the D128 training backward call
+    # (mw_block_causal_attn_bwd: row terms, then dK/dV, then dQ).  Its
+    # algorithmic FLOPs are the backward's useful 10 P D; the events bracket
+    # the three kernels, so the duration is the call's.
+    bwd_digest = source_digest(["paper_2608_01127_amd/csrc/attn_bwd.hip", "paper_2608_01127_amd/csrc/mw_device.h",
+                                "paper_2608_01127_amd/csrc/mw_kernels.h", "paper_2608_01127_amd/build.py"])
+    roofline = {"kernel": "mw_block_causal_attn_bwd at B1 H16 T42240 D128 L2640 = bwd_rowterms_kernel<128> + "
+                          "bwd_dkdv_kernel<128, 4, 64, 1> + bwd_dq_kernel<128, 4, 1, 64>",
+                "bound": "mfma", "achieved": round(tfl(t128.F_bwd, ph["bwd_d128"]), 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(tfl(t128.F_bwd, ph["bwd_d128"]) / PEAK_BF16_TFLOPS, 4),
+                "traffic": read_traffic("train_bwd_d128", bwd_digest),
+                "algorithmic_flops_per_launch": t128.F_bwd, "avg_launch_ms": round(ph["bwd_d128"], 4)}
+
+    def mf(name, F, ms):
+        a = tfl(F, ms)
+        return {"phase": name, "bound": "mfma", "achieved": round(a, 2), "unit": "TFLOP/s", "peak": PEAK_BF16_TFLOPS,
+                "frac": round(a / PEAK_BF16_TFLOPS, 4), "ms": round(ms, 4)}
+
+    def hb(name, nb, ms):
+        a = gbs(nb, ms)
+        return {"phase": name, "bound": "hbm", "achieved": round(a, 1), "unit": "GB/s", "peak": PEAK_HBM_GBS,
+                "frac": round(a / PEAK_HBM_GBS, 4), "ms": round(ms, 4)}
+
+    fwd_digest = source_digest(["paper_2608_01127_amd/csrc/attn_fwd.hip", "paper_2608_01127_amd/csrc/mw_device.h",
+                                "paper_2608_01127_amd/csrc/mw_kernels.h", "paper_2608_01127_amd/build.py"])
+    cached_rl = mf("cached chunk attention call", F_st, ph["cached"])
+    cached_rl["traffic"] = read_traffic("attn_fwd_cached", fwd_digest)
+    cached_rl["n_splits"], cached_rl["n_whole"] = n_splits, n_whole
+    rooflines = [mf("train fwd D128", t128.F_fwd, ph["fwd_d128"]), mf("train bwd D128", t128.F_bwd, ph["bwd_d128"]),
+                 mf("train fwd D64", t64.F_fwd, ph["fwd_d64"]), mf("train bwd D64", t64.F_bwd, ph["bwd_d64"]),
+                 cached_rl, hb("append (commit)", bytes_append, ph["append"]),
+                 hb("rope re-shift", bytes_rope, ph["rope_shift"])]
+
+    s3, s2 = synth.TRAIN_D128, synth.TRAIN_D64
     res = {
         "metric": "block-causal attn fwd+bwd TFLOP/s (% bf16 MFMA peak); cached-chunk attn GB/s",
         "value": round(value, 2),
@@ -497,29 +650,35 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"{tr.name} fwd+bwd + {st.name} streaming step",
-                   "train": {"B": B, "H": H, "T": T, "D": D, "chunk_len": L},
+        "config": {"workload": f"{s3.name} fwd+bwd (value) + {s2.name} fwd+bwd + {st.name} streaming step",
+                   "train": {"B": s3.B, "H": s3.H, "T": s3.T, "D": s3.D, "chunk_len": s3.chunk_len},
+                   "train_d64": {"B": s2.B, "H": s2.H, "T": s2.T, "D": s2.D, "chunk_len": s2.chunk_len},
                    "stream": {"B": st.B, "H": st.H, "D": st.D, "chunk_len": st.chunk_len, "n_queued": st.n_queued,
                               "q_len": st.q_len, "window": st.window, "slots": st.slots,
                               "visibility": "queued-causal"}},
         "frac_bf16_peak": round(value / PEAK_BF16_TFLOPS, 4),
         "phases_ms": {n: round(t, 4) for n, t in ph.items()},
-        "train_fwd_tflops": round(F_fwd / (ph["fwd"] * 1e-3) / 1e12, 2),
-        "train_bwd_tflops": round(F_bwd / (ph["bwd"] * 1e-3) / 1e12, 2),
-        "cached_attn": {"tflops": round(cached_tflops, 2), "gbs": round(bytes_cached / (ph["cached"] * 1e-3) / 1e9, 1),
+        "train_d128": {"fwd_tflops": round(tfl(t128.F_fwd, ph["fwd_d128"]), 2),
+                       "bwd_tflops": round(tfl(t128.F_bwd, ph["bwd_d128"]), 2), "fwd_bwd_tflops": round(value, 2)},
+        "train_d64": {"fwd_tflops": round(tfl(t64.F_fwd, ph["fwd_d64"]), 2),
+                      "bwd_tflops": round(tfl(t64.F_bwd, ph["bwd_d64"]), 2), "fwd_bwd_tflops": round(value64, 2),
+                      "frac_bf16_peak": round(value64 / PEAK_BF16_TFLOPS, 4)},
+        "cached_attn": {"tflops": round(cached_tflops, 2), "gbs": round(gbs(bytes_cached, ph["cached"]), 1),
                         "frac_bf16_peak": round(cached_tflops / PEAK_BF16_TFLOPS, 4)},
-        "append": {"gbs": round(bytes_append / (ph["append"] * 1e-3) / 1e9, 1),
-                   "frac_hbm_peak": round(bytes_append / (ph["append"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+        "append": {"gbs": round(gbs(bytes_append, ph["append"]), 1),
+                   "frac_hbm_peak": round(gbs(bytes_append, ph["append"]) / PEAK_HBM_GBS, 4)},
         "rope_shift": {"positions": frames_per_chunk, "band": [rope_off, rope_off + rope_cnt],
-                       "gbs": round(bytes_rope / (ph["rope_shift"] * 1e-3) / 1e9, 1),
-                       "frac_hbm_peak": round(bytes_rope / (ph["rope_shift"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)},
+                       "gbs": round(gbs(bytes_rope, ph["rope_shift"]), 1),
+                       "frac_hbm_peak": round(gbs(bytes_rope, ph["rope_shift"]) / PEAK_HBM_GBS, 4)},
         "roofline": roofline,
+        "rooflines": rooflines,
     }
     res["decode"] = decode_shapes(mw, torch, cache, st, dev)
+    res["rollout"] = rollout(mw, torch, dev, st)
     res["paper_1b"] = paper_shapes(mw, torch, dev)
     res["fp8_stream"] = fp8_stream(mw, torch, dev, st)
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(args.cpu_seconds, bits128)
     else:
         res["cpu_baseline"] = None
     print(json.dumps(res), flush=True)

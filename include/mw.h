@@ -42,7 +42,7 @@ typedef void* mw_stream_t; /* a hipStream_t */
 typedef enum {
   MW_OK = 0,
   MW_EINVAL = -1,        /* null pointer, non-positive size, inconsistent sizes */
-  MW_EUNSUPPORTED = -2,  /* head dimension other than 64 or 128, or a limit exceeded */
+  MW_EUNSUPPORTED = -2,  /* head dimension other than 64, 72 or 128, or a limit exceeded */
   MW_EALIGN = -3,        /* a pointer that is not 16-byte aligned */
   MW_EFULL = -4,         /* append to a ring whose slots are all live */
   MW_EEMPTY = -5,        /* evict more chunks than are live */
@@ -86,7 +86,7 @@ typedef struct {
  *
  * q, k, v, o : bf16 [B, H, T, D]
  * lse        : fp32 [B, H, T]  (needed by the backward pass)
- * D          : 64 or 128.  scale > 0 (the usual choice is 1/sqrt(D)).
+ * D          : 64, 72 or 128.  scale > 0 (the usual choice is 1/sqrt(D)).
  * Arithmetic: bf16 products, fp32 accumulation and softmax; the softmax
  * probabilities are rounded to bf16 before the product with V; O is rounded
  * to bf16 (nearest even).
@@ -167,7 +167,7 @@ typedef struct {
 
 /* Initialise an empty ring over k_slots/v_slots (bf16 [S,B,H,L,D]), without a
  * sink; no device work.
- * Errors: MW_EINVAL (null, sizes < 1), MW_EALIGN, MW_EUNSUPPORTED (D not 64/128). */
+ * Errors: MW_EINVAL (null, sizes < 1), MW_EALIGN, MW_EUNSUPPORTED (D not 64, 72 or 128). */
 int mw_kvcache_init(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, int H, int L, int D);
 
 /* Sink anchor (Sec. 3.5): the initial clean context kept permanently, outside

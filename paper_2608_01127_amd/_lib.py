@@ -177,6 +177,18 @@ def _strides(*ts):
     return arr
 
 
+def _check_lse(lse, shape, dev) -> None:
+    """An lse output (or None): fp32, contiguous, of the given shape, on `dev`."""
+    if lse is None:
+        return
+    torch = _torch()
+    if lse.dtype != torch.float32 or tuple(lse.shape) != tuple(shape) or not lse.is_contiguous():
+        raise ValueError(f"lse must be a contiguous fp32 tensor of shape {tuple(shape)}, got "
+                         f"{lse.dtype} {tuple(lse.shape)}")
+    if lse.device != dev:
+        raise ValueError("lse must be on the device of the inputs")
+
+
 def _same_device(*ts):
     dev = ts[0].device
     for t in ts:
@@ -199,9 +211,10 @@ def mw_block_causal_attn_fwd(q, k, v, chunk_len: int, scale=None, out=None, lse=
     o = torch.empty_like(q) if out is None else out
     lse = torch.empty((B, H, T), dtype=torch.float32, device=dev) if lse is None else lse
     _bf16_4d("out", o, view=True)
-    if o.shape != q.shape or lse.shape != (B, H, T) or lse.dtype != torch.float32 or not lse.is_contiguous():
-        raise ValueError("out/lse have the wrong shape or dtype")
-    _same_device(q, o, lse)
+    if o.shape != q.shape:
+        raise ValueError("out must have the shape of q")
+    _same_device(q, o)
+    _check_lse(lse, (B, H, T), dev)
     _check(load().mw_block_causal_attn_fwd_strided(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
                                                    _strides(q, k, v, o), B, H, T, D, int(chunk_len), scale,
                                                    _stream_handle(dev)))
@@ -320,10 +333,10 @@ def mw_kvcache_append(cache: KVCache, k_chunk, v_chunk) -> int:
         if tuple(t.shape) != (d.B, d.H, d.L, d.D):
             raise ValueError(f"{n} must be [B,H,L,D] = {(d.B, d.H, d.L, d.D)}")
     dev = _same_device(cache.k_slots, k_chunk, v_chunk)
-    slot = int(d.head % d.S)
     _check(load().mw_kvcache_append_strided(ctypes.byref(d), _ptr(k_chunk), _ptr(v_chunk),
                                             _strides(k_chunk, v_chunk), _stream_handle(dev)))
-    return slot
+    # the slot the library wrote: the newest committed chunk's, by the library's own rule
+    return _check(load().mw_kvcache_slot_of(ctypes.byref(d), int(d.head) - 1))
 
 
 def mw_kvcache_evict(cache: KVCache, n_chunks: int) -> None:
@@ -384,6 +397,7 @@ def mw_chunk_attn_cached(q, k_new, v_new, n_queued: int, q_len: int, cache: KVCa
         raise ValueError("out must have the shape of q")
     if want_lse and lse is None:
         lse = torch.empty((d.B, d.H, n_queued * q_len), dtype=torch.float32, device=dev)
+    _check_lse(lse, (d.B, d.H, n_queued * q_len), dev)
     if split and workspace is None:
         need = mw_chunk_attn_cached_workspace_size(cache, n_queued, q_len, window)
         workspace = torch.empty(need, dtype=torch.uint8, device=dev) if need > 0 else None
@@ -433,6 +447,7 @@ def mw_chunk_attn_cached_fp8(q8, k8_new, v8_new, n_queued: int, q_len: int, cach
         raise ValueError("out must have the shape of q8")
     if want_lse and lse is None:
         lse = torch.empty((d.B, d.H, n_queued * q_len), dtype=torch.float32, device=dev)
+    _check_lse(lse, (d.B, d.H, n_queued * q_len), dev)
     if split and workspace is None:
         need = mw_chunk_attn_cached_workspace_size(cache, n_queued, q_len, window)
         workspace = torch.empty(need, dtype=torch.uint8, device=dev) if need > 0 else None

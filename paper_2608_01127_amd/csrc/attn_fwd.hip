@@ -1,8 +1,12 @@
 // Block-causal attention forward and cached chunk attention (gfx950).
 //
-// One workgroup of 4 waves computes 128 query rows (32 per wave) of one
-// (batch, head).  Keys are visited in steps of 64; each step stages the K and
-// V tile in LDS once for all four waves.  Per wave and step:
+// One workgroup computes 256 query rows of one (batch, head): 4 waves of two
+// 32-row blocks at D = 64, 8 waves of one 32-row block at D = 72 and 128
+// (FwdCfg).  Cached attention with at most 512 queued rows runs 64- or
+// 128-row workgroups whose 8 waves split each key step into key groups
+// (FwdDecodeCfg).  Keys are visited in steps of 64 (128 for the key-group
+// configurations); each step stages the K and V tile in LDS once for all the
+// waves.  Per wave, 32-row block and 32-key block:
 //   S^T[key][q] = K Q^T              (bf16 MFMA 32x32x16, fp32 accumulate;
 //                                     Q stays in registers as the B operand)
 //   online softmax over keys         (a query is one lane column of S^T, so

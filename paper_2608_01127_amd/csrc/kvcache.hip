@@ -89,7 +89,7 @@ hipError_t launch_rope_shift(uint16_t* k_slots, long long slot_stride, int S, in
 }
 hipError_t launch_kv_copy(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_dst, uint16_t* v_dst,
                           long long n_elems, hipStream_t stream) {
-  const long long n16 = n_elems / 8;  // n_elems is a multiple of 8 (D is 64 or 128)
+  const long long n16 = n_elems / 8;  // n_elems is a multiple of 8 (D is 64, 72 or 128)
   long long blocks = (n16 + 255) / 256;
   if (blocks > 256 * 16) blocks = 256 * 16;
   if (blocks < 1) blocks = 1;

@@ -413,3 +413,22 @@ def test_fp8_workspace_size_policy():
     small = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 1, 128, 6)
     assert small % (16 * 128 * 130 * 4) == 0 and small // (16 * 128 * 130 * 4) >= 8
 
+
+
+def test_lse_output_checks():
+    """The binding's check of a caller-supplied lse (cached calls, bf16 and e4m3, and the
+    training forward) rejects a wrong dtype, shape, layout or device before any launch."""
+    import torch
+    shape = (1, 2, 6)
+    dev = torch.device("cpu")
+    _lib._check_lse(None, shape, dev)
+    _lib._check_lse(torch.empty(shape, dtype=torch.float32), shape, dev)
+    bad = [torch.empty(shape, dtype=torch.bfloat16),                    # wrong dtype
+           torch.empty((1, 2), dtype=torch.float32),                     # [B,H]
+           torch.empty((1, 2, 5), dtype=torch.float32),                  # too few rows
+           torch.empty((1, 6, 2), dtype=torch.float32).transpose(1, 2)]  # not contiguous
+    for t in bad:
+        with pytest.raises(ValueError):
+            _lib._check_lse(t, shape, dev)
+    with pytest.raises(ValueError):
+        _lib._check_lse(torch.empty(shape, dtype=torch.float32), shape, torch.device("meta"))

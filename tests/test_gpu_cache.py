@@ -167,6 +167,29 @@ def test_ring_errors_and_slots(mw):
     assert cache.slot_of(0) == -1
 
 
+def test_cached_rejects_bad_lse(mw):
+    """A caller-supplied lse of the wrong dtype, shape or layout raises before any launch, for
+    the bf16 and the e4m3 cached calls (the kernels write fp32 at [b, h, row])."""
+    import torch
+    B, H, D, L, S, nq = 1, 2, 128, 32, 3, 2
+    q = to_gpu(synth.normal_bf16((B, H, nq * L, D), 5))
+    q8 = mw.mw_quantize_fp8(q, 0.01)
+    bad = [torch.empty((B, H, nq * L), dtype=torch.bfloat16, device="cuda"),
+           torch.empty((B, H), dtype=torch.float32, device="cuda"),
+           torch.empty((B, H, nq * L - 1), dtype=torch.float32, device="cuda"),
+           torch.empty((B, nq * L, H), dtype=torch.float32, device="cuda").transpose(1, 2)]
+    for fp8 in (False, True):
+        cache = mw.KVCache(S, B, H, L, D, fp8=fp8, k_scale=0.01, v_scale=0.01)
+        mw.mw_kvcache_append(cache, q[:, :, :L], q[:, :, :L])
+        for lse in bad:
+            with pytest.raises(ValueError):
+                if fp8:
+                    mw.mw_chunk_attn_cached_fp8(q8, q8, q8, nq, L, cache, 0.01, lse=lse)
+                else:
+                    mw.mw_chunk_attn_cached(q, q, q, nq, L, cache, lse=lse)
+    sync()
+
+
 @pytest.mark.parametrize("q_len", [64, 128, 256, 300, 512])
 def test_decode_shape_split_vs_oracle(mw, q_len):
     """One short queued chunk over a full 6-chunk window (B1 H16 D128, 2640-token chunks):

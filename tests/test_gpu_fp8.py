@@ -229,3 +229,35 @@ def test_fp8_stream_config_sampled_heads(mw, mode):
     for b, h in heads:
         assert_close(f"o b{b} h{h} plan {(ns, nw)}", go[b, h], ro[b, h], FP8_MAX_ABS, FP8_MEAN_ABS)
         assert_close(f"lse b{b} h{h}", gl[b, h], rl[b, h], max_abs=2e-3, mean_abs=2e-4)
+
+
+@pytest.mark.parametrize("q_len", [64, 256])
+def test_fp8_decode_full_window(mw, q_len):
+    """The e4m3 cache-bound decode shapes the benchmark times: one queued chunk of q_len tokens
+    over the full window of the streaming shape (6 committed 2640-token chunks of an 8-slot ring,
+    B1 H16 D128), with the call's own key-range split; every head against the oracle on the
+    dequantized codes."""
+    s = synth.STREAM
+    print(f"[case] fp8 decode q_len={q_len} over {s.window} x {s.chunk_len}", flush=True)
+    ks, vs, qs = 0.011, 0.012, 0.0105
+    cache = mw.KVCache(s.slots, s.B, s.H, s.chunk_len, s.D, fp8=True, k_scale=ks, v_scale=vs)
+    hist = [(synth.normal_bf16((s.B, s.H, s.chunk_len, s.D), 9700 + 2 * i),
+             synth.normal_bf16((s.B, s.H, s.chunk_len, s.D), 9701 + 2 * i)) for i in range(s.slots + 1)]
+    for kc, vc in hist:  # 9 commits: the ring wraps; keep the newest 6
+        if cache.live == s.slots:
+            mw.mw_kvcache_evict(cache, 1)
+        mw.mw_kvcache_append(cache, to_gpu(kc), to_gpu(vc))
+    mw.mw_kvcache_evict(cache, cache.live - s.window)
+    ns, _ = mw.mw_chunk_attn_cached_plan(cache, 1, q_len, s.window)
+    inp = {n: synth.normal_bf16((s.B, s.H, q_len, s.D), 9690 + i) for i, n in enumerate("qkv")}
+    q8 = mw.mw_quantize_fp8(to_gpu(inp["q"]), qs)
+    k8 = mw.mw_quantize_fp8(to_gpu(inp["k"]), ks)
+    v8 = mw.mw_quantize_fp8(to_gpu(inp["v"]), vs)
+    o, lse = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, 1, q_len, cache, qs, window=s.window, want_lse=True)
+    sync()
+    dq = lambda b, sc: oracle.dequantize_fp8(codes(b, sc), sc)
+    win = hist[-s.window:]
+    ro, rl = oracle.cached_chunk_attn(dq(inp["q"], qs), dq(inp["k"], ks), dq(inp["v"], vs),
+                                      [dq(c[0], ks) for c in win], [dq(c[1], vs) for c in win], 1, q_len)
+    assert_close(f"o q_len={q_len} ({ns} key ranges)", to_f64(o), ro, FP8_MAX_ABS, FP8_MEAN_ABS)
+    assert_close("lse", to_f64(lse), rl, max_abs=2e-3, mean_abs=2e-4)

@@ -114,3 +114,25 @@ def test_paper_05b_training_d72(mw):
     for h in range(H):
         ro, rl = oracle.block_causal_attn_fwd_rows(qa, ka, va, L, 0, h, rows)
         assert_close(f"o rows h{h}", g["o"][0, h, rows], ro)
+
+
+def test_paper_05b_training_bench_shape(mw):
+    """The 0.5B training shape exactly as the benchmark times it (B1 H16 T19200 D72, 32 chunks of
+    600 tokens): heads 0 and 15 in full, every row of the output and of every gradient."""
+    import torch
+    B, H, T, D, L = 1, 16, 19200, 72, 600
+    print(f"[case] paper 0.5B training bench shape B{B} H{H} T{T} D{D} L{L}", flush=True)
+    bits = {n: synth.normal_bf16((B, H, T, D), 8200 + i) for i, n in enumerate(("q", "k", "v", "do"))}
+    q, k, v, do = (to_gpu(bits[n]) for n in ("q", "k", "v", "do"))
+    o, lse = mw.mw_block_causal_attn_fwd(q, k, v, L)
+    dq, dk, dv = mw.mw_block_causal_attn_bwd(q, k, v, o, do, lse, L)
+    torch.cuda.synchronize()
+    for h in (0, 15):
+        sel = lambda x: x[:, h:h + 1]
+        qf, kf, vf, dof = (f64(sel(bits[n])) for n in ("q", "k", "v", "do"))
+        ro, rl = oracle.block_causal_attn_fwd(qf, kf, vf, L, row_block=600)
+        assert_close(f"o h{h}", to_f64(o[:, h:h + 1]), ro)
+        assert_close(f"lse h{h}", to_f64(lse[:, h:h + 1]), rl, max_abs=2e-3, mean_abs=2e-4)
+        rdq, rdk, rdv = oracle.block_causal_attn_bwd(qf, kf, vf, dof, L, row_block=600)
+        for name, got, ref in (("dq", dq, rdq), ("dk", dk, rdk), ("dv", dv, rdv)):
+            assert_close(f"{name} h{h}", to_f64(got[:, h:h + 1]), ref)

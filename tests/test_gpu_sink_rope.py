@@ -150,3 +150,50 @@ def test_rollout_reshift_preserves_relative_positions(mw):
                                                                    off, cnt),
                                          sink_v=f64(raw_sink[1]))
         assert_close(f"step {t} (shift {shift_total})", to_f64(o), ro)
+
+
+def test_rope_reshift_drift_over_cache_life(mw):
+    """A key's whole life in the paper's largest cache (24 chunks): it is re-shifted once per
+    eviction, so up to 24 times, and each in-place shift rounds it to bf16 again.  Every key
+    after 24 shifts of 3 positions is compared with one fp64 rotation of the committed key by
+    the summed 72 positions.  Bound: each shift adds a rounding error of at most u = 2^-8
+    (bf16's unit roundoff) relative to each rotated element, and a rotation keeps the norm of a
+    pair, so after n shifts a pair's error is at most n * sqrt(2) * u * (1 + n u) times its norm
+    (plus fp32 rotation error, far smaller).  The drift must also leave the attention of two
+    queued chunks over the drifted window within the parity bar of the exact rotation."""
+    B, H, L, D, W, n, step = 1, 2, 128, 128, 24, 24, 3
+    off, cnt = band(D)
+    print(f"[case] rope drift: {n} shifts of {step} over a {W}-chunk window, D={D}", flush=True)
+    cache = mw.KVCache(W + 1, B, H, L, D)
+    chunks = _history(B, H, L, D, W, 2800)
+    for kc, vc in chunks:
+        mw.mw_kvcache_append(cache, to_gpu(kc), to_gpu(vc))
+    for _ in range(n):
+        mw.mw_kvcache_rope_shift(cache, step, off, cnt)
+    sync()
+    u = 2.0 ** -8
+    worst_ratio, errs = 0.0, []
+    exact = []
+    for c in range(W):
+        k0 = f64(chunks[c][0])
+        ref = oracle.rope_rotate(k0, -float(n * step), off, cnt)
+        exact.append(ref)
+        got = to_f64(cache.k_slots[cache.slot_of(c)])
+        assert np.array_equal(got[..., off + cnt:], k0[..., off + cnt:])  # outside the band: never touched
+        e = np.abs(got - ref)[..., off:off + cnt]
+        pair_norm = np.sqrt(k0[..., off:off + cnt:2] ** 2 + k0[..., off + 1:off + cnt:2] ** 2)
+        bound = n * np.sqrt(2.0) * u * (1.0 + n * u) * np.repeat(pair_norm, 2, axis=-1) + 1e-6
+        worst_ratio = max(worst_ratio, float((e / bound).max()))
+        errs.append(e)
+    e = np.concatenate([x.ravel() for x in errs])
+    print(f"[drift] after {n} shifts: max_abs={e.max():.3e} mean_abs={e.mean():.3e} rms={np.sqrt((e ** 2).mean()):.3e} "
+          f"worst fraction of the bound={worst_ratio:.3f}", flush=True)
+    assert worst_ratio <= 1.0
+    # attention over the drifted window vs the exact single rotation
+    nq = 2
+    inp = {x: synth.normal_bf16((B, H, nq * L, D), 2990 + i) for i, x in enumerate("qkv")}
+    o, _ = mw.mw_chunk_attn_cached(to_gpu(inp["q"]), to_gpu(inp["k"]), to_gpu(inp["v"]), nq, L, cache, window=W)
+    sync()
+    ro, _ = oracle.cached_chunk_attn(f64(inp["q"]), f64(inp["k"]), f64(inp["v"]), exact,
+                                     [f64(cv) for _, cv in chunks], nq, L)
+    assert_close("attention over the drifted window", to_f64(o), ro)
