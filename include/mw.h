@@ -139,6 +139,25 @@ int mw_block_causal_attn_bwd_strided(const void* q, const void* k, const void* v
                                      int B, int H, int T, int D, int chunk_len, float scale,
                                      mw_stream_t stream);
 
+/* The backward above (contiguous tensors) with no workspace argument, for
+ * callers that cannot allocate device memory: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation.  The row terms
+ * (8 bytes per row) live in a 32 MiB device array inside the library, one
+ * copy per GPU, held until the process ends; so B * H * T must not exceed
+ * 4,194,304 (MW_EUNSUPPORTED beyond).  The call allocates and frees nothing.
+ * Every call on a GPU shares that GPU's array: calls that overlap on one GPU
+ * (other streams, other host threads) race, and the caller must serialise
+ * them.  Nothing has to be cleared between calls: every row term is written
+ * before it is read.  The calling thread's current device must be the device
+ * of the stream and of the tensors.  Arguments, layout, arithmetic and result
+ * as mw_block_causal_attn_bwd.
+ * Errors: as mw_block_causal_attn_bwd, plus MW_EUNSUPPORTED above the row
+ * limit and MW_EHIP if the array's device address cannot be obtained. */
+int mw_block_causal_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o,
+                                     const void* d_o, const float* lse, void* dq, void* dk, void* dv,
+                                     int B, int H, int T, int D, int chunk_len, float scale,
+                                     mw_stream_t stream);
+
 /* ------------------------------------------------------------------------
  * Rolling KV cache (Sec. 3.5, "Structured Rolling KV Cache").
  *

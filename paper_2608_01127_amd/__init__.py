@@ -24,6 +24,7 @@ from ._lib import (  # noqa: F401
     MW_QUEUED_ISOLATED,
     load,
     mw_block_causal_attn_bwd,
+    mw_block_causal_attn_bwd_noalloc,
     mw_block_causal_attn_bwd_workspace_size,
     mw_block_causal_attn_fwd,
     mw_chunk_attn_cached,

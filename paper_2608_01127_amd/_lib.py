@@ -89,6 +89,7 @@ SIGNATURES = {
     "mw_chunk_attn_cached": ([_vp, _vp, _vp, _i, _i, _cache_p, _i, _i, _vp, _vp, _f, _vp, _sz, _vp], _i),
     "mw_block_causal_attn_fwd_strided": ([_vp, _vp, _vp, _vp, _vp, _str_p, _i, _i, _i, _i, _i, _f, _vp], _i),
     "mw_block_causal_attn_bwd_strided": ([_vp] * 9 + [_vp, _sz, _str_p, _i, _i, _i, _i, _i, _f, _vp], _i),
+    "mw_block_causal_attn_bwd_noalloc": ([_vp] * 9 + [_i, _i, _i, _i, _i, _f, _vp], _i),
     "mw_kvcache_append_strided": ([_cache_p, _vp, _vp, _str_p, _vp], _i),
     "mw_chunk_attn_cached_strided": ([_vp, _vp, _vp, _i, _i, _cache_p, _i, _i, _vp, _vp, _f, _vp, _sz, _str_p,
                                       _vp], _i),
@@ -255,6 +256,29 @@ def mw_block_causal_attn_bwd(q, k, v, o, d_o, lse, chunk_len: int, scale=None, w
                                                    _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), nbytes,
                                                    _strides(q, k, v, o, d_o, dq, dk, dv), B, H, T, D,
                                                    int(chunk_len), scale, _stream_handle(dev)))
+    return dq, dk, dv
+
+
+def mw_block_causal_attn_bwd_noalloc(q, k, v, o, d_o, lse, chunk_len: int, dq, dk, dv, scale=None):
+    """The backward without a workspace: its row terms live in the library's own per-GPU
+    scratch array, and neither the library nor this wrapper allocates anything, so dq, dk, dv
+    must be given.  Contiguous bf16 [B,H,T,D] tensors, lse fp32 [B,H,T]; B*H*T <= 4,194,304.
+    Calls that overlap on one GPU share the array and race.  Returns (dq, dk, dv)."""
+    torch = _torch()
+    for n, t in (("q", q), ("k", k), ("v", v), ("o", o), ("d_o", d_o), ("dq", dq), ("dk", dk), ("dv", dv)):
+        _bf16_4d(n, t)
+        if t.shape != q.shape:
+            raise ValueError(f"{n} must have the shape of q")
+    B, H, T, D = q.shape
+    dev = _same_device(q, k, v, o, d_o, lse, dq, dk, dv)
+    if lse is None:
+        raise ValueError("lse is required")
+    _check_lse(lse, (B, H, T), dev)
+    scale = 1.0 / math.sqrt(D) if scale is None else float(scale)
+    with torch.cuda.device(dev):  # the library takes the current device's copy of its array
+        _check(load().mw_block_causal_attn_bwd_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(d_o), _ptr(lse),
+                                                       _ptr(dq), _ptr(dk), _ptr(dv), B, H, T, D, int(chunk_len),
+                                                       scale, _stream_handle(dev)))
     return dq, dk, dv
 
 

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "mw.h"
@@ -228,6 +229,66 @@ int mw_block_causal_attn_bwd(const void* q, const void* k, const void* v, const 
                              int B, int H, int T, int D, int chunk_len, float scale, mw_stream_t stream) {
   return mw_block_causal_attn_bwd_strided(q, k, v, o, d_o, lse, dq, dk, dv, workspace, workspace_bytes, nullptr, B, H,
                                           T, D, chunk_len, scale, stream);
+}
+
+// ---------------------------------------------------------------------------
+// The backward without a caller workspace.  Its row terms (-Delta and the
+// base-2 LSE, 8 bytes per row) live in `scratch`, a fixed device array of this
+// library: every GPU the library runs on holds one copy of it for the life of
+// the process.  In host code the array's name stands for a host-side shadow,
+// so the device copy's address is asked of the runtime once per device and
+// only that address is ever handed to kernels.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr size_t kScratchBytes = size_t(32) << 20;  // 2 x 16 MiB: up to 4,194,304 rows (B * H * T)
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's copy of `scratch` (looked up on the
+// first call on that device, with the device current).
+int scratch_address(const char* fn, void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(MW_EHIP, "%s: hipGetDevice failed: %s", fn, hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(MW_EUNSUPPORTED, "%s: device %d is beyond %d", fn, dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(MW_EHIP, "%s: no device address for the scratch array on device %d: %s", fn, dev,
+                  hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MW_OK;
+}
+
+}  // namespace
+
+int mw_block_causal_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o, const void* d_o,
+                                     const float* lse, void* dq, void* dk, void* dv, int B, int H, int T, int D,
+                                     int chunk_len, float scale, mw_stream_t stream) {
+  const char* fn = "mw_block_causal_attn_bwd_noalloc";
+  int st = check_ptrs(fn, {{"q", q}, {"k", k}, {"v", v}, {"o", o}, {"d_o", d_o}, {"lse", lse}, {"dq", dq},
+                           {"dk", dk}, {"dv", dv}});
+  if (st) return st;
+  st = check_train_dims(fn, B, H, T, D, chunk_len, scale);
+  if (st) return st;
+  const size_t need = mw_block_causal_attn_bwd_workspace_size(B, H, T, D);
+  if (need > kScratchBytes)
+    return fail(MW_EUNSUPPORTED, "%s: B*H*T = %lld rows need %zu bytes of row terms, beyond the library's %zu-byte "
+                "scratch array (at most %zu rows)", fn, (long long)B * H * T, need, kScratchBytes,
+                kScratchBytes / (2 * sizeof(float)));
+  void* ws = nullptr;
+  st = scratch_address(fn, &ws);
+  if (st) return st;
+  return mw_block_causal_attn_bwd_strided(q, k, v, o, d_o, lse, dq, dk, dv, ws, kScratchBytes, nullptr, B, H, T, D,
+                                          chunk_len, scale, stream);
 }
 
 int mw_kvcache_init(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, int H, int L, int D) {
