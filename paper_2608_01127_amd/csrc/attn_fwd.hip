@@ -501,18 +501,12 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   const long long orow = (bh / H) * so.b + (bh % H) * so.h + t * so.t;
   const int c = (int)(gid % TPR) * 4;
   const float* ml = part + (long long)NS * rows * D;
-  // splits are read in groups of G so that G loads are in flight at once
-  constexpr int G = 8;
-  float M = -INFINITY;
-  for (int s0 = 0; s0 < NS; s0 += G) {
-    float mv[G];
-#pragma unroll
-    for (int g = 0; g < G; ++g) mv[g] = s0 + g < NS ? ml[2 * ((long long)(s0 + g) * rows + row)] : -INFINITY;
-#pragma unroll
-    for (int g = 0; g < G; ++g) M = fmaxf(M, mv[g]);
-  }
+  // One pass over the splits, G at a time with all their loads in flight (one
+  // round trip for up to G splits): a running reference M, rescaled when a
+  // group raises it, as in the attention kernel itself.
+  constexpr int G = 16;
+  float M = -INFINITY, L = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  float L = 0.f;
   for (int s0 = 0; s0 < NS; s0 += G) {
     float mv[G], lv[G];
     f32x4 v[G];
@@ -524,13 +518,22 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
       lv[g] = in ? ml[2 * r + 1] : 0.f;
       v[g] = in ? *reinterpret_cast<const f32x4*>(part + r * D + c) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
+    float Mn = M;
+#pragma unroll
+    for (int g = 0; g < G; ++g) Mn = fmaxf(Mn, mv[g]);
+    if (Mn == -INFINITY) continue;  // no keys in these splits (or so far)
+    const float a = (M == -INFINITY) ? 0.f : fast_exp2(M - Mn);
+    L *= a;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] *= a;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const float w = (mv[g] == -INFINITY) ? 0.f : fast_exp2(mv[g] - M);  // empty split: no keys
+      const float w = (mv[g] == -INFINITY) ? 0.f : fast_exp2(mv[g] - Mn);  // empty split: no keys
       L = fmaf(w, lv[g], L);
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[j] = fmaf(w, v[g][j], acc[j]);
     }
+    M = Mn;
   }
   const float inv = 1.f / L;
   bf16x4 out;

@@ -370,3 +370,52 @@ def test_rollout_200_steps(mw):
             for c in win:
                 sl = cache.slot_of(c)
                 assert bits_equal(cache.k_slots[sl], to_gpu(committed[c][0]))
+
+
+def test_snapshot_restore_continue_bit_identical(mw):
+    """Checkpoint and resume of a rollout: after k steps the ring descriptor (KVCache.snapshot)
+    and the slot buffers are saved; the rollout continues n steps (commit, evict to the window,
+    cached attention, RoPE re-shift); then the saved state is restored and the same n steps run
+    again.  Every output, every slot and the ring counters match the first continuation
+    bit for bit; the slot numbering agrees with the ring model throughout."""
+    import torch
+    B, H, L, D, S, W, nq, k, n = 1, 2, 96, 128, 5, 3, 2, 7, 6
+    cache = mw.KVCache(S, B, H, L, D)
+    ring = oracle.RingModel(S)
+
+    def step(t):
+        kc, vc = (to_gpu(synth.normal_bf16((B, H, L, D), 3000 + 2 * t + j)) for j in range(2))
+        slot = mw.mw_kvcache_append(cache, kc, vc)
+        if cache.live > W:
+            mw.mw_kvcache_evict(cache, cache.live - W)
+            mw.mw_kvcache_rope_shift(cache, 2, 0, 44)
+        q, kn, vn = (to_gpu(synth.normal_bf16((B, H, nq * L, D), 3500 + 3 * t + j)) for j in range(3))
+        o, lse = mw.mw_chunk_attn_cached(q, kn, vn, nq, L, cache, window=cache.live, want_lse=True)
+        return slot, o, lse
+
+    for t in range(k):
+        slot, _, _ = step(t)
+        assert slot == ring.append()
+        if ring.live > W:
+            ring.evict(ring.live - W)
+    snap = cache.snapshot()
+    saved_k, saved_v = cache.k_slots.clone(), cache.v_slots.clone()
+    first = []
+    for t in range(k, k + n):
+        first.append(step(t))
+    sync()
+    end_state = (cache.snapshot(), cache.k_slots.clone(), cache.v_slots.clone())
+    # restore and run the same steps again
+    cache.restore(snap)
+    cache.k_slots.copy_(saved_k)
+    cache.v_slots.copy_(saved_v)
+    for i, t in enumerate(range(k, k + n)):
+        slot, o, lse = step(t)
+        assert slot == first[i][0] == ring.append()
+        if ring.live > W:
+            ring.evict(ring.live - W)
+        assert bits_equal(o, first[i][1]), f"output of step {t} differs after restore"
+        assert torch.equal(lse, first[i][2])
+    sync()
+    assert cache.snapshot() == end_state[0]
+    assert bits_equal(cache.k_slots, end_state[1]) and bits_equal(cache.v_slots, end_state[2])
