@@ -307,7 +307,9 @@ def fp8_stream(mw, torch, dev, st, reps=10):
     """The e4m3 inference variant on the streaming shape (B1 H16 D128, 4 in-flight
     chunks of 2640 tokens over a 6-chunk window of an 8-slot ring): per step,
     quantize the queued chunks' Q, K, V (bf16 -> e4m3), commit one chunk
-    (quantize-on-commit), evict to the window, and run the e4m3 cached attention.
+    (quantize-on-commit), evict to the window, re-shift the retained keys by the
+    evicted chunk's 3 positions (recorded; the keys are rotated when the call
+    loads the window), and run the e4m3 cached attention.
     Also the cache-bound decode shapes (one queued chunk of 64 / 128 / 256 tokens
     over the full window, Infinity Cache flushed before each call; algorithmic
     bytes = e4m3 window K and V + e4m3 Q, K_new, V_new + bf16 O), and the paper's
@@ -342,7 +344,9 @@ def fp8_stream(mw, torch, dev, st, reps=10):
         e1 = ev()
         mw.mw_kvcache_append(cache, kc, vc)
         e2 = ev()
-        mw.mw_kvcache_evict(cache, cache.live - W)
+        n_ev = cache.live - W
+        mw.mw_kvcache_evict(cache, n_ev)
+        mw.mw_kvcache_rope_shift(cache, 3 * n_ev, 0, 44)
         e3 = ev()
         mw.mw_chunk_attn_cached_fp8(q8, k8, v8, nq, ql, cache, sc, window=W, out=o, workspace=ws)
         e4 = ev()
@@ -364,6 +368,7 @@ def fp8_stream(mw, torch, dev, st, reps=10):
     F = 4.0 * pairs_cached(B, H, W, L, nq, ql, causal=True) * D
     n_el = B * H * Tq * D
     out = {"workload": st.name + "_e4m3", "dtype": "e4m3 (fp32 accumulate)", "scale": sc,
+           "rope": "re-shift of 3 positions per step, rotated on load (inside the cached call)",
            "step_ms": round(step_ms, 4),
            "phases_ms": {k: round(v, 4) for k, v in ph.items()},
            "cached_tflops": round(F / (ph["cached"] * 1e-3) / 1e12, 2),
@@ -371,7 +376,10 @@ def fp8_stream(mw, torch, dev, st, reps=10):
            "step_tflops": round(F / (step_ms * 1e-3) / 1e12, 2),
            "quantize_qkv_gbs": round(3 * n_el * 3 / (ph["quantize_qkv"] * 1e-3) / 1e9, 1),
            "append_gbs": round(2 * B * H * L * D * 3 / (ph["append"] * 1e-3) / 1e9, 1)}
-    # decode shapes
+    # decode shapes, on a cache of the same window with no shift pending (pure streaming of the window)
+    cache = mw.KVCache(st.slots, B, H, L, D, device=dev, fp8=True, k_scale=sc, v_scale=sc)
+    for _ in range(W):
+        mw.mw_kvcache_append(cache, kc, vc)
     flush = torch.ones(128 << 20, dtype=torch.float32, device=dev)
     dec = []
     for dq in (64, 128, 256):

@@ -72,6 +72,8 @@ typedef struct {
 /* Largest supported window (committed chunks attended to) and queued-chunk count. */
 #define MW_MAX_WINDOW 64
 #define MW_MAX_QUEUED 64
+/* Largest ring of an e4m3 cache (its per-slot re-shift record, below). */
+#define MW_MAX_SLOTS 128
 
 /* ------------------------------------------------------------------------
  * Training: block-causal attention (Sec. 3.2).
@@ -182,6 +184,15 @@ typedef struct {
   int elem_bytes;      /* 2: bf16 slots (mw_kvcache_init); 1: e4m3 slots (mw_kvcache_init_fp8) */
   float k_scale;       /* e4m3 slots: key value = code * k_scale (1 for bf16 slots) */
   float v_scale;       /* e4m3 slots: value value = code * v_scale (1 for bf16 slots) */
+  /* RoPE re-shift record of e4m3 slots, whose keys are rotated when a call
+   * loads them instead of in place (see mw_kvcache_rope_shift); all zero for
+   * bf16 slots. */
+  int64_t rope_total;  /* sum of the shifts applied so far */
+  int rope_offset;     /* band of those shifts: dim_offset, dim_count and theta of the */
+  int rope_count;      /* first one (later shifts must use the same band) */
+  float rope_theta;
+  int rope_set;        /* 1 once a band is recorded */
+  int64_t rope_at_commit[MW_MAX_SLOTS]; /* rope_total when the chunk in each slot was committed */
 } mw_kvcache;
 
 /* Initialise an empty ring over k_slots/v_slots (bf16 [S,B,H,L,D]), without a
@@ -209,17 +220,28 @@ typedef struct {
 } mw_rope;
 
 /* RoPE re-shifting (Sec. 3.5): rotate the keys of every live committed chunk
- * (not the sink) by -shift positions on the rope band, in place, so the
- * retained window is re-indexed from the start after `shift` positions of
- * history were evicted (shift = evicted chunks x positions per chunk).
- * Relative positions inside the window are unchanged; values are untouched.
- * Arithmetic: bf16 in, fp32 rotation (cos/sin computed on the host in double),
- * bf16 out (nearest even).  shift = 0 or no live chunk: no device work.
- * Errors: MW_EINVAL (null cache or rope, invalid band, theta <= 0), MW_EHIP. */
+ * (not the sink) by -shift positions on the rope band, so the retained window
+ * is re-indexed from the start after `shift` positions of history were evicted
+ * (shift = evicted chunks x positions per chunk).  Relative positions inside
+ * the window are unchanged; values are untouched.
+ * bf16 slots are rotated in place (the paper's first option): bf16 in, fp32
+ * rotation (cos/sin computed on the host in double), bf16 out (nearest even);
+ * shift = 0 or no live chunk: no device work.
+ * e4m3 slots are rotated on load (the paper's second option), since rotating
+ * 8-bit keys in place would re-round them at every shift: this call only adds
+ * shift to c->rope_total (host only, no device work); a chunk's keys are kept
+ * as committed, and mw_chunk_attn_cached_fp8 rotates each window chunk by
+ * -(rope_total - its rope_at_commit) positions when it loads the window (one
+ * rounding to e4m3 per call, none accumulated over shifts).  The band and
+ * theta of an e4m3 cache's first shift are recorded; later shifts must use the
+ * same ones.
+ * Errors: MW_EINVAL (null cache or rope, invalid band, theta <= 0, a band or
+ * theta other than the recorded one of an e4m3 cache), MW_EHIP. */
 int mw_kvcache_rope_shift(mw_kvcache* c, int shift, const mw_rope* rope, mw_stream_t stream);
 
 /* Commit one chunk: enqueue a copy of k_chunk and v_chunk (bf16 [B,H,L,D]) into
- * slot head mod S, then head += 1 (host state changes at call time).
+ * slot head mod S, then head += 1 (host state changes at call time).  An e4m3
+ * cache also records rope_at_commit[slot] = rope_total.
  * Errors: MW_EINVAL, MW_EALIGN, MW_EFULL (head - tail == S), MW_EHIP. */
 int mw_kvcache_append(mw_kvcache* c, const void* k_chunk, const void* v_chunk, mw_stream_t stream);
 
@@ -277,7 +299,10 @@ enum { MW_QUEUED_CAUSAL = 0, MW_QUEUED_ISOLATED = 1 };
 
 /* Workspace bytes that let mw_chunk_attn_cached use its preferred split plan
  * for this shape under either visibility rule (0 when neither would split).
- * Negative window: all live. */
+ * For an e4m3 cache, also the rotated window keys of mw_chunk_attn_cached_fp8's
+ * rotation on load (window * B * H * L * 128 bytes, rounded up to 256), needed
+ * only while shifts are pending but always included.  Negative window: all
+ * live. */
 size_t mw_chunk_attn_cached_workspace_size(const mw_kvcache* c, int n_queued, int q_len, int window);
 
 /* The key-range split plan that mw_chunk_attn_cached (mw_chunk_attn_cached_fp8
@@ -338,13 +363,12 @@ int mw_quantize_fp8(const void* x, const mw_strides* x_strides, void* y, int B, 
  * mw_kvcache_append_strided take bf16 chunks and quantize them into the slot
  * with these scales (mw_quantize_fp8's rounding).  The sink
  * (mw_kvcache_set_sink) must be e4m3 [B, H, sink_len, D] quantized with the
- * same scales.  mw_kvcache_rope_shift is not available for e4m3 slots
- * (MW_EUNSUPPORTED): rotating 8-bit keys in place would re-round them at every
- * shift.  mw_chunk_attn_cached rejects an e4m3 cache (MW_EINVAL); use
+ * same scales.  mw_kvcache_rope_shift records shifts for rotation on load
+ * (see there).  mw_chunk_attn_cached rejects an e4m3 cache (MW_EINVAL); use
  * mw_chunk_attn_cached_fp8.  Eviction, live counts and slot numbering are
  * those of the bf16 ring.  No device work.
  * Errors: MW_EINVAL (null, sizes < 1, bad scales), MW_EALIGN,
- * MW_EUNSUPPORTED (D other than 128). */
+ * MW_EUNSUPPORTED (D other than 128, S > MW_MAX_SLOTS). */
 int mw_kvcache_init_fp8(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, int H, int L, int D,
                         float k_scale, float v_scale);
 
@@ -359,8 +383,18 @@ int mw_kvcache_init_fp8(mw_kvcache* c, void* k_slots, void* v_slots, int S, int 
  * sum_j p_j v8_j * v_scale / sum_j p_j.  window, flags, workspace (size from
  * mw_chunk_attn_cached_workspace_size on the e4m3 cache) as in
  * mw_chunk_attn_cached.
- * Errors: as mw_chunk_attn_cached, plus MW_EINVAL for a bf16 cache or
- * q_scale not finite and > 0. */
+ * Rotation on load: when a window chunk has shifts pending (rope_total !=
+ * its rope_at_commit), the call first writes every window chunk's keys,
+ * rotated by -(rope_total - rope_at_commit[slot]) positions on the recorded
+ * band, to the start of the workspace: each pair is decoded, rotated in fp32
+ * (cos/sin of the angle computed in double), clamped to +-448 and rounded to
+ * e4m3 (nearest even); the attention then reads the window keys from there
+ * (the slots are not modified).  This needs window * B * H * L * 128 bytes of
+ * workspace (rounded up to 256) before the key-range partials;
+ * mw_chunk_attn_cached_workspace_size of an e4m3 cache always includes them.
+ * Errors: as mw_chunk_attn_cached, plus MW_EINVAL for a bf16 cache, q_scale
+ * not finite and > 0, or shifts pending with a workspace too small for the
+ * rotated window keys. */
 int mw_chunk_attn_cached_fp8(const void* q8, const void* k8_new, const void* v8_new, int n_queued, int q_len,
                              const mw_kvcache* c, int window, int flags, void* o, float* lse, float scale,
                              float q_scale, void* workspace, size_t workspace_bytes, const mw_strides* o_strides,

@@ -18,6 +18,7 @@ from ._lib import (  # noqa: F401
     MW_EINVAL,
     MW_EUNSUPPORTED,
     MW_MAX_QUEUED,
+    MW_MAX_SLOTS,
     MW_MAX_WINDOW,
     MW_OK,
     MW_QUEUED_CAUSAL,

@@ -25,6 +25,7 @@ MW_QUEUED_CAUSAL = 0
 MW_QUEUED_ISOLATED = 1
 MW_MAX_WINDOW = 64
 MW_MAX_QUEUED = 64
+MW_MAX_SLOTS = 128
 
 STATUS_NAMES = {0: "MW_OK", -1: "MW_EINVAL", -2: "MW_EUNSUPPORTED", -3: "MW_EALIGN", -4: "MW_EFULL",
                 -5: "MW_EEMPTY", -6: "MW_EHIP"}
@@ -41,7 +42,10 @@ class mw_kvcache(ctypes.Structure):
                 ("S", ctypes.c_int), ("B", ctypes.c_int), ("H", ctypes.c_int), ("L", ctypes.c_int),
                 ("D", ctypes.c_int), ("head", ctypes.c_int64), ("tail", ctypes.c_int64),
                 ("k_sink", ctypes.c_void_p), ("v_sink", ctypes.c_void_p), ("sink_len", ctypes.c_int),
-                ("elem_bytes", ctypes.c_int), ("k_scale", ctypes.c_float), ("v_scale", ctypes.c_float)]
+                ("elem_bytes", ctypes.c_int), ("k_scale", ctypes.c_float), ("v_scale", ctypes.c_float),
+                ("rope_total", ctypes.c_int64), ("rope_offset", ctypes.c_int), ("rope_count", ctypes.c_int),
+                ("rope_theta", ctypes.c_float), ("rope_set", ctypes.c_int),
+                ("rope_at_commit", ctypes.c_int64 * MW_MAX_SLOTS)]
 
 
 class mw_rope(ctypes.Structure):
@@ -341,11 +345,13 @@ class KVCache:
         _check(load().mw_kvcache_set_sink(ctypes.byref(d), _ptr(k_sink), _ptr(v_sink), int(k_sink.shape[2])))
         self._sink = (k_sink, v_sink)  # keep the tensors alive while the cache points at them
 
-    def snapshot(self) -> tuple:
-        return (int(self.desc.head), int(self.desc.tail))
+    def snapshot(self) -> bytes:
+        """A copy of the whole descriptor (ring counters, sink, e4m3 re-shift record); the slot
+        buffers' contents are the caller's to save alongside."""
+        return bytes(self.desc)
 
-    def restore(self, snap) -> None:
-        self.desc.head, self.desc.tail = snap
+    def restore(self, snap: bytes) -> None:
+        ctypes.memmove(ctypes.byref(self.desc), snap, ctypes.sizeof(mw_kvcache))
 
 
 def mw_kvcache_append(cache: KVCache, k_chunk, v_chunk) -> int:
@@ -372,7 +378,8 @@ def mw_kvcache_set_sink(cache: KVCache, k_sink, v_sink) -> None:
 
 
 def mw_kvcache_rope_shift(cache: KVCache, shift: int, dim_offset: int, dim_count: int, theta: float = 10000.0) -> None:
-    """Rotate the keys of all live chunks by -shift positions on the rope band (in place)."""
+    """Rotate the keys of all live chunks by -shift positions on the rope band: in place for a
+    bf16 cache; recorded, and applied when a call loads the window, for an e4m3 cache."""
     rope = mw_rope(int(dim_offset), int(dim_count), float(theta))
     _check(load().mw_kvcache_rope_shift(ctypes.byref(cache.desc), int(shift), ctypes.byref(rope),
                                         _stream_handle(cache.k_slots.device)))

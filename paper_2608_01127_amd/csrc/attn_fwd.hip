@@ -488,7 +488,7 @@ struct FwdDecodeCfg {
 //   O = sum_s w_s O_s / sum_s w_s l_s,   LSE = (M + log2 sum_s w_s l_s) ln 2.
 // The split rows are rows [0, split_rows) of each head (rows = BH * split_rows).
 // One thread per 4 output columns of a row.
-template <int D>
+template <int D, int G>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part, uint16_t* __restrict__ o,
                                                            Strides so, int H, int Tq, int split_rows,
                                                            float* __restrict__ lse, int NS, long long rows) {
@@ -502,9 +502,9 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   const int c = (int)(gid % TPR) * 4;
   const float* ml = part + (long long)NS * rows * D;
   // One pass over the splits, G at a time with all their loads in flight (one
-  // round trip for up to G splits): a running reference M, rescaled when a
-  // group raises it, as in the attention kernel itself.
-  constexpr int G = 16;
+  // round trip for up to G splits; G is the smallest of 4, 8, 16 that covers
+  // the split count, or 16): a running reference M, rescaled when a group
+  // raises it, as in the attention kernel itself.
   float M = -INFINITY, L = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   for (int s0 = 0; s0 < NS; s0 += G) {
@@ -543,6 +543,25 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   if (lse != nullptr && c == 0) lse[bh * Tq + t] = (M + __log2f(L)) * 0.69314718055994530942f;
 }
 
+// The merge kernel for p's split rows, with its group size chosen by the split count.
+template <int D>
+static hipError_t launch_combine_d(const FwdParams& p, hipStream_t stream) {
+  const long long rows = (long long)p.BH * p.split_rows;
+  const long long threads = rows * (D / 4);
+  const dim3 grid((unsigned)((threads + 255) / 256));
+  if (p.n_splits <= 4) {
+    hipLaunchKernelGGL((attn_combine_kernel<D, 4>), grid, dim3(256), 0, stream, p.part, p.o, p.so, p.H, p.Tq,
+                       p.split_rows, p.lse, p.n_splits, rows);
+  } else if (p.n_splits <= 8) {
+    hipLaunchKernelGGL((attn_combine_kernel<D, 8>), grid, dim3(256), 0, stream, p.part, p.o, p.so, p.H, p.Tq,
+                       p.split_rows, p.lse, p.n_splits, rows);
+  } else {
+    hipLaunchKernelGGL((attn_combine_kernel<D, 16>), grid, dim3(256), 0, stream, p.part, p.o, p.so, p.H, p.Tq,
+                       p.split_rows, p.lse, p.n_splits, rows);
+  }
+  return hipGetLastError();
+}
+
 template <int D, bool CACHED, int NW, int BN, int RB, int KG>
 static hipError_t launch_fwd_tpl(FwdParams p, hipStream_t stream) {
   constexpr int BM = 32 * RB * (NW / KG);
@@ -550,11 +569,7 @@ static hipError_t launch_fwd_tpl(FwdParams p, hipStream_t stream) {
   hipLaunchKernelGGL((attn_fwd_kernel<D, CACHED, NW, BN, RB, KG>), dim3((unsigned)grid), dim3(64 * NW), 0, stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_splits == 1) return e;
-  const long long rows = (long long)p.BH * p.split_rows;
-  const long long threads = rows * (D / 4);
-  hipLaunchKernelGGL(attn_combine_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p.part,
-                     p.o, p.so, p.H, p.Tq, p.split_rows, p.lse, p.n_splits, rows);
-  return hipGetLastError();
+  return launch_combine_d<D>(p, stream);
 }
 
 template <int D, bool CACHED>
@@ -643,11 +658,7 @@ FwdChoice fwd_choice(int D, bool cached, int Tq) {
 
 hipError_t launch_combine(const FwdParams& p, int D, hipStream_t stream) {
   if (D != 128) return hipErrorInvalidValue;
-  const long long rows = (long long)p.BH * p.split_rows;
-  const long long threads = rows * (128 / 4);
-  hipLaunchKernelGGL(attn_combine_kernel<128>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p.part,
-                     p.o, p.so, p.H, p.Tq, p.split_rows, p.lse, p.n_splits, rows);
-  return hipGetLastError();
+  return launch_combine_d<128>(p, stream);
 }
 
 size_t fwd_split_bytes(int D, int BH, int split_rows, int n_splits) {

@@ -162,11 +162,15 @@ __device__ __forceinline__ void stage_kv8(const FwdParams& p, int bh, int k0, fp
     stage8_s<BN, NT>(Vt, qv + j * DH, ro, tid);
     return;
   }
+  // window keys rotated on load come from p.k_win (window order), values
+  // always from the slots
+  const fp8_t* kw = p.k_win;
   if (kw0 >= 0 && kl < p.wL && off0 + (kl - k0) < p.L) {  // one window chunk
     int slot = p.first_slot + w0;
     slot = slot >= p.S ? slot - p.S : slot;
-    const long long e = (long long)slot * p.slot_stride + ((long long)bh * p.L + off0) * DH;
-    stage8_s<BN, NT>(Kt, ks + e, ro, tid);
+    const long long in_chunk = ((long long)bh * p.L + off0) * DH;
+    const long long e = (long long)slot * p.slot_stride + in_chunk;
+    stage8_s<BN, NT>(Kt, kw != nullptr ? kw + (long long)w0 * p.slot_stride + in_chunk : ks + e, ro, tid);
     stage8_s<BN, NT>(Vt, vs + e, ro, tid);
     return;
   }
@@ -184,8 +188,9 @@ __device__ __forceinline__ void stage_kv8(const FwdParams& p, int bh, int k0, fp
       }
       int slot = p.first_slot + w;
       slot = slot >= p.S ? slot - p.S : slot;
-      const long long e = (long long)slot * p.slot_stride + ((long long)bh * p.L + off) * DH;
-      return {ks + e, vs + e};
+      const long long in_chunk = ((long long)bh * p.L + off) * DH;
+      const long long e = (long long)slot * p.slot_stride + in_chunk;
+      return {kw != nullptr ? kw + (long long)w * p.slot_stride + in_chunk : ks + e, vs + e};
     }
     const long long j = key - p.wL;
     return {qk + j * DH, qv + j * DH};
@@ -437,6 +442,69 @@ __global__ __launch_bounds__(256) void quantize_fp8_kernel(QuantJobs jobs, int H
   *reinterpret_cast<u32x2*>(jb.y + row * D + c) = out;
 }
 
+// Rotation on load of e4m3 window keys (paper Sec. 3.5, re-indexing the
+// retained window after an eviction, done when the keys are used rather than
+// in place): window chunk blockIdx.y (in window order) is copied from its slot
+// to k_win with its rope band rotated by -pend[w] positions.  One thread per
+// 128-byte key row; each band pair is decoded, rotated in fp32 with the cos/sin
+// of its angle, clamped to +-448 and rounded back to e4m3 (nearest even, the
+// quantizer's rounding).  The scale cancels: a rotation is linear, so codes
+// are rotated as values.  The cos/sin of pair i are computed once per block,
+// in double, as the rotation of one position (cos, sin of its frequency, from
+// the host) raised to the power -pend[w] by repeated squaring: no device
+// trigonometry, and a relative error of a few 1e-15 for any pend.
+__global__ __launch_bounds__(256) void rope_load_fp8_kernel(const fp8_t* __restrict__ k_slots, fp8_t* __restrict__ k_win,
+                                                            long long slot_bytes, int S, int first_slot,
+                                                            long long pieces, int dim_offset, int n_pairs,
+                                                            RopeLoadArgs a) {
+  __shared__ float cs[2][64];
+  const int w = blockIdx.y;
+  if ((int)threadIdx.x < n_pairs) {
+    // (cos, sin) of -pend * freq = (c1 - i s1)^pend
+    long long n = a.pend[w];
+    double br = a.c1[threadIdx.x], bi = n >= 0 ? -a.s1[threadIdx.x] : a.s1[threadIdx.x];
+    n = n >= 0 ? n : -n;
+    double cr = 1.0, ci = 0.0;
+    while (n != 0) {  // at most 63 rounds
+      if (n & 1) {
+        const double t = cr * br - ci * bi;
+        ci = cr * bi + ci * br;
+        cr = t;
+      }
+      const double t = br * br - bi * bi;
+      bi = 2.0 * br * bi;
+      br = t;
+      n >>= 1;
+    }
+    cs[0][threadIdx.x] = (float)cr;
+    cs[1][threadIdx.x] = (float)ci;
+  }
+  __syncthreads();
+  // one thread per 16-byte piece (8 pairs) of a key row
+  const long long j = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= pieces) return;
+  const int slot = first_slot + w < S ? first_slot + w : first_slot + w - S;
+  u32x4 v = *reinterpret_cast<const u32x4*>(k_slots + (long long)slot * slot_bytes + j * 16);
+  const int pc = (int)(j % (DH / 16));  // piece of the row: pairs 8 pc .. 8 pc + 7
+  const int p0 = dim_offset / 2;         // first pair of the band (dim_offset is even)
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int pr = 8 * pc + q - p0;  // band pair index of this byte pair
+    if (pr < 0 || pr >= n_pairs) continue;
+    unsigned u = v[q / 2];
+    // (the byte and half selectors of the conversions are immediates)
+    const float x0 = (q % 2) ? __builtin_amdgcn_cvt_f32_fp8(u, 2) : __builtin_amdgcn_cvt_f32_fp8(u, 0);
+    const float x1 = (q % 2) ? __builtin_amdgcn_cvt_f32_fp8(u, 3) : __builtin_amdgcn_cvt_f32_fp8(u, 1);
+    const float c = cs[0][pr], sn = cs[1][pr];
+    const float y0 = fminf(fmaxf(fmaf(x0, c, -x1 * sn), -kE4m3Max), kE4m3Max);
+    const float y1 = fminf(fmaxf(fmaf(x0, sn, x1 * c), -kE4m3Max), kE4m3Max);
+    u = (q % 2) ? (unsigned)__builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, (int)u, true)
+                : (unsigned)__builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, (int)u, false);
+    v[q / 2] = u;
+  }
+  *reinterpret_cast<u32x4*>(k_win + (long long)w * slot_bytes + j * 16) = v;
+}
+
 // Tile configuration: 8 waves of one 32-row block (256 queries; one workgroup
 // per CU), 128 keys per step.  Measured on the streaming shapes: 128 keys per
 // step 12-15% faster than 64; two row blocks per wave (4 waves, one per SIMD)
@@ -487,6 +555,18 @@ hipError_t launch_fwd_fp8(FwdParams p, hipStream_t stream) {
   if (bm == 64) return launch_fp8_tpl<2, Fwd8FewRows<2>::RB, Fwd8FewRows<2>::BN>(p, stream);
   if (bm == 128) return launch_fp8_tpl<4, Fwd8FewRows<4>::RB, Fwd8FewRows<4>::BN>(p, stream);
   return launch_fp8_tpl<Fwd8Cfg::NW, Fwd8Cfg::RB, Fwd8Cfg::BN>(p, stream);
+}
+
+hipError_t launch_rope_load_fp8(const uint8_t* k_slots, uint8_t* k_win, long long slot_bytes, int S, int first_slot,
+                                int n_window, long long rows_per_slot, int dim_offset, int n_pairs,
+                                const RopeLoadArgs& args, hipStream_t stream) {
+  const long long pieces = rows_per_slot * (DH / 16);
+  if (n_window < 1 || pieces < 1) return hipSuccess;
+  if (n_window > 64 || n_pairs < 1 || n_pairs > 64 || pieces > 0x7fffffffLL * 255LL)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rope_load_fp8_kernel, dim3((unsigned)((pieces + 255) / 256), (unsigned)n_window), dim3(256), 0,
+                     stream, k_slots, k_win, slot_bytes, S, first_slot, pieces, dim_offset, n_pairs, args);
+  return hipGetLastError();
 }
 
 hipError_t launch_quantize_fp8(const QuantJobs& jobs, int n_jobs, int B, int H, int T, int D, hipStream_t stream) {

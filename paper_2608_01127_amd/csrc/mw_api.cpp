@@ -316,6 +316,12 @@ int mw_kvcache_init(mw_kvcache* c, void* k_slots, void* v_slots, int S, int B, i
   c->elem_bytes = 2;
   c->k_scale = 1.f;
   c->v_scale = 1.f;
+  c->rope_total = 0;
+  c->rope_offset = 0;
+  c->rope_count = 0;
+  c->rope_theta = 0.f;
+  c->rope_set = 0;
+  for (int i = 0; i < MW_MAX_SLOTS; ++i) c->rope_at_commit[i] = 0;
   return ok();
 }
 
@@ -328,6 +334,7 @@ int mw_kvcache_init_fp8(mw_kvcache* c, void* k_slots, void* v_slots, int S, int 
   if (D != 128) return fail(MW_EUNSUPPORTED, "%s: head dimension %d is not supported (128)", fn, D);
   if (!good_scale(k_scale) || !good_scale(v_scale))
     return fail(MW_EINVAL, "%s: k_scale and v_scale must be finite and > 0", fn);
+  if (S > MW_MAX_SLOTS) return fail(MW_EUNSUPPORTED, "%s: S = %d exceeds %d slots", fn, S, MW_MAX_SLOTS);
   mw_kvcache t;
   const int st = mw_kvcache_init(&t, k_slots, v_slots, S, B, H, L, D);
   if (st) return fail(st, "%s: %s", fn, mw_last_error());
@@ -344,8 +351,20 @@ static int check_cache(const char* fn, const mw_kvcache* c) {
       (c->D != 64 && c->D != 72 && c->D != 128) || c->tail < 0 || c->head < c->tail || c->head - c->tail > c->S ||
       c->sink_len < 0 || (c->sink_len > 0 && (c->k_sink == nullptr || c->v_sink == nullptr)) ||
       (c->elem_bytes != 1 && c->elem_bytes != 2) ||
-      (c->elem_bytes == 1 && (c->D != 128 || !good_scale(c->k_scale) || !good_scale(c->v_scale))))
+      (c->elem_bytes == 1 && (c->D != 128 || !good_scale(c->k_scale) || !good_scale(c->v_scale) ||
+                              c->S > MW_MAX_SLOTS)) ||
+      (c->rope_set != 0 && c->rope_set != 1))
     return fail(MW_EINVAL, "%s: cache descriptor is not initialised or is corrupt", fn);
+  return MW_OK;
+}
+
+// A RoPE band of `D` head dims: even offset, even count of 2..128 dims, inside D.
+static int check_band(const char* fn, const mw_rope* rope, int D) {
+  if (rope->dim_offset < 0 || rope->dim_offset % 2 || rope->dim_count < 2 || rope->dim_count % 2 ||
+      rope->dim_count > 128 || rope->dim_offset + rope->dim_count > D)
+    return fail(MW_EINVAL, "%s: rope band [%d, %d) is not a valid even band of the %d head dims", fn, rope->dim_offset,
+                rope->dim_offset + rope->dim_count, D);
+  if (!(rope->theta > 0.f) || !std::isfinite(rope->theta)) return fail(MW_EINVAL, "%s: theta must be > 0", fn);
   return MW_OK;
 }
 
@@ -374,6 +393,7 @@ int mw_kvcache_append_strided(mw_kvcache* c, const void* k_chunk, const void* v_
                  static_cast<uint8_t*>(c->v_slots) + (long long)slot * n, 1.f / c->v_scale};
     hipError_t e = mw::launch_quantize_fp8(jobs, 2, c->B, c->H, c->L, c->D, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_status(fn, e);
+    c->rope_at_commit[slot] = c->rope_total;  // shifts from here on are pending for this chunk
     c->head += 1;
     return ok();
   }
@@ -422,13 +442,22 @@ int mw_kvcache_rope_shift(mw_kvcache* c, int shift, const mw_rope* rope, mw_stre
   int st = check_cache(fn, c);
   if (st) return st;
   if (rope == nullptr) return fail(MW_EINVAL, "%s: rope is NULL", fn);
-  if (c->elem_bytes == 1)
-    return fail(MW_EUNSUPPORTED, "%s: not available for e4m3 slots (an in-place rotation re-rounds them)", fn);
-  if (rope->dim_offset < 0 || rope->dim_offset % 2 || rope->dim_count < 2 || rope->dim_count % 2 ||
-      rope->dim_count > 128 || rope->dim_offset + rope->dim_count > c->D)
-    return fail(MW_EINVAL, "%s: rope band [%d, %d) is not a valid even band of the %d head dims", fn, rope->dim_offset,
-                rope->dim_offset + rope->dim_count, c->D);
-  if (!(rope->theta > 0.f) || !std::isfinite(rope->theta)) return fail(MW_EINVAL, "%s: theta must be > 0", fn);
+  st = check_band(fn, rope, c->D);
+  if (st) return st;
+  if (c->elem_bytes == 1) {
+    // e4m3 slots: rotation on load; record the shift (and the band of the first)
+    if (c->rope_set && (rope->dim_offset != c->rope_offset || rope->dim_count != c->rope_count ||
+                        rope->theta != c->rope_theta))
+      return fail(MW_EINVAL, "%s: the band of this e4m3 cache's shifts is [%d, %d) with theta %g; got [%d, %d), %g", fn,
+                  c->rope_offset, c->rope_offset + c->rope_count, (double)c->rope_theta, rope->dim_offset,
+                  rope->dim_offset + rope->dim_count, (double)rope->theta);
+    c->rope_offset = rope->dim_offset;
+    c->rope_count = rope->dim_count;
+    c->rope_theta = rope->theta;
+    c->rope_set = 1;
+    c->rope_total += shift;
+    return ok();
+  }
   const long long live = c->head - c->tail;
   if (shift == 0 || live == 0) return ok();
   mw::RopeTable tab{};
@@ -478,6 +507,25 @@ static long long window_chunks(const mw_kvcache* c, int window) {
   return window < 0 ? live : window;
 }
 
+// Workspace bytes of an e4m3 cache's window keys rotated on load (w chunks),
+// a multiple of 256 so that the split partials after them stay aligned.
+static size_t rope_window_bytes(const mw_kvcache* c, long long w) {
+  const size_t b = (size_t)w * c->B * c->H * c->L * c->D;
+  return (b + 255) & ~(size_t)255;
+}
+
+// Shifts pending per window chunk of an e4m3 cache (window order), and
+// whether any is; the rotation on load runs only then.
+static bool rope_pending(const mw_kvcache* c, long long w, long long* pend) {
+  bool any = false;
+  for (long long i = 0; i < w; ++i) {
+    const long long chunk = c->head - w + i;
+    pend[i] = c->rope_total - c->rope_at_commit[chunk % c->S];
+    any = any || pend[i] != 0;
+  }
+  return any;
+}
+
 size_t mw_chunk_attn_cached_workspace_size(const mw_kvcache* c, int n_queued, int q_len, int window) {
   if (c == nullptr || n_queued < 1 || q_len < 1 || c->L < 1 || (c->D != 64 && c->D != 72 && c->D != 128)) return 0;
   const long long w = window_chunks(c, window);
@@ -496,6 +544,7 @@ size_t mw_chunk_attn_cached_workspace_size(const mw_kvcache* c, int n_queued, in
             : mw::fwd_plan_cached(c->D, bh, (int)tq, (int)tk, q_len, isolated, (size_t)-1);
     bytes = std::max(bytes, mw::fwd_split_bytes(c->D, bh, mw::fwd_split_rows(ch.bm, (int)tq, sp), sp.n_splits));
   }
+  if (c->elem_bytes == 1 && w > 0) bytes += rope_window_bytes(c, w);  // keys rotated on load
   return bytes;
 }
 
@@ -518,6 +567,13 @@ int mw_chunk_attn_cached_plan(const mw_kvcache* c, int n_queued, int q_len, int 
   if (tk > kMaxT) return fail(MW_EUNSUPPORTED, "%s: too many tokens", fn);
   const int bh = c->B * c->H;
   const bool isolated = flags == MW_QUEUED_ISOLATED;
+  if (c->elem_bytes == 1) {  // the rotated window keys come first in the workspace while shifts are pending
+    long long pend[MW_MAX_WINDOW];
+    if (rope_pending(c, w, pend)) {
+      const size_t kw = rope_window_bytes(c, w);
+      workspace_bytes = workspace_bytes > kw ? workspace_bytes - kw : 0;
+    }
+  }
   const mw::SplitPlan sp =
       c->elem_bytes == 1
           ? mw::fwd_plan_splits(mw::fwd8_choice((int)tq), kFp8Flops, 1, c->D, bh, (int)tq, (int)tk, q_len, isolated,
@@ -685,11 +741,38 @@ int mw_chunk_attn_cached_fp8(const void* q8, const void* k8_new, const void* v8_
   p.slot_stride = (long long)c->B * c->H * c->L * c->D;  // bytes = elements
   p.S = c->S;
   p.first_slot = (int)((c->head - w) % c->S);
+  // rotation on load: window keys with shifts pending are rotated into the
+  // start of the workspace, and the attention reads them from there
+  long long pend[MW_MAX_WINDOW];
+  char* ws = static_cast<char*>(workspace);
+  size_t ws_bytes = workspace != nullptr ? workspace_bytes : 0;
+  if (rope_pending(c, w, pend)) {
+    const size_t kw = rope_window_bytes(c, w);
+    if (ws == nullptr || ws_bytes < kw)
+      return fail(MW_EINVAL, "%s: shifts are pending on the window; its rotated keys need %zu bytes of workspace, got %zu",
+                  fn, kw, ws_bytes);
+    mw::RopeLoadArgs a{};
+    const int np = c->rope_count / 2;
+    for (long long i = 0; i < w; ++i) a.pend[i] = pend[i];
+    for (int i = 0; i < np; ++i) {
+      const double freq = std::pow((double)c->rope_theta, -2.0 * i / c->rope_count);
+      a.c1[i] = std::cos(freq);
+      a.s1[i] = std::sin(freq);
+    }
+    hipError_t e = mw::launch_rope_load_fp8(static_cast<const uint8_t*>(c->k_slots), reinterpret_cast<uint8_t*>(ws),
+                                            p.slot_stride, c->S, p.first_slot, (int)w,
+                                            (long long)c->B * c->H * c->L, c->rope_offset, np, a,
+                                            static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_status(fn, e);
+    p.k_win = reinterpret_cast<const uint8_t*>(ws);
+    ws += kw;
+    ws_bytes -= kw;
+  }
   const mw::SplitPlan sp = mw::fwd_plan_splits(mw::fwd8_choice(p.Tq), kFp8Flops, 1, c->D, p.BH, p.Tq, p.Tk, q_len,
-                                               flags == MW_QUEUED_ISOLATED, workspace != nullptr ? workspace_bytes : 0);
+                                               flags == MW_QUEUED_ISOLATED, ws_bytes);
   p.n_splits = sp.n_splits;
   p.n_whole = sp.n_whole;
-  p.part = static_cast<float*>(workspace);
+  p.part = reinterpret_cast<float*>(ws_bytes > 0 ? ws : nullptr);
   p.so = so;
   p.o_scale = c->v_scale;
   return hip_status(fn, mw::launch_fwd_fp8(p, static_cast<hipStream_t>(stream)));

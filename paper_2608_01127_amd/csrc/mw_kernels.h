@@ -58,6 +58,9 @@ struct FwdParams {
   // (contiguous; element strides are byte strides) and O is multiplied by
   // o_scale (the V scale) before it is stored
   float o_scale;
+  // fp8 kernel only: window keys rotated on load, [n_window][BH, L, 128] bytes
+  // in window order (chunk w at w * slot_stride), or null (keys from the slots)
+  const uint8_t* k_win;
 };
 
 struct BwdParams {
@@ -170,6 +173,18 @@ struct RopeTable {
 hipError_t launch_rope_shift(uint16_t* k_slots, long long slot_stride, int S, int first_slot, int n_live,
                              long long rows_per_slot, int D, int dim_offset, int n_pairs, const RopeTable& tab,
                              hipStream_t stream);
+// Rotation on load of an e4m3 cache's window keys: window chunk w (in window
+// order, in slot (first_slot + w) % S) is rotated by -pend[w] positions on the
+// band [dim_offset, dim_offset + 2 n_pairs); c1[i], s1[i] are the cos and sin
+// of pair i's frequency (its rotation per position).
+struct RopeLoadArgs {
+  long long pend[64];
+  double c1[64];
+  double s1[64];
+};
+hipError_t launch_rope_load_fp8(const uint8_t* k_slots, uint8_t* k_win, long long slot_bytes, int S, int first_slot,
+                                int n_window, long long rows_per_slot, int dim_offset, int n_pairs,
+                                const RopeLoadArgs& args, hipStream_t stream);
 hipError_t launch_kv_copy(const uint16_t* k_src, const uint16_t* v_src, uint16_t* k_dst,
                           uint16_t* v_dst, long long n_elems, hipStream_t stream);
 // Gather of a strided [B, H, L, D] K/V chunk into a contiguous slot.

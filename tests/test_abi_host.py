@@ -36,10 +36,14 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_struct_layout_matches_header():
-    assert ctypes.sizeof(_lib.mw_kvcache) == 88
+    assert ctypes.sizeof(_lib.mw_kvcache) == 112 + 8 * _lib.MW_MAX_SLOTS
     assert _lib.mw_kvcache.head.offset == 40 and _lib.mw_kvcache.tail.offset == 48
     assert _lib.mw_kvcache.k_sink.offset == 56 and _lib.mw_kvcache.sink_len.offset == 72
     assert _lib.mw_kvcache.elem_bytes.offset == 76 and _lib.mw_kvcache.v_scale.offset == 84
+    assert _lib.mw_kvcache.rope_total.offset == 88 and _lib.mw_kvcache.rope_set.offset == 108
+    assert _lib.mw_kvcache.rope_at_commit.offset == 112
+    text = open(os.path.join(ROOT, "include", "mw.h")).read()
+    assert re.search(r"#define MW_MAX_SLOTS %d\b" % _lib.MW_MAX_SLOTS, text)
     assert ctypes.sizeof(_lib.mw_rope) == 12
 
 
@@ -377,7 +381,8 @@ def test_fp8_validation():
     assert (b.elem_bytes, b.k_scale, b.v_scale) == (2, 1.0, 1.0)
     rope = _lib.mw_rope(0, 44, 10000.0)
     c.head = 2
-    assert lib.mw_kvcache_rope_shift(ctypes.byref(c), 3, ctypes.byref(rope), None) == mw.MW_EUNSUPPORTED
+    assert lib.mw_kvcache_rope_shift(ctypes.byref(c), 3, ctypes.byref(rope), None) == mw.MW_OK  # recorded
+    c.rope_total, c.rope_set = 0, 0
     cached = lambda cache, *a: lib.mw_chunk_attn_cached(A, A, A, 2, 16, ctypes.byref(cache), 1, 0, A, None, 0.125,
                                                         None, 0, None)
     assert cached(c) == mw.MW_EINVAL and "e4m3" in err()
@@ -406,12 +411,54 @@ def test_fp8_validation():
 
 
 def test_fp8_workspace_size_policy():
+    """An e4m3 cache's workspace size covers the split partials and the window's keys rotated
+    on load (always included, whether shifts are pending or not)."""
     lib = mw.load()
     c = _lib.mw_kvcache()
     assert lib.mw_kvcache_init_fp8(ctypes.byref(c), A, A, 8, 1, 16, 2640, 128, 0.02, 0.02) == mw.MW_OK
     c.head = 6
-    small = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 1, 128, 6)
+    kwin = 6 * 16 * 2640 * 128  # a multiple of 256
+    small = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 1, 128, 6) - kwin
     assert small % (16 * 128 * 130 * 4) == 0 and small // (16 * 128 * 130 * 4) >= 8
+    assert lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 1, 128, 2) - 2 * 16 * 2640 * 128 >= 0
+
+
+def test_fp8_reshift_record_and_pending_workspace():
+    """e4m3 re-shift by rotation on load, host side: a shift only adds to rope_total and fixes
+    the band; a later shift with another band or theta is rejected; S beyond MW_MAX_SLOTS is
+    refused at init; with shifts pending the split plan gets the workspace left after the
+    rotated window keys, and a call whose workspace cannot hold them fails before any launch."""
+    lib = mw.load()
+    c = _lib.mw_kvcache()
+    assert lib.mw_kvcache_init_fp8(ctypes.byref(c), A, A, _lib.MW_MAX_SLOTS + 1, 1, 2, 16, 128, 1.0, 1.0) \
+        == mw.MW_EUNSUPPORTED
+    assert lib.mw_kvcache_init_fp8(ctypes.byref(c), A, A, 4, 1, 16, 2640, 128, 0.02, 0.02) == mw.MW_OK
+    assert (c.rope_total, c.rope_set) == (0, 0) and list(c.rope_at_commit[:4]) == [0, 0, 0, 0]
+    c.head, c.tail = 3, 0                                 # chunks 0, 1, 2 committed before any shift
+    shift = lib.mw_kvcache_rope_shift
+    assert shift(ctypes.byref(c), 3, ctypes.byref(_lib.mw_rope(0, 44, 10000.0)), None) == mw.MW_OK
+    assert shift(ctypes.byref(c), -1, ctypes.byref(_lib.mw_rope(0, 44, 10000.0)), None) == mw.MW_OK
+    assert (c.rope_total, c.rope_set, c.rope_offset, c.rope_count) == (2, 1, 0, 44)
+    assert shift(ctypes.byref(c), 3, ctypes.byref(_lib.mw_rope(2, 44, 10000.0)), None) == mw.MW_EINVAL
+    assert "band" in err()
+    assert shift(ctypes.byref(c), 3, ctypes.byref(_lib.mw_rope(0, 44, 500.0)), None) == mw.MW_EINVAL
+    assert shift(ctypes.byref(c), 3, ctypes.byref(_lib.mw_rope(1, 44, 10000.0)), None) == mw.MW_EINVAL
+    assert c.rope_total == 2
+    kwin = 3 * 16 * 2640 * 128
+    need = lib.mw_chunk_attn_cached_workspace_size(ctypes.byref(c), 1, 64, 3)
+    ns, nw = ctypes.c_int(0), ctypes.c_int(0)
+    plan = lambda ws: (lib.mw_chunk_attn_cached_plan(ctypes.byref(c), 1, 64, 3, 0, ws, ctypes.byref(ns),
+                                                     ctypes.byref(nw)), ns.value)
+    assert plan(need) == (mw.MW_OK, plan(need - kwin + kwin)[1])
+    splits_pending = plan(need)[1]
+    assert plan(kwin)[1] == 1                             # nothing left for partials: unsplit
+    c.rope_at_commit[0] = c.rope_at_commit[1] = c.rope_at_commit[2] = 2   # nothing pending
+    assert plan(need - kwin)[1] == splits_pending         # the same partials fit without the rotated keys
+    c.rope_at_commit[1] = 0                               # chunk 1 pending again
+    f8 = lib.mw_chunk_attn_cached_fp8
+    assert f8(A, A, A, 1, 64, ctypes.byref(c), 3, 0, A, None, 0.125, 1.0, A, kwin - 256, None, None) == mw.MW_EINVAL
+    assert "rotated keys" in err()
+    assert f8(A, A, A, 1, 64, ctypes.byref(c), 3, 0, A, None, 0.125, 1.0, None, 0, None, None) == mw.MW_EINVAL
 
 
 

@@ -68,8 +68,10 @@ def test_fp8_append_quantizes_into_the_slot(mw):
         sync()
         assert np.array_equal(u8(cache.k_slots[slot]), codes(kb, ks))
         assert np.array_equal(u8(cache.v_slots[slot]), codes(vb, vs))
-    with pytest.raises(mw.MWError):
-        mw.mw_kvcache_rope_shift(cache, 2, 0, 44)
+    mw.mw_kvcache_rope_shift(cache, 2, 0, 44)  # e4m3: recorded for rotation on load, the slots stay as committed
+    sync()
+    assert cache.desc.rope_total == 2 and cache.desc.rope_set == 1
+    assert np.array_equal(u8(cache.k_slots[slot]), codes(kb, ks))
 
 
 def run_fp8_case(mw, B, H, L, S, n_commit, window, nq, qlen, mode, split, sink_len=0, seed=0):
@@ -261,3 +263,70 @@ def test_fp8_decode_full_window(mw, q_len):
                                       [dq(c[0], ks) for c in win], [dq(c[1], vs) for c in win], 1, q_len)
     assert_close(f"o q_len={q_len} ({ns} key ranges)", to_f64(o), ro, FP8_MAX_ABS, FP8_MEAN_ABS)
     assert_close("lse", to_f64(lse), rl, max_abs=2e-3, mean_abs=2e-4)
+
+
+def _reshift_rollout(mw, shifts_per_eviction, steps=6, seed=9800):
+    """e4m3 rollout (B1 H2 L96 D128, 4-slot ring, 3-chunk window): commit, evict down to the
+    window, then re-shift by the given list of shifts per eviction.  Returns the cache, the
+    committed chunks' bits and, per chunk, the shift total pending on it."""
+    B, H, L, D, S, W = 1, 2, 96, 128, 4, 3
+    ks, vs = 0.011, 0.012
+    cache = mw.KVCache(S, B, H, L, D, fp8=True, k_scale=ks, v_scale=vs)
+    hist, at_commit, total = [], [], 0
+    for t in range(steps):
+        kb, vb = (synth.normal_bf16((B, H, L, D), seed + 2 * t + j) for j in range(2))
+        mw.mw_kvcache_append(cache, to_gpu(kb), to_gpu(vb))
+        hist.append((kb, vb))
+        at_commit.append(total)
+        if cache.live > W:
+            mw.mw_kvcache_evict(cache, cache.live - W)
+            for sh in shifts_per_eviction:
+                mw.mw_kvcache_rope_shift(cache, sh, 0, 44)
+                total += sh
+    return cache, hist, [total - a for a in at_commit], (B, H, L, D, W, ks, vs)
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_fp8_rope_reshift_on_load_vs_oracle(mw, mode):
+    """Re-shift of an e4m3 cache by rotation on load (paper Sec. 3.5, its second option): after a
+    rollout with a re-shift of 2 positions per eviction, the attention of two queued chunks equals
+    the oracle's over the window keys rotated by each chunk's pending shift and rounded to e4m3
+    once (within the fp8 bar), while the slots keep the committed codes bit for bit."""
+    cache, hist, pend, (B, H, L, D, W, ks, vs) = _reshift_rollout(mw, [2])
+    print(f"[case] fp8 re-shift on load mode={mode} pending={pend[-W:]}", flush=True)
+    nq = 2
+    inp = {n: synth.normal_bf16((B, H, nq * L, D), 9890 + i) for i, n in enumerate("qkv")}
+    qs = 0.0105
+    q8, k8, v8 = (mw.mw_quantize_fp8(to_gpu(inp[n]), sc) for n, sc in (("q", qs), ("k", ks), ("v", vs)))
+    o, lse = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, nq, L, cache, qs, window=W, flags=mode, want_lse=True)
+    sync()
+    live = range(len(hist) - W, len(hist))
+    for c in live:  # the slots are never rewritten
+        assert np.array_equal(u8(cache.k_slots[cache.slot_of(c)]), codes(hist[c][0], ks))
+    dq = lambda b, sc: oracle.dequantize_fp8(codes(b, sc), sc)
+    win_k = []
+    for c in live:  # rotate the committed code values, round to e4m3 once, scale
+        vals = oracle.dequantize_fp8(codes(hist[c][0], ks), 1.0)
+        rot = oracle.rope_rotate(vals, -float(pend[c]), 0, 44).astype(np.float32)
+        win_k.append(oracle.dequantize_fp8(oracle.quantize_fp8(rot, 1.0), ks))
+    ro, rl = oracle.cached_chunk_attn(dq(inp["q"], qs), dq(inp["k"], ks), dq(inp["v"], vs), win_k,
+                                      [dq(hist[c][1], vs) for c in live], nq, L, mode=mode)
+    assert_close("o (rotated on load)", to_f64(o), ro, FP8_MAX_ABS, FP8_MEAN_ABS)
+    assert_close("lse", to_f64(lse), rl, max_abs=2e-3, mean_abs=2e-4)
+
+
+def test_fp8_rope_reshift_pending_total_only(mw):
+    """Rotation on load applies each chunk's pending total at once: shifting by 1 three times per
+    eviction gives the same output bit for bit as shifting by 3 once, and a shift of +5 then -5
+    gives the output of no shift at all (nothing pending, nothing rounded)."""
+    outs = []
+    for shifts in ([1, 1, 1], [3], [5, -5], []):
+        cache, hist, pend, (B, H, L, D, W, ks, vs) = _reshift_rollout(mw, shifts, seed=9900)
+        q8, k8, v8 = (mw.mw_quantize_fp8(to_gpu(synth.normal_bf16((B, H, 2 * L, D), 9950 + i)), 0.01)
+                      for i in range(3))
+        o, _ = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, 2, L, cache, 0.01, window=W)
+        outs.append(o.clone())
+    sync()
+    assert bits_equal(outs[0], outs[1])
+    assert bits_equal(outs[2], outs[3])
+    assert not bits_equal(outs[1], outs[3])
