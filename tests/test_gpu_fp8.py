@@ -330,3 +330,46 @@ def test_fp8_rope_reshift_pending_total_only(mw):
     assert bits_equal(outs[0], outs[1])
     assert bits_equal(outs[2], outs[3])
     assert not bits_equal(outs[1], outs[3])
+
+
+@pytest.mark.parametrize("q_len,window", [(64, 2), (96, 3)])
+def test_fp8_rope_reshift_on_load_sink_partial_window(mw, q_len, window):
+    """Rotation on load with a sink (never shifted: it keeps its position), a window smaller than
+    the live chunks of a wrapped ring, and (q_len 64) a short queued chunk whose call splits the
+    keys, so the split partials sit in the workspace after the rotated window keys; against the
+    oracle over the window keys rotated by their pending shifts and rounded once, fp8 bar."""
+    B, H, L, D, S = 1, 2, 128, 128, 4
+    ks, vs, qs = 0.011, 0.012, 0.0105
+    cache = mw.KVCache(S, B, H, L, D, fp8=True, k_scale=ks, v_scale=vs)
+    sink_len = 40
+    sk, sv = (synth.normal_bf16((B, H, sink_len, D), 9960 + i) for i in range(2))
+    cache.set_sink(mw.mw_quantize_fp8(to_gpu(sk), ks), mw.mw_quantize_fp8(to_gpu(sv), vs))
+    hist, at_commit, total = [], [], 0
+    for t in range(7):  # the ring wraps; each eviction re-shifts by 3
+        kb, vb = (synth.normal_bf16((B, H, L, D), 9970 + 2 * t + j) for j in range(2))
+        if cache.live == S:
+            mw.mw_kvcache_evict(cache, 1)
+            mw.mw_kvcache_rope_shift(cache, 3, 0, 44)
+            total += 3
+        mw.mw_kvcache_append(cache, to_gpu(kb), to_gpu(vb))
+        hist.append((kb, vb))
+        at_commit.append(total)
+    ns, _ = mw.mw_chunk_attn_cached_plan(cache, 1, q_len, window)
+    print(f"[case] fp8 re-shift on load q_len={q_len} window={window} splits={ns}", flush=True)
+    inp = {n: synth.normal_bf16((B, H, q_len, D), 9990 + i) for i, n in enumerate("qkv")}
+    q8, k8, v8 = (mw.mw_quantize_fp8(to_gpu(inp[n]), sc) for n, sc in (("q", qs), ("k", ks), ("v", vs)))
+    o, _ = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, 1, q_len, cache, qs, window=window)
+    sync()
+    if q_len == 64:
+        assert ns > 1
+    dq = lambda b, sc: oracle.dequantize_fp8(codes(b, sc), sc)
+    win = range(len(hist) - window, len(hist))
+    win_k = []
+    for c in win:
+        vals = oracle.dequantize_fp8(codes(hist[c][0], ks), 1.0)
+        rot = oracle.rope_rotate(vals, -float(total - at_commit[c]), 0, 44).astype(np.float32)
+        win_k.append(oracle.dequantize_fp8(oracle.quantize_fp8(rot, 1.0), ks))
+    ro, _ = oracle.cached_chunk_attn(dq(inp["q"], qs), dq(inp["k"], ks), dq(inp["v"], vs), win_k,
+                                     [dq(hist[c][1], vs) for c in win], 1, q_len, sink_k=dq(sk, ks),
+                                     sink_v=dq(sv, vs))
+    assert_close(f"o q_len={q_len} window={window}", to_f64(o), ro, FP8_MAX_ABS, FP8_MEAN_ABS)
