@@ -335,10 +335,11 @@ def test_fp8_rope_reshift_pending_total_only(mw):
 @pytest.mark.parametrize("q_len,window", [(64, 2), (96, 3)])
 def test_fp8_rope_reshift_on_load_sink_partial_window(mw, q_len, window):
     """Rotation on load with a sink (never shifted: it keeps its position), a window smaller than
-    the live chunks of a wrapped ring, and (q_len 64) a short queued chunk whose call splits the
-    keys, so the split partials sit in the workspace after the rotated window keys; against the
-    oracle over the window keys rotated by their pending shifts and rounded once, fp8 bar."""
-    B, H, L, D, S = 1, 2, 128, 128, 4
+    the live chunks of a wrapped ring, and a short queued chunk whose call splits the keys (2 and
+    3 key ranges at these shapes), so the split partials sit in the workspace after the rotated
+    window keys; against the oracle over the window keys rotated by their pending shifts and
+    rounded once, fp8 bar."""
+    B, H, L, D, S = 1, 2, 256, 128, 4
     ks, vs, qs = 0.011, 0.012, 0.0105
     cache = mw.KVCache(S, B, H, L, D, fp8=True, k_scale=ks, v_scale=vs)
     sink_len = 40
@@ -360,8 +361,7 @@ def test_fp8_rope_reshift_on_load_sink_partial_window(mw, q_len, window):
     q8, k8, v8 = (mw.mw_quantize_fp8(to_gpu(inp[n]), sc) for n, sc in (("q", qs), ("k", ks), ("v", vs)))
     o, _ = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, 1, q_len, cache, qs, window=window)
     sync()
-    if q_len == 64:
-        assert ns > 1
+    assert ns > 1
     dq = lambda b, sc: oracle.dequantize_fp8(codes(b, sc), sc)
     win = range(len(hist) - window, len(hist))
     win_k = []
