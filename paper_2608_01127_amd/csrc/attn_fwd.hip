@@ -120,6 +120,11 @@ __device__ __forceinline__ void stage_kv(const FwdParams& p, int bh, long long k
 // O rescale is skipped on almost every step.
 constexpr float kRescaleThreshold = 8.f;
 
+// K/V stages of a configuration: two (double buffering) except for the
+// four-wave key-group configuration of 64 queued rows, which streams 64-key
+// tiles four deep.
+constexpr int fwd_stages(int nw, int kg) { return kg > 1 && nw == 4 ? 4 : 2; }
+
 // NW waves per workgroup, each owning RB blocks of 32 query rows; BN keys per
 // main-loop step.  With RB = 2 every K and V fragment read from LDS feeds two
 // MFMAs (one per row block), halving LDS traffic per MFMA: with one 32-row
@@ -138,7 +143,8 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   constexpr int KK = (D + 15) / 16;  // contraction steps over D (D = 72: the last one half zeros)
   constexpr int DB = (D + 31) / 32;  // 32-wide column blocks of D (D = 72: the last one 8 wide)
   constexpr int TE = stage_elems<D, BK, NT>();  // elements of one staged tile buffer
-  __shared__ __attribute__((aligned(16))) bf16_t lds[2][2][TE];  // K, V x double buffer
+  constexpr int NSTG = fwd_stages(NW, KG);      // K/V stages (see the main loop)
+  __shared__ __attribute__((aligned(16))) bf16_t lds[2][NSTG][TE];  // K, V x stages
   bf16_t(*Ks)[TE] = lds[0];
   bf16_t(*Vs)[TE] = lds[1];
 
@@ -169,6 +175,7 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
     qrow[rb] = q0 + (rw * RB + rb) * 32 + (lane & 31);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
+      if constexpr (NSTG > 2) break;  // staged through LDS with the first K/V tiles
       if (qrow[rb] < p.Tq && (D % 16 == 0 || 16 * kk + 8 * (lane >> 5) < D)) {
         qf[rb][kk] = *reinterpret_cast<const bf16x8*>(p.q + qbase + qrow[rb] * p.sq.t + 16 * kk + 8 * (lane >> 5));
       } else {  // rows past Tq and columns past D contribute zeros
@@ -321,7 +328,72 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   auto slice = [&](auto masked, const int k0, const int st) { step(masked, k0 + kg * BN, Ks[st], Vs[st]); };
   const KVOffsets<D, CACHED, BK, NT> kvo(p, tid);
   int kc = advance(kbeg - BK);  // next tile to use
-  {
+  if constexpr (NSTG > 2) {
+    // Streaming configurations (few query rows, bound by reading the keys):
+    // up to NSTG - 1 tiles in flight.  Each wave waits only for the oldest of
+    // its outstanding tiles (s_waitcnt on the vector-memory counter, which the
+    // LDS-direct loads of a tile decrement in issue order), then one barrier
+    // makes the tile visible and frees the buffer computed last, which takes
+    // the next tile.  A tile is 2 * ROUNDS loads per thread on every path.
+    // The Q tile is staged the same way, first, into the last stage buffer
+    // (64 rows in its K half, the next 64 in its V half), which the first
+    // tiles leave free; every Q load has landed once at most the tiles' loads
+    // are outstanding, and the Q fragments are read from LDS before the first
+    // barrier of the loop frees that buffer.  (Loading Q straight into
+    // registers would leave the compiler, which cannot see the LDS-direct
+    // loads, waiting for all outstanding loads inside the loop.)
+    constexpr int P = 2 * StagePlan<D, BK, NT>::ROUNDS;
+    static_assert(P * (NSTG - 1) <= 63, "vector-memory counter range");
+    static_assert(BM % 64 == 0 && BM <= 128 && TE >= 64 * D, "the Q tile fits the last stage buffer");
+#pragma unroll
+    for (int h = 0; h < BM / 64; ++h) {
+      bf16_t* qs = h == 0 ? Ks[NSTG - 1] : Vs[NSTG - 1];
+      stage_rows_direct<D, 64, NT>(qs, [&](int r) { return p.q + qbase + min(q0 + 64 * h + r, p.Tq - 1) * p.sq.t; },
+                                   tid);
+    }
+    int ki = kc, ib = 0, ahead = 0;  // next tile to issue, its buffer, tiles issued and not yet used
+#pragma unroll
+    for (int s = 0; s < NSTG - 1; ++s) {
+      if (ki < kend) {
+        stage_kv<D, CACHED, BK, NT>(p, bh, kbase, vbase, ki, Ks[ib], Vs[ib], kvo, tid);
+        ki = advance(ki);
+        ib = ib + 1 == NSTG ? 0 : ib + 1;
+        ++ahead;
+      }
+    }
+    wait_vmem_upto<P, NSTG - 1>(ahead);  // the Q loads
+    __syncthreads();
+    {
+      const FragOffsets<D> fq(lane, 0);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int r0 = (rw * RB + rb) * 32;  // this row block within the Q tile
+        const bf16_t* qs = r0 < 64 ? Ks[NSTG - 1] : Vs[NSTG - 1];
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) qf[rb][kk] = fq.row8(qs, r0 & 63, kk);
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    }
+    int cb = 0;
+    auto run = [&](auto masked, const int kstop) {
+      while (kc < kstop) {
+        wait_vmem_upto<P, NSTG - 2>(ahead - 1);  // tile kc has landed
+        __syncthreads();
+        if (ki < kend) {
+          stage_kv<D, CACHED, BK, NT>(p, bh, kbase, vbase, ki, Ks[ib], Vs[ib], kvo, tid);
+          ki = advance(ki);
+          ib = ib + 1 == NSTG ? 0 : ib + 1;
+          ++ahead;
+        }
+        slice(masked, kc, cb);
+        --ahead;
+        cb = cb + 1 == NSTG ? 0 : cb + 1;
+        kc = advance(kc);
+      }
+    };
+    run(std::false_type{}, min(kfull, kend));
+    run(std::true_type{}, kend);
+  } else {
     // double buffering: the next tile streams in during this step's math
     int buf = 0;
     if (kc < kend) stage_kv<D, CACHED, BK, NT>(p, bh, kbase, vbase, kc, Ks[0], Vs[0], kvo, tid);
@@ -470,17 +542,20 @@ struct FwdCfg {
 // wider accumulators leave no room for two row blocks per wave.)
 
 // Cached attention with few queued rows (a short chunk over a long window) is
-// bound by streaming the window from HBM.  Eight waves split into key groups
-// (4 groups of 2 row waves for 64 rows, 2 groups of 4 for 128 rows) stage 128
-// keys per step, so every SIMD of the CU has two waves at work on the rows.
+// bound by streaming the window from HBM.  The waves split into key groups of
+// row waves: for 64 rows, four waves in 2 groups of 2 stage 64 keys per step,
+// four stages deep (one wave per SIMD; measured 3-4% faster than eight waves
+// in 4 groups double-buffering 128-key steps, whose bulk waits leave the
+// memory pipe idle between steps); for 128 rows, eight waves in 2 groups of 4
+// stage 128 keys per step, double-buffered.
 // Up to 512 queued rows run as 128-row tiles of this kind (their workgroups read
 // the same window, which the L2 and the Infinity Cache share): measured 20% and
 // 11% faster than 256-row tiles at 256 and 512 rows over a 6 x 2640-token window.
 template <int D, int NWR>
 struct FwdDecodeCfg {
-  static constexpr int NW = 8;
+  static constexpr int NW = NWR == 2 ? 4 : 8;
   static constexpr int KG = NW / NWR;
-  static constexpr int BN = 128 / KG;
+  static constexpr int BN = NWR == 2 ? 32 : 128 / KG;
   static constexpr int RB = 1;
 };
 
@@ -632,7 +707,7 @@ hipError_t launch_fwd_decode_128(const FwdParams& p, int bm, hipStream_t stream)
   using C = FwdDecodeCfg<128, 4>;
   return launch_fwd_tpl<128, true, C::NW, C::BN, C::RB, C::KG>(p, stream);
 }
-// (fallback: 8 waves of 190-235 registers and 128 KB of LDS, one per CU)
+// (fallback: 4 or 8 waves of 180-245 registers and 128 KB of LDS, one per CU)
 int fwd_resident_wgs_decode_128(int bm) {
   using C2 = FwdDecodeCfg<128, 2>;
   using C4 = FwdDecodeCfg<128, 4>;

@@ -325,6 +325,39 @@ __device__ __forceinline__ void stage_f32x64_direct(float* lds, const float* g, 
 // counter at zero.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0); }
 
+// Wait until at most n * P of this wave's vector-memory operations are
+// outstanding (0 <= n <= NMAX <= 3, wave-uniform); the other counters are not
+// waited on.  gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4,
+// lgkmcnt 11:8 (7 and 15: no wait).
+template <int N>
+__device__ __forceinline__ void waitcnt_vm() {
+  static_assert(N >= 0 && N <= 63, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+template <int P, int NMAX>
+__device__ __forceinline__ void wait_vmem_upto(int n) {
+  static_assert(NMAX <= 3, "up to three groups outstanding");
+  if constexpr (NMAX >= 3) {
+    if (n >= 3) {
+      waitcnt_vm<3 * P>();
+      return;
+    }
+  }
+  if constexpr (NMAX >= 2) {
+    if (n >= 2) {
+      waitcnt_vm<2 * P>();
+      return;
+    }
+  }
+  if constexpr (NMAX >= 1) {
+    if (n >= 1) {
+      waitcnt_vm<P>();
+      return;
+    }
+  }
+  waitcnt_vm<0>();
+}
+
 
 // Combine a value with the one held by lane l ^ 32: gfx950's permlane32 swap
 // exchanges the two 32-lane halves of a register in the VALU, without the LDS
