@@ -199,19 +199,26 @@ __device__ __forceinline__ void stage_kv8(const FwdParams& p, int bh, int k0, fp
 
 constexpr float kRescaleThreshold8 = 8.f;  // probabilities stay <= 2^8 < 448
 
-// NW waves of RB 32-row query blocks; BN keys (a multiple of 64) per step.
-template <int NW, int RB, int BN>
+// NW waves of RB 32-row query blocks in KG key groups of NW / KG row waves;
+// each step stages KG * BN keys (BN a multiple of 64) and group g works on
+// its BN-key slice; the groups merge (m, l, O) through LDS at the end.  With
+// key groups (the few-row configurations) the tiles stream four stages deep.
+template <int NW, int RB, int BN, int KG>
 __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd_fp8_kernel(FwdParams p) {
-  constexpr int BM = 32 * RB * NW, NT = 64 * NW, KB = BN / 32, KP = BN / 64;
+  static_assert(NW % KG == 0, "waves split evenly into key groups");
+  constexpr int NWR = NW / KG;
+  constexpr int BM = 32 * RB * NWR, NT = 64 * NW, KB = BN / 32, KP = BN / 64, BK = BN * KG;
   constexpr int KK = DH / 64, DB = DH / 32;
-  __shared__ __attribute__((aligned(16))) fp8_t lds[2][2][BN * DH];  // K, V x double buffer
-  fp8_t(*Ks)[BN * DH] = lds[0];
-  fp8_t(*Vs)[BN * DH] = lds[1];
+  constexpr int NSTG = KG > 1 ? 4 : 2;
+  __shared__ __attribute__((aligned(16))) fp8_t lds[2][NSTG][BK * DH];  // K, V x stages
+  fp8_t(*Ks)[BK * DH] = lds[0];
+  fp8_t(*Vs)[BK * DH] = lds[1];
 
   const int NS = p.n_splits;  // key ranges of a split tile (partials layout)
   int bh, qt, split, nst;      // nst: key ranges of this workgroup's tile
   cached_item(blockIdx.x, gridDim.x, p.n_qtiles, NS, p.n_whole, bh, qt, split, nst);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int rw = wave % NWR, kg = wave / NWR;  // row wave, key group
   const int q0 = qt * BM;
   const int b_ = bh / p.H, h_ = bh - b_ * p.H;
   const fp8_t* qg = reinterpret_cast<const fp8_t*>(p.q) + (long long)bh * p.Tq * DH;
@@ -222,9 +229,10 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   i32x8 qf[RB][KK];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    qrow[rb] = q0 + (wave * RB + rb) * 32 + (lane & 31);
+    qrow[rb] = q0 + (rw * RB + rb) * 32 + (lane & 31);
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
+      if constexpr (NSTG > 2) break;  // staged through LDS with the first K/V tiles
       if (qrow[rb] < p.Tq) {
         const fp8_t* src = qg + (long long)qrow[rb] * DH + 64 * kk + 32 * (lane >> 5);
         const i32x4 a = *reinterpret_cast<const i32x4*>(src);
@@ -240,12 +248,12 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
   vis.range(q0, e1f, s2f, e2f);
   vis.range(min(q0 + BM, p.Tq) - 1, e1l, s2l, e2l);
   const int kend_all = max(e1l, e2l);
-  const int ntiles = (kend_all + BN - 1) / BN;
-  const int kbeg = (int)((long long)ntiles * split / nst) * BN;
-  const int kend = min(kend_all, (int)((long long)ntiles * (split + 1) / nst) * BN);
+  const int ntiles = (kend_all + BK - 1) / BK;
+  const int kbeg = (int)((long long)ntiles * split / nst) * BK;
+  const int kend = min(kend_all, (int)((long long)ntiles * (split + 1) / nst) * BK);
   auto advance = [&](int k) {
-    int n = k + BN;
-    if (n >= e1l && n + BN <= s2f) n = (s2f / BN) * BN;
+    int n = k + BK;
+    if (n >= e1l && n + BK <= s2f) n = (s2f / BK) * BK;
     return n;
   };
 
@@ -259,7 +267,7 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
     lsum[rb] = 0.f;
   }
   const float c = p.scale_log2;  // softmax scale * q_scale * k_scale * log2(e)
-  const int kfull = max(0, (e1f / BN) * BN);
+  const int kfull = max(0, (e1f / BK) * BK);
 
   auto step = [&](auto masked, const int k0, const fp8_t* Kt, const fp8_t* Vt) {
     f32x16 s[RB][KB];
@@ -347,18 +355,81 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
     }
   };
 
-  const RowOffsets8<BN, NT> ro(DH, tid);
-  int kc = advance(kbeg - BN);
-  {
+  // this wave's slice of a staged step: keys [kg * BN, (kg + 1) * BN)
+  auto slice = [&](auto masked, const int k0, const int st) {
+    step(masked, k0 + kg * BN, Ks[st] + kg * BN * DH, Vs[st] + kg * BN * DH);
+  };
+  const RowOffsets8<BK, NT> ro(DH, tid);
+  int kc = advance(kbeg - BK);
+  if constexpr (NSTG > 2) {
+    // Up to NSTG - 1 tiles in flight: each wave waits on the vector-memory
+    // counter only for the oldest of its tiles (a tile is 2 * ROUNDS loads per
+    // thread on every staging path), then one barrier publishes the tile and
+    // frees the buffer computed last for the next one.  The Q tile is staged
+    // first, into the last stage buffer, which the first tiles leave free, and
+    // read into registers before the loop's first barrier frees it (loaded
+    // straight into registers, the compiler, blind to the LDS-direct loads,
+    // would wait for all outstanding loads inside the loop).
+    constexpr int P = 2 * RowOffsets8<BK, NT>::ROUNDS;
+    constexpr int QR = BM * 8 / NT;  // Q staging rounds
+    static_assert(P * (NSTG - 1) <= 63, "vector-memory counter range");
+    static_assert((BM * 8) % NT == 0 && BM <= BK, "the Q tile is whole rounds and fits a K buffer");
+    fp8_t* qs = Ks[NSTG - 1];
+#pragma unroll
+    for (int it = 0; it < QR; ++it) {
+      const int ci = it * NT + tid;
+      const int row = ci >> 3;
+      const int ls = (ci & 7) ^ Tile8::swz(row);
+      const fp8_t* src = qg + (long long)min(q0 + row, p.Tq - 1) * DH + 16 * ls;
+      dma_lds_16(src, lds_addr(qs) + it * NT * 16 + wave_stage_off(tid));
+    }
+    int ki = kc, ib = 0, ahead = 0;  // next tile to issue, its buffer, tiles issued and not yet used
+#pragma unroll
+    for (int s = 0; s < NSTG - 1; ++s) {
+      if (ki < kend) {
+        stage_kv8<BK, NT>(p, bh, ki, Ks[ib], Vs[ib], ro, tid);
+        ki = advance(ki);
+        ib = ib + 1 == NSTG ? 0 : ib + 1;
+        ++ahead;
+      }
+    }
+    wait_vmem_upto<P, NSTG - 1>(ahead);  // the Q loads
+    __syncthreads();
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) qf[rb][kk] = lds_k8(qs, (rw * RB + rb) * 32 + (lane & 31), kk, lane);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    int cb = 0;
+    auto run = [&](auto masked, const int kstop) {
+      while (kc < kstop) {
+        wait_vmem_upto<P, NSTG - 2>(ahead - 1);  // tile kc has landed
+        __syncthreads();
+        if (ki < kend) {
+          stage_kv8<BK, NT>(p, bh, ki, Ks[ib], Vs[ib], ro, tid);
+          ki = advance(ki);
+          ib = ib + 1 == NSTG ? 0 : ib + 1;
+          ++ahead;
+        }
+        slice(masked, kc, cb);
+        --ahead;
+        cb = cb + 1 == NSTG ? 0 : cb + 1;
+        kc = advance(kc);
+      }
+    };
+    run(std::false_type{}, min(kfull, kend));
+    run(std::true_type{}, kend);
+  } else {
     int buf = 0;
-    if (kc < kend) stage_kv8<BN, NT>(p, bh, kc, Ks[0], Vs[0], ro, tid);
+    if (kc < kend) stage_kv8<BK, NT>(p, bh, kc, Ks[0], Vs[0], ro, tid);
     wait_vmem();
     __syncthreads();
     auto run = [&](auto masked, const int kstop) {
       while (kc < kstop) {
         const int kn = advance(kc);
-        if (kn < kend) stage_kv8<BN, NT>(p, bh, kn, Ks[buf ^ 1], Vs[buf ^ 1], ro, tid);
-        step(masked, kc, Ks[buf], Vs[buf]);
+        if (kn < kend) stage_kv8<BK, NT>(p, bh, kn, Ks[buf ^ 1], Vs[buf ^ 1], ro, tid);
+        slice(masked, kc, buf);
         wait_vmem();
         __syncthreads();
         buf ^= 1;
@@ -367,6 +438,64 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
     };
     run(std::false_type{}, min(kfull, kend));
     run(std::true_type{}, kend);
+  }
+
+  if constexpr (KG > 1) {
+    // merge the key groups' (m, l, O) into group 0 through LDS (the stages are
+    // free once every wave has passed the barrier):
+    // M = max_g m_g, w_g = 2^(m_g - M), O = sum_g w_g O_g, l = sum_g w_g l_g
+    constexpr int XO = (KG - 1) * NWR * RB * DB * 16 * 64;
+    constexpr int XM = (KG - 1) * NWR * RB * 2 * 64;
+    static_assert((XO + XM) * 4 <= (int)sizeof(lds), "exchange fits the K/V stages");
+    float* xo = reinterpret_cast<float*>(&lds[0][0][0]);
+    float* xm = xo + XO;
+    __syncthreads();
+    if (kg > 0) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int slot = ((kg - 1) * NWR + rw) * RB + rb;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i) xo[((slot * DB + db) * 16 + i) * 64 + lane] = o[rb][db][i];
+        }
+        xm[(slot * 2) * 64 + lane] = m[rb];
+        xm[(slot * 2 + 1) * 64 + lane] = lsum[rb];
+      }
+    }
+    __syncthreads();
+    if (kg > 0) return;  // no barrier follows
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      float mg[KG], wg[KG];
+      mg[0] = m[rb];
+      float M = m[rb];
+#pragma unroll
+      for (int g = 1; g < KG; ++g) {
+        mg[g] = xm[((((g - 1) * NWR + rw) * RB + rb) * 2) * 64 + lane];
+        M = fmaxf(M, mg[g]);
+      }
+#pragma unroll
+      for (int g = 0; g < KG; ++g) wg[g] = (mg[g] == -INFINITY) ? 0.f : fast_exp2(mg[g] - M);
+      float l = wg[0] * lsum[rb];
+#pragma unroll
+      for (int g = 1; g < KG; ++g) l += wg[g] * xm[((((g - 1) * NWR + rw) * RB + rb) * 2 + 1) * 64 + lane];
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          float acc = wg[0] * o[rb][db][i];
+#pragma unroll
+          for (int g = 1; g < KG; ++g) {
+            const int slot = ((g - 1) * NWR + rw) * RB + rb;
+            acc += wg[g] * xo[((slot * DB + db) * 16 + i) * 64 + lane];
+          }
+          o[rb][db][i] = acc;
+        }
+      }
+      m[rb] = M;
+      lsum[rb] = l;
+    }
   }
 
 #pragma unroll
@@ -513,24 +642,29 @@ struct Fwd8Cfg {
   static constexpr int NW = 8;
   static constexpr int RB = 1;
   static constexpr int BN = 128;
+  static constexpr int KG = 1;
 };
 
 // Few queued rows (a short chunk over a long window) stream the window from
-// HBM: workgroups of 2 waves (64 rows, 128 keys per step, two per CU by LDS)
-// or 4 waves (128 rows, 64 keys per step) instead of 256-row ones that would
-// mostly compute padding rows (measured 7-10% faster on one 64- or 128-token
-// chunk over a 6 x 2640-token window).
-template <int NW>
+// HBM: 64 rows run 4 waves and 128 rows 8 waves, as 2 key groups of 64 keys
+// (128 keys per step, four stages deep), so that every SIMD has a wave at
+// work and tiles stay in flight between steps (measured 12% and 6% faster on
+// one 64- or 128-token chunk over a 6 x 2640-token window than 2 and 4 waves
+// without key groups, double-buffered; 8 waves in 4 groups for 64 rows gain
+// nothing more).
+template <int NWR>
 struct Fwd8FewRows {
+  static constexpr int NW = 2 * NWR;
   static constexpr int RB = 1;
-  static constexpr int BN = NW == 2 ? 128 : 64;
+  static constexpr int BN = 64;
+  static constexpr int KG = 2;
 };
 
-template <int NW, int RB, int BN>
+template <int NW, int RB, int BN, int KG>
 hipError_t launch_fp8_tpl(FwdParams p, hipStream_t stream) {
-  constexpr int BM = 32 * RB * NW;
+  constexpr int BM = 32 * RB * (NW / KG);
   const long long grid = fwd_prepare(p, BM, true);
-  hipLaunchKernelGGL((attn_fwd_fp8_kernel<NW, RB, BN>), dim3((unsigned)grid), dim3(64 * NW), 0, stream, p);
+  hipLaunchKernelGGL((attn_fwd_fp8_kernel<NW, RB, BN, KG>), dim3((unsigned)grid), dim3(64 * NW), 0, stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_splits == 1) return e;
   return launch_combine(p, DH, stream);
@@ -539,22 +673,28 @@ hipError_t launch_fp8_tpl(FwdParams p, hipStream_t stream) {
 }  // namespace
 
 // Must agree with the dispatch in launch_fwd_fp8.  Resident workgroups per CU
-// from the runtime (fallbacks as built: two 2-wave workgroups of 64 KB LDS,
-// three 4-wave ones of about 170 registers, one 8-wave one).
+// from the runtime (fallback one: the few-row configurations hold 128 KB of
+// LDS, the 256-row one eight waves of about 230 registers).
 FwdChoice fwd8_choice(int Tq) {
-  static const int r64 = resident_workgroups(attn_fwd_fp8_kernel<2, Fwd8FewRows<2>::RB, Fwd8FewRows<2>::BN>, 128, 2);
-  static const int r128 = resident_workgroups(attn_fwd_fp8_kernel<4, Fwd8FewRows<4>::RB, Fwd8FewRows<4>::BN>, 256, 3);
-  static const int r256 = resident_workgroups(attn_fwd_fp8_kernel<Fwd8Cfg::NW, Fwd8Cfg::RB, Fwd8Cfg::BN>, 512, 1);
-  if (Tq <= 64) return {64, Fwd8FewRows<2>::BN, r64};
-  if (Tq <= 128) return {128, Fwd8FewRows<4>::BN, r128};
-  return {32 * Fwd8Cfg::RB * Fwd8Cfg::NW, Fwd8Cfg::BN, r256};
+  using F2 = Fwd8FewRows<2>;
+  using F4 = Fwd8FewRows<4>;
+  using C = Fwd8Cfg;
+  static const int r64 = resident_workgroups(attn_fwd_fp8_kernel<F2::NW, F2::RB, F2::BN, F2::KG>, 64 * F2::NW, 1);
+  static const int r128 = resident_workgroups(attn_fwd_fp8_kernel<F4::NW, F4::RB, F4::BN, F4::KG>, 64 * F4::NW, 1);
+  static const int r256 = resident_workgroups(attn_fwd_fp8_kernel<C::NW, C::RB, C::BN, C::KG>, 64 * C::NW, 1);
+  if (Tq <= 64) return {64, F2::BN * F2::KG, r64};
+  if (Tq <= 128) return {128, F4::BN * F4::KG, r128};
+  return {32 * C::RB * C::NW, C::BN, r256};
 }
 
 hipError_t launch_fwd_fp8(FwdParams p, hipStream_t stream) {
+  using F2 = Fwd8FewRows<2>;
+  using F4 = Fwd8FewRows<4>;
+  using C = Fwd8Cfg;
   const int bm = fwd8_choice(p.Tq).bm;
-  if (bm == 64) return launch_fp8_tpl<2, Fwd8FewRows<2>::RB, Fwd8FewRows<2>::BN>(p, stream);
-  if (bm == 128) return launch_fp8_tpl<4, Fwd8FewRows<4>::RB, Fwd8FewRows<4>::BN>(p, stream);
-  return launch_fp8_tpl<Fwd8Cfg::NW, Fwd8Cfg::RB, Fwd8Cfg::BN>(p, stream);
+  if (bm == 64) return launch_fp8_tpl<F2::NW, F2::RB, F2::BN, F2::KG>(p, stream);
+  if (bm == 128) return launch_fp8_tpl<F4::NW, F4::RB, F4::BN, F4::KG>(p, stream);
+  return launch_fp8_tpl<C::NW, C::RB, C::BN, C::KG>(p, stream);
 }
 
 hipError_t launch_rope_load_fp8(const uint8_t* k_slots, uint8_t* k_win, long long slot_bytes, int S, int first_slot,
