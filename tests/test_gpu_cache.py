@@ -217,10 +217,11 @@ def test_decode_shape_split_vs_oracle(mw, q_len):
 @pytest.mark.parametrize("split", [True, False])
 @pytest.mark.parametrize("mode", [0, 1])
 @pytest.mark.parametrize("B,H,L,S,n_commit,window,nq,qlen,sink_len", [
-    (1, 2, 250, 4, 5, 3, 1, 64, 0),     # 64 rows: four key groups of two row waves
+    (1, 2, 250, 4, 5, 3, 1, 64, 0),     # 64 rows: two key groups of two row waves, 64-key tiles four deep
+    (1, 2, 600, 4, 5, 3, 2, 30, 40),    # 60 rows in two queued chunks, sink: key ranges cross sink/window/queued
     (1, 3, 300, 4, 6, 3, 2, 50, 0),     # 100 rows in two queued chunks: two key groups of four
     (2, 1, 200, 5, 5, 4, 3, 40, 17),    # 120 rows, three queued chunks, sink of 17 tokens
-    (1, 1, 96, 3, 4, 2, 1, 7, 0),       # 7 rows, window shorter than one 128-key step
+    (1, 1, 96, 3, 4, 2, 1, 7, 0),       # 7 rows over 199 keys: fewer tiles than the pipeline holds, ragged end
     (1, 2, 130, 4, 6, -1, 2, 33, 5),    # all live chunks, ragged 66 rows, sink
     (1, 2, 200, 4, 5, 3, 3, 100, 9),    # 300 rows: three 128-row tiles of two key groups, sink
 ])

@@ -125,7 +125,9 @@ def run_fp8_case(mw, B, H, L, S, n_commit, window, nq, qlen, mode, split, sink_l
     (1, 2, 100, 3, 2, 0, 2, 70, 0),      # empty window: block-causal attention of the queued chunks
     (1, 1, 64, 8, 9, 7, 4, 33, 0),       # short queued chunks
     (1, 2, 120, 4, 4, 3, 3, 120, 40),    # with a sink
-    (1, 2, 128, 6, 6, 5, 1, 64, 0),      # one short queued chunk (64-row configuration)
+    (1, 2, 128, 6, 6, 5, 1, 64, 0),      # one short queued chunk (64-row configuration: two key groups)
+    (1, 1, 64, 8, 9, 7, 2, 30, 17),      # 60 rows in two queued chunks, sink of 17, wrapped ring (64-row)
+    (1, 2, 96, 3, 4, 2, 1, 7, 0),        # 7 rows over 199 keys: fewer tiles than the pipeline holds
     (1, 2, 128, 6, 6, 5, 1, 100, 32),    # 128-row configuration, ragged
     (1, 1, 300, 3, 1, 1, 3, 300, 0),     # isolated: one whole query tile, the others over 4 key ranges
 ])
