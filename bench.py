@@ -312,7 +312,10 @@ def fp8_stream(mw, torch, dev, st, reps=10):
     loads the window), and run the e4m3 cached attention.
     Also the cache-bound decode shapes (one queued chunk of 64 / 128 / 256 tokens
     over the full window, Infinity Cache flushed before each call; algorithmic
-    bytes = e4m3 window K and V + e4m3 Q, K_new, V_new + bf16 O), and the paper's
+    bytes = e4m3 window K and V + e4m3 Q, K_new, V_new + bf16 O), with nothing
+    pending and with one re-shift pending (the window keys rotated as they are
+    loaded: in the attention kernel's staging at 64 and 128 rows, in a separate
+    pass over the window at 256), and the paper's
     1B streaming shape (CFG batch 2, 8 in-flight 600-token chunks, 300-token sink)
     over 24 / 12 / 6 cached chunks.  HIP events on the launch stream."""
     import synth
@@ -376,35 +379,40 @@ def fp8_stream(mw, torch, dev, st, reps=10):
            "step_tflops": round(F / (step_ms * 1e-3) / 1e12, 2),
            "quantize_qkv_gbs": round(3 * n_el * 3 / (ph["quantize_qkv"] * 1e-3) / 1e9, 1),
            "append_gbs": round(2 * B * H * L * D * 3 / (ph["append"] * 1e-3) / 1e9, 1)}
-    # decode shapes, on a cache of the same window with no shift pending (pure streaming of the window)
-    cache = mw.KVCache(st.slots, B, H, L, D, device=dev, fp8=True, k_scale=sc, v_scale=sc)
-    for _ in range(W):
-        mw.mw_kvcache_append(cache, kc, vc)
+    # decode shapes: on a cache of the same window with no shift pending (pure
+    # streaming of the window), and after one re-shift (the state of a rollout
+    # between evictions: the window keys are rotated as the call loads them)
     flush = torch.ones(128 << 20, dtype=torch.float32, device=dev)
-    dec = []
-    for dq in (64, 128, 256):
-        q1, k1, v1 = (torch.randint(0, 120, (B, H, dq, D), dtype=torch.uint8, device=dev, generator=g)
-                      for _ in range(3))
-        o1 = torch.empty((B, H, dq, D), dtype=torch.bfloat16, device=dev)
-        ws1 = torch.empty(max(16, mw.mw_chunk_attn_cached_workspace_size(cache, 1, dq, W)), dtype=torch.uint8,
-                          device=dev)
-        run = lambda: mw.mw_chunk_attn_cached_fp8(q1, k1, v1, 1, dq, cache, sc, window=W, out=o1, workspace=ws1)
-        for _ in range(3):
-            run()
-        tot = 0.0
-        for _ in range(reps):
-            flush.sum()
-            e0 = ev()
-            run()
-            e1 = ev()
-            torch.cuda.synchronize()
-            tot += e0.elapsed_time(e1)
-        ms = tot / reps
-        nbytes = 2 * W * B * H * L * D + 3 * B * H * dq * D + B * H * dq * D * 2
-        gbs = nbytes / (ms * 1e-3) / 1e9
-        dec.append({"q_len": dq, "us": round(ms * 1e3, 2), "gbs": round(gbs, 1),
-                    "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4), "bytes": nbytes})
-    out["decode"] = dec
+    for key, shift in (("decode", 0), ("decode_shift_pending", 3)):
+        cache = mw.KVCache(st.slots, B, H, L, D, device=dev, fp8=True, k_scale=sc, v_scale=sc)
+        for _ in range(W):
+            mw.mw_kvcache_append(cache, kc, vc)
+        if shift:
+            mw.mw_kvcache_rope_shift(cache, shift, 0, 44)
+        dec = []
+        for dq in (64, 128, 256):
+            q1, k1, v1 = (torch.randint(0, 120, (B, H, dq, D), dtype=torch.uint8, device=dev, generator=g)
+                          for _ in range(3))
+            o1 = torch.empty((B, H, dq, D), dtype=torch.bfloat16, device=dev)
+            ws1 = torch.empty(max(16, mw.mw_chunk_attn_cached_workspace_size(cache, 1, dq, W)), dtype=torch.uint8,
+                              device=dev)
+            run = lambda: mw.mw_chunk_attn_cached_fp8(q1, k1, v1, 1, dq, cache, sc, window=W, out=o1, workspace=ws1)
+            for _ in range(3):
+                run()
+            tot = 0.0
+            for _ in range(reps):
+                flush.sum()
+                e0 = ev()
+                run()
+                e1 = ev()
+                torch.cuda.synchronize()
+                tot += e0.elapsed_time(e1)
+            ms = tot / reps
+            nbytes = 2 * W * B * H * L * D + 3 * B * H * dq * D + B * H * dq * D * 2
+            gbs = nbytes / (ms * 1e-3) / 1e9
+            dec.append({"q_len": dq, "us": round(ms * 1e3, 2), "gbs": round(gbs, 1),
+                        "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4), "bytes": nbytes})
+        out[key] = dec
     # the paper's 1B streaming shape
     ps = synth.PAPER_1B_STREAM
     B, H, D, L, nq = ps.B, ps.H, ps.D, ps.chunk_len, ps.n_queued

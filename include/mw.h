@@ -384,14 +384,18 @@ int mw_kvcache_init_fp8(mw_kvcache* c, void* k_slots, void* v_slots, int S, int 
  * mw_chunk_attn_cached_workspace_size on the e4m3 cache) as in
  * mw_chunk_attn_cached.
  * Rotation on load: when a window chunk has shifts pending (rope_total !=
- * its rope_at_commit), the call first writes every window chunk's keys,
- * rotated by -(rope_total - rope_at_commit[slot]) positions on the recorded
- * band, to the start of the workspace: each pair is decoded, rotated in fp32
- * (cos/sin of the angle computed in double), clamped to +-448 and rounded to
- * e4m3 (nearest even); the attention then reads the window keys from there
- * (the slots are not modified).  This needs window * B * H * L * 128 bytes of
- * workspace (rounded up to 256) before the key-range partials;
- * mw_chunk_attn_cached_workspace_size of an e4m3 cache always includes them.
+ * its rope_at_commit), every window chunk's keys are used rotated by
+ * -(rope_total - rope_at_commit[slot]) positions on the recorded band: each
+ * pair is decoded, rotated in fp32 (cos/sin of the angle computed in double),
+ * clamped to +-448 and rounded to e4m3 (nearest even); the slots are not
+ * modified.  Calls of at most 128 queued rows whose key ranges span few
+ * window chunks (chunks of at least 64 keys) rotate each K tile as the
+ * attention kernel stages it; the others first write the rotated window keys
+ * to the start of the workspace and the attention reads them from there.
+ * Both routes give the same bytes.  Either way the call reserves
+ * window * B * H * L * 128 bytes of workspace (rounded up to 256) before the
+ * key-range partials; mw_chunk_attn_cached_workspace_size of an e4m3 cache
+ * always includes them.
  * Errors: as mw_chunk_attn_cached, plus MW_EINVAL for a bf16 cache, q_scale
  * not finite and > 0, or shifts pending with a workspace too small for the
  * rotated window keys. */

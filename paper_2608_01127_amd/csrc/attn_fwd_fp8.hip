@@ -197,14 +197,67 @@ __device__ __forceinline__ void stage_kv8(const FwdParams& p, int bh, int k0, fp
   }, tid);
 }
 
+// RoPE re-shift of e4m3 keys when they are used (paper Sec. 3.5, re-indexing
+// the retained window after an eviction), shared by the separate rotation pass
+// and the rotation in the few-row kernel's staging so that both produce the
+// same bytes.  (cos, sin) of a rotation by -n positions of a pair whose
+// one-position rotation is (c1, s1): (c1 - i s1)^n by repeated squaring in
+// double (no device trigonometry; a relative error of a few 1e-15 for any n).
+__device__ __forceinline__ void rope_cos_sin(long long n, double c1, double s1, float& c, float& s) {
+  double br = c1, bi = n >= 0 ? -s1 : s1;
+  n = n >= 0 ? n : -n;
+  double cr = 1.0, ci = 0.0;
+  while (n != 0) {  // at most 63 rounds
+    if (n & 1) {
+      const double t = cr * br - ci * bi;
+      ci = cr * bi + ci * br;
+      cr = t;
+    }
+    const double t = br * br - bi * bi;
+    bi = 2.0 * br * bi;
+    br = t;
+    n >>= 1;
+  }
+  c = (float)cr;
+  s = (float)ci;
+}
+
+// One 16-byte piece of a key row (pairs 8 pc .. 8 pc + 7; the band's pairs are
+// p0 .. p0 + n_pairs - 1): each band pair is decoded, rotated in fp32 with the
+// cos/sin of its band index, clamped to +-448 and rounded back to e4m3
+// (nearest even, the quantizer's rounding).  The scale cancels: a rotation is
+// linear, so codes are rotated as values.
+__device__ __forceinline__ u32x4 rope_rotate_piece(u32x4 v, int pc, int p0, int n_pairs, const float* cosv,
+                                                   const float* sinv) {
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int pr = 8 * pc + q - p0;  // band pair index of this byte pair
+    if (pr < 0 || pr >= n_pairs) continue;
+    unsigned u = v[q / 2];
+    // (the half selectors of the conversions are immediates; the clamp is one
+    // median-of-three, equal to min(max(y, -448), 448) for the finite values
+    // a rotation of e4m3 codes gives)
+    const auto x = (q % 2) ? __builtin_amdgcn_cvt_pk_f32_fp8((int)u, true) : __builtin_amdgcn_cvt_pk_f32_fp8((int)u, false);
+    const float c = cosv[pr], sn = sinv[pr];
+    const float y0 = __builtin_amdgcn_fmed3f(fmaf(x[0], c, -x[1] * sn), -kE4m3Max, kE4m3Max);
+    const float y1 = __builtin_amdgcn_fmed3f(fmaf(x[0], sn, x[1] * c), -kE4m3Max, kE4m3Max);
+    u = (q % 2) ? (unsigned)__builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, (int)u, true)
+                : (unsigned)__builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, (int)u, false);
+    v[q / 2] = u;
+  }
+  return v;
+}
+
 constexpr float kRescaleThreshold8 = 8.f;  // probabilities stay <= 2^8 < 448
 
 // NW waves of RB 32-row query blocks in KG key groups of NW / KG row waves;
 // each step stages KG * BN keys (BN a multiple of 64) and group g works on
 // its BN-key slice; the groups merge (m, l, O) through LDS at the end.  With
-// key groups (the few-row configurations) the tiles stream four stages deep.
+// key groups (the few-row configurations) the tiles stream four stages deep,
+// and window keys with re-shifts pending are rotated in staging (rs).
 template <int NW, int RB, int BN, int KG>
-__global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd_fp8_kernel(FwdParams p) {
+__global__ __launch_bounds__(64 * NW, KG > 1 ? 1 : ((8 / NW) > 0 ? (8 / NW) : 1)) void attn_fwd_fp8_kernel(
+    FwdParams p, const RopeStage rs) {  // (key-group configurations hold 132 KB of LDS: one workgroup per CU)
   static_assert(NW % KG == 0, "waves split evenly into key groups");
   constexpr int NWR = NW / KG;
   constexpr int BM = 32 * RB * NWR, NT = 64 * NW, KB = BN / 32, KP = BN / 64, BK = BN * KG;
@@ -383,6 +436,52 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
       const fp8_t* src = qg + (long long)min(q0 + row, p.Tq - 1) * DH + 16 * ls;
       dma_lds_16(src, lds_addr(qs) + it * NT * 16 + wave_stage_off(tid));
     }
+    // Rotation in staging: the window chunks this workgroup's key range spans
+    // (at most kRopeStageChunks, chunks of at least BK / 2 keys, as the host
+    // checks) get a cos/sin table of their band pairs in LDS, computed once the
+    // first tiles are in flight.
+    static_assert(NT % BK == 0 && (BK & (BK - 1)) == 0, "rotation maps a thread to one row of the tile");
+    __shared__ float rtab[kRopeStageChunks][2][64];
+    const bool rot = rs.n_pairs > 0;
+    int w_lo = 0, nwc = 0;
+    if (rot) {
+      const int a0 = max(kbeg, p.sink_len), a1 = min(((kend + BK - 1) / BK) * BK, p.wL);
+      if (a0 < a1) {
+        w_lo = (a0 - p.sink_len) / p.L;
+        nwc = min((a1 - 1 - p.sink_len) / p.L - w_lo + 1, kRopeStageChunks);
+      }
+    }
+    // window rows of the staged tile [k0, k0 + BK): their band pieces, rotated
+    // in place, thread t on row t mod BK (a uniform test says whether the tile
+    // has any); a tile spans at most three window chunks, whose first rows are
+    // found once per tile
+    auto rotate = [&](const int k0, const int buf) {
+      const int r0 = max(p.sink_len - k0, 0), r1 = min(p.wL - k0, BK);
+      if (r0 >= r1 || nwc == 0) return false;
+      const int kw = k0 + r0 - p.sink_len;  // window index of row r0
+      const int wa = kw / p.L;
+      const int b1 = r0 + (wa + 1) * p.L - kw, b2 = b1 + p.L;  // first rows of the next two chunks
+      const int pc0 = rs.dim_offset >> 4, pc1 = (rs.dim_offset + 2 * rs.n_pairs - 1) >> 4;
+      const int row = tid & (BK - 1);
+      if (row >= r0 && row < r1) {
+        const int wi = min(max(wa - w_lo + (row >= b1) + (row >= b2), 0), nwc - 1);
+        const int p0 = rs.dim_offset >> 1;
+        fp8_t* kt = Ks[buf];
+        // the thread's first two pieces with both reads in flight, then any more
+        constexpr int G = NT / BK;
+        const int pa = pc0 + tid / BK, pb = pa + G;
+        u32x4* aa = reinterpret_cast<u32x4*>(kt + Tile8::off(row, 16 * min(pa, 7)));
+        u32x4* ab = reinterpret_cast<u32x4*>(kt + Tile8::off(row, 16 * min(pb, 7)));
+        const u32x4 va = *aa, vb = *ab;
+        if (pa <= pc1) *aa = rope_rotate_piece(va, pa, p0, rs.n_pairs, rtab[wi][0], rtab[wi][1]);
+        if (pb <= pc1) *ab = rope_rotate_piece(vb, pb, p0, rs.n_pairs, rtab[wi][0], rtab[wi][1]);
+        for (int pc = pb + G; pc <= pc1; pc += G) {
+          u32x4* a = reinterpret_cast<u32x4*>(kt + Tile8::off(row, 16 * pc));
+          *a = rope_rotate_piece(*a, pc, p0, rs.n_pairs, rtab[wi][0], rtab[wi][1]);
+        }
+      }
+      return true;
+    };
     int ki = kc, ib = 0, ahead = 0;  // next tile to issue, its buffer, tiles issued and not yet used
 #pragma unroll
     for (int s = 0; s < NSTG - 1; ++s) {
@@ -391,6 +490,21 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
         ki = advance(ki);
         ib = ib + 1 == NSTG ? 0 : ib + 1;
         ++ahead;
+      }
+    }
+    if (rot) {
+      // lane i takes pair i's one-position rotation, read with scalar loads
+      // (a vector load here would be the only one the compiler tracks, and it
+      // would wait for the tiles in flight as well); wave w the chunks w, w + NW, ...
+      double c1 = 1.0, s1 = 0.0;
+      for (int i = 0; i < rs.n_pairs; ++i) {
+        const double ci = rs.a.c1[i], si = rs.a.s1[i];
+        c1 = lane == i ? ci : c1;
+        s1 = lane == i ? si : s1;
+      }
+      for (int wi = __builtin_amdgcn_readfirstlane(wave); wi < nwc; wi += NW) {
+        const long long n = rs.a.pend[w_lo + wi];
+        if (lane < rs.n_pairs) rope_cos_sin(n, c1, s1, rtab[wi][0][lane], rtab[wi][1][lane]);
       }
     }
     wait_vmem_upto<P, NSTG - 1>(ahead);  // the Q loads
@@ -412,6 +526,7 @@ __global__ __launch_bounds__(64 * NW, (8 / NW) > 0 ? (8 / NW) : 1) void attn_fwd
           ib = ib + 1 == NSTG ? 0 : ib + 1;
           ++ahead;
         }
+        if (rot && rotate(kc, cb)) __syncthreads();  // rotated keys visible to every wave
         slice(masked, kc, cb);
         --ahead;
         cb = cb + 1 == NSTG ? 0 : cb + 1;
@@ -588,50 +703,16 @@ __global__ __launch_bounds__(256) void rope_load_fp8_kernel(const fp8_t* __restr
                                                             RopeLoadArgs a) {
   __shared__ float cs[2][64];
   const int w = blockIdx.y;
-  if ((int)threadIdx.x < n_pairs) {
-    // (cos, sin) of -pend * freq = (c1 - i s1)^pend
-    long long n = a.pend[w];
-    double br = a.c1[threadIdx.x], bi = n >= 0 ? -a.s1[threadIdx.x] : a.s1[threadIdx.x];
-    n = n >= 0 ? n : -n;
-    double cr = 1.0, ci = 0.0;
-    while (n != 0) {  // at most 63 rounds
-      if (n & 1) {
-        const double t = cr * br - ci * bi;
-        ci = cr * bi + ci * br;
-        cr = t;
-      }
-      const double t = br * br - bi * bi;
-      bi = 2.0 * br * bi;
-      br = t;
-      n >>= 1;
-    }
-    cs[0][threadIdx.x] = (float)cr;
-    cs[1][threadIdx.x] = (float)ci;
-  }
+  if ((int)threadIdx.x < n_pairs) rope_cos_sin(a.pend[w], a.c1[threadIdx.x], a.s1[threadIdx.x], cs[0][threadIdx.x], cs[1][threadIdx.x]);
   __syncthreads();
   // one thread per 16-byte piece (8 pairs) of a key row
   const long long j = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= pieces) return;
   const int slot = first_slot + w < S ? first_slot + w : first_slot + w - S;
-  u32x4 v = *reinterpret_cast<const u32x4*>(k_slots + (long long)slot * slot_bytes + j * 16);
-  const int pc = (int)(j % (DH / 16));  // piece of the row: pairs 8 pc .. 8 pc + 7
-  const int p0 = dim_offset / 2;         // first pair of the band (dim_offset is even)
-#pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const int pr = 8 * pc + q - p0;  // band pair index of this byte pair
-    if (pr < 0 || pr >= n_pairs) continue;
-    unsigned u = v[q / 2];
-    // (the byte and half selectors of the conversions are immediates)
-    const float x0 = (q % 2) ? __builtin_amdgcn_cvt_f32_fp8(u, 2) : __builtin_amdgcn_cvt_f32_fp8(u, 0);
-    const float x1 = (q % 2) ? __builtin_amdgcn_cvt_f32_fp8(u, 3) : __builtin_amdgcn_cvt_f32_fp8(u, 1);
-    const float c = cs[0][pr], sn = cs[1][pr];
-    const float y0 = fminf(fmaxf(fmaf(x0, c, -x1 * sn), -kE4m3Max), kE4m3Max);
-    const float y1 = fminf(fmaxf(fmaf(x0, sn, x1 * c), -kE4m3Max), kE4m3Max);
-    u = (q % 2) ? (unsigned)__builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, (int)u, true)
-                : (unsigned)__builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, (int)u, false);
-    v[q / 2] = u;
-  }
-  *reinterpret_cast<u32x4*>(k_win + (long long)w * slot_bytes + j * 16) = v;
+  const u32x4 v = *reinterpret_cast<const u32x4*>(k_slots + (long long)slot * slot_bytes + j * 16);
+  const int pc = (int)(j % (DH / 16));  // piece of the row
+  *reinterpret_cast<u32x4*>(k_win + (long long)w * slot_bytes + j * 16) =
+      rope_rotate_piece(v, pc, dim_offset / 2, n_pairs, cs[0], cs[1]);
 }
 
 // Tile configuration: 8 waves of one 32-row block (256 queries; one workgroup
@@ -661,10 +742,10 @@ struct Fwd8FewRows {
 };
 
 template <int NW, int RB, int BN, int KG>
-hipError_t launch_fp8_tpl(FwdParams p, hipStream_t stream) {
+hipError_t launch_fp8_tpl(FwdParams p, const RopeStage& rs, hipStream_t stream) {
   constexpr int BM = 32 * RB * (NW / KG);
   const long long grid = fwd_prepare(p, BM, true);
-  hipLaunchKernelGGL((attn_fwd_fp8_kernel<NW, RB, BN, KG>), dim3((unsigned)grid), dim3(64 * NW), 0, stream, p);
+  hipLaunchKernelGGL((attn_fwd_fp8_kernel<NW, RB, BN, KG>), dim3((unsigned)grid), dim3(64 * NW), 0, stream, p, rs);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_splits == 1) return e;
   return launch_combine(p, DH, stream);
@@ -687,14 +768,28 @@ FwdChoice fwd8_choice(int Tq) {
   return {32 * C::RB * C::NW, C::BN, r256};
 }
 
-hipError_t launch_fwd_fp8(FwdParams p, hipStream_t stream) {
+bool fwd8_rotates_in_staging(int Tq, int Tk, int L, const SplitPlan& sp) {
+  const FwdChoice ch = fwd8_choice(Tq);
+  if (ch.bm > 128 || L < 1 || Tk < 1) return false;  // the 256-row configuration rotates in a separate pass
+  if (2 * L < ch.bk) return false;  // a staged tile spans at most three window chunks
+  const long long ntiles = (Tk + ch.bk - 1) / ch.bk;
+  const long long ns = std::max(sp.n_splits, 1);
+  // tiles of one workgroup's key range (whole tiles run every key tile)
+  const long long tiles = (sp.n_whole > 0 || ns == 1) ? ntiles : (ntiles + ns - 1) / ns;
+  return tiles * ch.bk / L + 2 <= kRopeStageChunks;
+}
+
+hipError_t launch_fwd_fp8(FwdParams p, const RopeStage& rs, hipStream_t stream) {
   using F2 = Fwd8FewRows<2>;
   using F4 = Fwd8FewRows<4>;
   using C = Fwd8Cfg;
   const int bm = fwd8_choice(p.Tq).bm;
-  if (bm == 64) return launch_fp8_tpl<F2::NW, F2::RB, F2::BN, F2::KG>(p, stream);
-  if (bm == 128) return launch_fp8_tpl<F4::NW, F4::RB, F4::BN, F4::KG>(p, stream);
-  return launch_fp8_tpl<C::NW, C::RB, C::BN, C::KG>(p, stream);
+  if (rs.n_pairs > 0 && (bm > 128 || rs.n_pairs > 64 || rs.dim_offset < 0 || rs.dim_offset % 2 != 0 ||
+                         rs.dim_offset + 2 * rs.n_pairs > DH))
+    return hipErrorInvalidValue;
+  if (bm == 64) return launch_fp8_tpl<F2::NW, F2::RB, F2::BN, F2::KG>(p, rs, stream);
+  if (bm == 128) return launch_fp8_tpl<F4::NW, F4::RB, F4::BN, F4::KG>(p, rs, stream);
+  return launch_fp8_tpl<C::NW, C::RB, C::BN, C::KG>(p, rs, stream);
 }
 
 hipError_t launch_rope_load_fp8(const uint8_t* k_slots, uint8_t* k_win, long long slot_bytes, int S, int first_slot,

@@ -741,41 +741,53 @@ int mw_chunk_attn_cached_fp8(const void* q8, const void* k8_new, const void* v8_
   p.slot_stride = (long long)c->B * c->H * c->L * c->D;  // bytes = elements
   p.S = c->S;
   p.first_slot = (int)((c->head - w) % c->S);
-  // rotation on load: window keys with shifts pending are rotated into the
-  // start of the workspace, and the attention reads them from there
+  // Rotation on load of window keys with shifts pending: the start of the
+  // workspace is reserved for the rotated window (the plan never depends on
+  // which of the two routes runs).  Few-row calls rotate each staged K tile
+  // inside the attention kernel; the others rotate the window into the
+  // reserved bytes first and the attention reads the keys from there.
   long long pend[MW_MAX_WINDOW];
   char* ws = static_cast<char*>(workspace);
   size_t ws_bytes = workspace != nullptr ? workspace_bytes : 0;
-  if (rope_pending(c, w, pend)) {
+  const bool pending = rope_pending(c, w, pend);
+  uint8_t* k_win = nullptr;
+  if (pending) {
     const size_t kw = rope_window_bytes(c, w);
     if (ws == nullptr || ws_bytes < kw)
       return fail(MW_EINVAL, "%s: shifts are pending on the window; its rotated keys need %zu bytes of workspace, got %zu",
                   fn, kw, ws_bytes);
-    mw::RopeLoadArgs a{};
-    const int np = c->rope_count / 2;
-    for (long long i = 0; i < w; ++i) a.pend[i] = pend[i];
-    for (int i = 0; i < np; ++i) {
-      const double freq = std::pow((double)c->rope_theta, -2.0 * i / c->rope_count);
-      a.c1[i] = std::cos(freq);
-      a.s1[i] = std::sin(freq);
-    }
-    hipError_t e = mw::launch_rope_load_fp8(static_cast<const uint8_t*>(c->k_slots), reinterpret_cast<uint8_t*>(ws),
-                                            p.slot_stride, c->S, p.first_slot, (int)w,
-                                            (long long)c->B * c->H * c->L, c->rope_offset, np, a,
-                                            static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return hip_status(fn, e);
-    p.k_win = reinterpret_cast<const uint8_t*>(ws);
+    k_win = reinterpret_cast<uint8_t*>(ws);
     ws += kw;
     ws_bytes -= kw;
   }
   const mw::SplitPlan sp = mw::fwd_plan_splits(mw::fwd8_choice(p.Tq), kFp8Flops, 1, c->D, p.BH, p.Tq, p.Tk, q_len,
                                                flags == MW_QUEUED_ISOLATED, ws_bytes);
+  mw::RopeStage rs{};  // n_pairs = 0: nothing rotated in staging
+  if (pending) {
+    const int np = c->rope_count / 2;
+    for (long long i = 0; i < w; ++i) rs.a.pend[i] = pend[i];
+    for (int i = 0; i < np; ++i) {
+      const double freq = std::pow((double)c->rope_theta, -2.0 * i / c->rope_count);
+      rs.a.c1[i] = std::cos(freq);
+      rs.a.s1[i] = std::sin(freq);
+    }
+    if (mw::fwd8_rotates_in_staging(p.Tq, p.Tk, c->L, sp)) {
+      rs.n_pairs = np;
+      rs.dim_offset = c->rope_offset;
+    } else {
+      hipError_t e = mw::launch_rope_load_fp8(static_cast<const uint8_t*>(c->k_slots), k_win, p.slot_stride, c->S,
+                                              p.first_slot, (int)w, (long long)c->B * c->H * c->L, c->rope_offset, np,
+                                              rs.a, static_cast<hipStream_t>(stream));
+      if (e != hipSuccess) return hip_status(fn, e);
+      p.k_win = k_win;
+    }
+  }
   p.n_splits = sp.n_splits;
   p.n_whole = sp.n_whole;
   p.part = reinterpret_cast<float*>(ws_bytes > 0 ? ws : nullptr);
   p.so = so;
   p.o_scale = c->v_scale;
-  return hip_status(fn, mw::launch_fwd_fp8(p, static_cast<hipStream_t>(stream)));
+  return hip_status(fn, mw::launch_fwd_fp8(p, rs, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

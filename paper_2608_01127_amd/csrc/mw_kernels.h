@@ -117,7 +117,6 @@ FwdChoice fwd_choice(int D, bool cached, int Tq);
 // fp8 (e4m3) cached attention at D = 128: its tile configuration and launcher
 // (FwdParams as described above), and the merge of split partials (D = 128).
 FwdChoice fwd8_choice(int Tq);
-hipError_t launch_fwd_fp8(FwdParams p, hipStream_t stream);
 hipError_t launch_combine(const FwdParams& p, int D, hipStream_t stream);
 // bf16 view -> contiguous e4m3, code = RNE(clamp(x * inv_scale, +-448)); up to
 // two jobs of the same shape in one launch.
@@ -182,6 +181,24 @@ struct RopeLoadArgs {
   double c1[64];
   double s1[64];
 };
+// The same rotation done inside the e4m3 attention kernel's staging, on each
+// staged K tile in LDS (the few-row configurations only): pend[w] for the
+// window chunks of the call, band as above; n_pairs = 0 rotates nothing.
+struct RopeStage {
+  RopeLoadArgs a;
+  int n_pairs;
+  int dim_offset;
+};
+// Window chunks one workgroup of the in-staging rotation can span (their
+// cos/sin tables live in LDS).
+constexpr int kRopeStageChunks = 8;
+// Whether a call (Tq queued rows over Tk keys, window chunks of L keys, split
+// plan sp) runs a few-row configuration whose every workgroup's key range
+// spans at most kRopeStageChunks window chunks, with chunks of at least half
+// a staged tile, so that it can rotate its window keys in staging instead of
+// in a separate pass.
+bool fwd8_rotates_in_staging(int Tq, int Tk, int L, const SplitPlan& sp);
+hipError_t launch_fwd_fp8(FwdParams p, const RopeStage& rs, hipStream_t stream);
 hipError_t launch_rope_load_fp8(const uint8_t* k_slots, uint8_t* k_win, long long slot_bytes, int S, int first_slot,
                                 int n_window, long long rows_per_slot, int dim_offset, int n_pairs,
                                 const RopeLoadArgs& args, hipStream_t stream);

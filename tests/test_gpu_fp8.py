@@ -375,3 +375,95 @@ def test_fp8_rope_reshift_on_load_sink_partial_window(mw, q_len, window):
                                      [dq(hist[c][1], vs) for c in win], 1, q_len, sink_k=dq(sk, ks),
                                      sink_v=dq(sv, vs))
     assert_close(f"o q_len={q_len} window={window}", to_f64(o), ro, FP8_MAX_ABS, FP8_MEAN_ABS)
+
+
+def _rotated_window_rollout(mw, L, seed):
+    """An e4m3 ring (B1 H2 D128, 5 slots, window 4) whose window chunks carry different pending
+    re-shifts (3 per eviction, plus one extra shift of 1 midway), with a 40-token sink."""
+    B, H, D, S = 1, 2, 128, 5
+    ks, vs = 0.011, 0.012
+    cache = mw.KVCache(S, B, H, L, D, fp8=True, k_scale=ks, v_scale=vs)
+    sk, sv = (mw.mw_quantize_fp8(to_gpu(synth.normal_bf16((B, H, 40, D), seed + i)), sc) for i, sc in ((0, ks), (1, vs)))
+    cache.set_sink(sk, sv)
+    for t in range(7):
+        kb, vb = (synth.normal_bf16((B, H, L, D), seed + 10 + 2 * t + j) for j in range(2))
+        if cache.live == S:
+            mw.mw_kvcache_evict(cache, 1)
+            mw.mw_kvcache_rope_shift(cache, 3, 0, 44)
+        if t == 4:
+            mw.mw_kvcache_rope_shift(cache, 1, 0, 44)
+        mw.mw_kvcache_append(cache, to_gpu(kb), to_gpu(vb))
+    return cache, (sk, sv), (B, H, D, S, ks, vs)
+
+
+def test_fp8_rotation_in_staging_bit_identical_to_separate_pass(mw):
+    """Few-row e4m3 calls with re-shifts pending rotate each staged K tile inside the attention
+    kernel; calls of more rows rotate the window in a separate pass into the start of the
+    workspace.  Both run the same arithmetic, so: a 256-row call leaves the rotated window in its
+    workspace; a second cache holding those rotated codes in its slots, with nothing pending,
+    gives a 64-row call bit for bit the output the shifted cache gives it; and the shifted
+    cache's 64-row call (split into key ranges) leaves the workspace's rotated-window bytes
+    untouched, i.e. no separate pass ran."""
+    import torch
+    L, W = 256, 4
+    A, (sk, sv), (B, H, D, S, ks, vs) = _rotated_window_rollout(mw, L, seed=9500)
+    pend = [A.desc.rope_total - A.desc.rope_at_commit[A.slot_of(c)] for c in range(A.desc.head - W, A.desc.head)]
+    assert len(set(pend)) > 1 and max(pend) > 0  # (the newest chunk has nothing pending: identity rotation)
+    qs = 0.0105
+    kw = W * B * H * L * D
+    q2, k2, v2 = (mw.mw_quantize_fp8(to_gpu(synth.normal_bf16((B, H, 256, D), 9560 + i)), qs) for i in range(3))
+    ws = torch.full((mw.mw_chunk_attn_cached_workspace_size(A, 1, 256, W),), 0xAB, dtype=torch.uint8, device="cuda")
+    mw.mw_chunk_attn_cached_fp8(q2, k2, v2, 1, 256, A, qs, window=W, workspace=ws)
+    sync()
+    rotated = ws[:kw].view(W, B, H, L, D).clone()
+    assert not bool((rotated == 0xAB).all())
+    Bc = mw.KVCache(S, B, H, L, D, fp8=True, k_scale=ks, v_scale=vs)
+    for t in range(W):
+        mw.mw_kvcache_append(Bc, to_gpu(synth.normal_bf16((B, H, L, D), 9570 + t)),
+                             to_gpu(synth.normal_bf16((B, H, L, D), 9580 + t)))
+    for i, c in enumerate(range(A.desc.head - W, A.desc.head)):
+        Bc.k_slots[Bc.slot_of(i)].copy_(rotated[i])
+        Bc.v_slots[Bc.slot_of(i)].copy_(A.v_slots[A.slot_of(c)])
+    Bc.set_sink(sk, sv)
+    q8, k8, v8 = (mw.mw_quantize_fp8(to_gpu(synth.normal_bf16((B, H, 64, D), 9590 + i)), qs) for i in range(3))
+    ns, _ = mw.mw_chunk_attn_cached_plan(A, 1, 64, W)
+    print(f"[case] fp8 rotation in staging vs separate pass, pend={pend}, splits={ns}", flush=True)
+    assert ns > 1
+    ws_a = torch.full((mw.mw_chunk_attn_cached_workspace_size(A, 1, 64, W),), 0xAB, dtype=torch.uint8, device="cuda")
+    oa, la = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, 1, 64, A, qs, window=W, workspace=ws_a, want_lse=True)
+    ob, lb = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, 1, 64, Bc, qs, window=W, want_lse=True)
+    sync()
+    assert bool((ws_a[:kw] == 0xAB).all())
+    assert bits_equal(oa, ob)
+    assert torch.equal(la, lb)
+
+
+def test_fp8_rotation_separate_pass_when_chunks_are_short(mw):
+    """With 32-token chunks a 64-row call's key range spans more window chunks than the kernel's
+    cos/sin tables hold, so the window is rotated in the separate pass (the workspace's
+    rotated-window bytes are written); the output against the oracle over the window keys
+    rotated by their pending shifts and rounded once, fp8 bar."""
+    import torch
+    L, W = 32, 4
+    A, (sk, sv), (B, H, D, S, ks, vs) = _rotated_window_rollout(mw, L, seed=9600)
+    qs = 0.0105
+    kw = W * B * H * L * D
+    inp = {n: synth.normal_bf16((B, H, 64, D), 9690 + i) for i, n in enumerate("qkv")}
+    q8, k8, v8 = (mw.mw_quantize_fp8(to_gpu(inp[n]), sc) for n, sc in (("q", qs), ("k", ks), ("v", vs)))
+    ws = torch.full((mw.mw_chunk_attn_cached_workspace_size(A, 1, 64, W),), 0xAB, dtype=torch.uint8, device="cuda")
+    print(f"[case] fp8 rotation, short chunks L={L}", flush=True)
+    o, _ = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, 1, 64, A, qs, window=W, workspace=ws)
+    sync()
+    assert not bool((ws[:kw] == 0xAB).all())
+    win = list(range(A.desc.head - W, A.desc.head))
+    dq = lambda b, sc: oracle.dequantize_fp8(codes(b, sc), sc)
+    win_k = []
+    for c in win:
+        kcodes = u8(A.k_slots[A.slot_of(c)])
+        vals = oracle.dequantize_fp8(kcodes, 1.0)
+        rot = oracle.rope_rotate(vals, -float(A.desc.rope_total - A.desc.rope_at_commit[A.slot_of(c)]), 0, 44)
+        win_k.append(oracle.dequantize_fp8(oracle.quantize_fp8(rot.astype(np.float32), 1.0), ks))
+    win_v = [oracle.dequantize_fp8(u8(A.v_slots[A.slot_of(c)]), vs) for c in win]
+    ro, _ = oracle.cached_chunk_attn(dq(inp["q"], qs), dq(inp["k"], ks), dq(inp["v"], vs), win_k, win_v, 1, 64,
+                                     sink_k=oracle.dequantize_fp8(u8(sk), ks), sink_v=oracle.dequantize_fp8(u8(sv), vs))
+    assert_close(f"o L={L}", to_f64(o), ro, FP8_MAX_ABS, FP8_MEAN_ABS)
