@@ -438,23 +438,26 @@ def test_fp8_rotation_in_staging_bit_identical_to_separate_pass(mw):
     assert torch.equal(la, lb)
 
 
-def test_fp8_rotation_separate_pass_when_chunks_are_short(mw):
-    """With 32-token chunks a 64-row call's key range spans more window chunks than the kernel's
-    cos/sin tables hold, so the window is rotated in the separate pass (the workspace's
-    rotated-window bytes are written); the output against the oracle over the window keys
-    rotated by their pending shifts and rounded once, fp8 bar."""
+@pytest.mark.parametrize("L,in_staging", [(32, False), (80, True)])
+def test_fp8_rotation_route_vs_oracle(mw, L, in_staging):
+    """A 64-row call over a re-shifted window of short chunks.  With 32-token chunks its key range
+    spans more window chunks than the kernel's cos/sin tables hold, so the window is rotated in
+    the separate pass (the workspace's rotated-window bytes are written); with 80-token chunks it
+    rotates in staging, where a 128-key tile spans up to three chunks (the workspace bytes stay
+    untouched).  The output against the oracle over the window keys rotated by their pending
+    shifts and rounded once, fp8 bar."""
     import torch
-    L, W = 32, 4
-    A, (sk, sv), (B, H, D, S, ks, vs) = _rotated_window_rollout(mw, L, seed=9600)
+    W = 4
+    A, (sk, sv), (B, H, D, S, ks, vs) = _rotated_window_rollout(mw, L, seed=9600 + L)
     qs = 0.0105
     kw = W * B * H * L * D
     inp = {n: synth.normal_bf16((B, H, 64, D), 9690 + i) for i, n in enumerate("qkv")}
     q8, k8, v8 = (mw.mw_quantize_fp8(to_gpu(inp[n]), sc) for n, sc in (("q", qs), ("k", ks), ("v", vs)))
     ws = torch.full((mw.mw_chunk_attn_cached_workspace_size(A, 1, 64, W),), 0xAB, dtype=torch.uint8, device="cuda")
-    print(f"[case] fp8 rotation, short chunks L={L}", flush=True)
+    print(f"[case] fp8 rotation route L={L} in_staging={in_staging}", flush=True)
     o, _ = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, 1, 64, A, qs, window=W, workspace=ws)
     sync()
-    assert not bool((ws[:kw] == 0xAB).all())
+    assert bool((ws[:kw] == 0xAB).all()) == in_staging
     win = list(range(A.desc.head - W, A.desc.head))
     dq = lambda b, sc: oracle.dequantize_fp8(codes(b, sc), sc)
     win_k = []
