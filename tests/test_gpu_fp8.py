@@ -235,14 +235,15 @@ def test_fp8_stream_config_sampled_heads(mw, mode):
         assert_close(f"lse b{b} h{h}", gl[b, h], rl[b, h], max_abs=2e-3, mean_abs=2e-4)
 
 
-@pytest.mark.parametrize("q_len", [64, 256])
-def test_fp8_decode_full_window(mw, q_len):
+@pytest.mark.parametrize("q_len,shift", [(64, 0), (256, 0), (64, 3), (256, 3)])
+def test_fp8_decode_full_window(mw, q_len, shift):
     """The e4m3 cache-bound decode shapes the benchmark times: one queued chunk of q_len tokens
     over the full window of the streaming shape (6 committed 2640-token chunks of an 8-slot ring,
-    B1 H16 D128), with the call's own key-range split; every head against the oracle on the
-    dequantized codes."""
+    B1 H16 D128), with the call's own key-range split, with nothing pending and after one
+    re-shift of 3 positions (rotated in staging at 64 rows, in the separate pass at 256); every
+    head against the oracle on the dequantized codes (the window keys rotated and rounded once)."""
     s = synth.STREAM
-    print(f"[case] fp8 decode q_len={q_len} over {s.window} x {s.chunk_len}", flush=True)
+    print(f"[case] fp8 decode q_len={q_len} shift={shift} over {s.window} x {s.chunk_len}", flush=True)
     ks, vs, qs = 0.011, 0.012, 0.0105
     cache = mw.KVCache(s.slots, s.B, s.H, s.chunk_len, s.D, fp8=True, k_scale=ks, v_scale=vs)
     hist = [(synth.normal_bf16((s.B, s.H, s.chunk_len, s.D), 9700 + 2 * i),
@@ -252,6 +253,8 @@ def test_fp8_decode_full_window(mw, q_len):
             mw.mw_kvcache_evict(cache, 1)
         mw.mw_kvcache_append(cache, to_gpu(kc), to_gpu(vc))
     mw.mw_kvcache_evict(cache, cache.live - s.window)
+    if shift:
+        mw.mw_kvcache_rope_shift(cache, shift, 0, 44)
     ns, _ = mw.mw_chunk_attn_cached_plan(cache, 1, q_len, s.window)
     inp = {n: synth.normal_bf16((s.B, s.H, q_len, s.D), 9690 + i) for i, n in enumerate("qkv")}
     q8 = mw.mw_quantize_fp8(to_gpu(inp["q"]), qs)
@@ -261,9 +264,15 @@ def test_fp8_decode_full_window(mw, q_len):
     sync()
     dq = lambda b, sc: oracle.dequantize_fp8(codes(b, sc), sc)
     win = hist[-s.window:]
+    if shift:  # rotate the committed code values by -shift, round to e4m3 once, scale
+        win_k = [oracle.dequantize_fp8(oracle.quantize_fp8(
+            oracle.rope_rotate(oracle.dequantize_fp8(codes(c[0], ks), 1.0), -float(shift), 0, 44).astype(np.float32),
+            1.0), ks) for c in win]
+    else:
+        win_k = [dq(c[0], ks) for c in win]
     ro, rl = oracle.cached_chunk_attn(dq(inp["q"], qs), dq(inp["k"], ks), dq(inp["v"], vs),
-                                      [dq(c[0], ks) for c in win], [dq(c[1], vs) for c in win], 1, q_len)
-    assert_close(f"o q_len={q_len} ({ns} key ranges)", to_f64(o), ro, FP8_MAX_ABS, FP8_MEAN_ABS)
+                                      win_k, [dq(c[1], vs) for c in win], 1, q_len)
+    assert_close(f"o q_len={q_len} shift={shift} ({ns} key ranges)", to_f64(o), ro, FP8_MAX_ABS, FP8_MEAN_ABS)
     assert_close("lse", to_f64(lse), rl, max_abs=2e-3, mean_abs=2e-4)
 
 
