@@ -495,7 +495,7 @@ def synth_name(st, steps):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1 (the hot path is "
+        print(json.dumps({"error": "the benchmark runs on exactly one GPU; --gpus must be 1 (the hot path is "
                                    "measured on one GPU's share; sharding is a design note only)"}))
         sys.exit(2)
     import numpy as np
