@@ -479,3 +479,67 @@ def test_fp8_rotation_route_vs_oracle(mw, L, in_staging):
     ro, _ = oracle.cached_chunk_attn(dq(inp["q"], qs), dq(inp["k"], ks), dq(inp["v"], vs), win_k, win_v, 1, 64,
                                      sink_k=oracle.dequantize_fp8(u8(sk), ks), sink_v=oracle.dequantize_fp8(u8(sv), vs))
     assert_close(f"o L={L}", to_f64(o), ro, FP8_MAX_ABS, FP8_MEAN_ABS)
+
+
+@pytest.mark.parametrize("L,W,sink_len,nq,qlen,mode", [
+    (256, 4, 0, 1, 1, 0),        # one queued row, no sink
+    (80, 5, 17, 1, 64, 0),       # 80-token chunks: a 128-key tile spans up to three chunks
+    (256, 3, 300, 1, 33, 0),     # a sink longer than two tiles, ragged 33 rows
+    (128, 4, 40, 2, 50, 1),      # two queued chunks (100 rows, 128-row configuration), isolated
+    (100, 6, 5, 1, 128, 0),      # 128 rows, the whole ring's window after wrapping
+])
+def test_fp8_rotation_in_staging_sweep(mw, L, W, sink_len, nq, qlen, mode):
+    """Rotation in staging against the separate pass, bit for bit, over shapes that move the
+    window's chunk edges, the sink and the ragged end around the staged tiles: the separate pass
+    of a 256-row call on the shifted cache writes the rotated window into its workspace; a second
+    cache holds those codes with nothing pending; a few-row call gives both caches the same output
+    and LSE, and leaves the shifted call's workspace bytes of the rotated window untouched."""
+    import torch
+    B, H, D = 1, 2, 128
+    S = W + 1
+    ks, vs, qs = 0.011, 0.012, 0.0105
+    seed = 9800 + L + 7 * W + sink_len + qlen
+    A = mw.KVCache(S, B, H, L, D, fp8=True, k_scale=ks, v_scale=vs)
+    sink = None
+    if sink_len:
+        sink = tuple(mw.mw_quantize_fp8(to_gpu(synth.normal_bf16((B, H, sink_len, D), seed + i)), sc)
+                     for i, sc in ((0, ks), (1, vs)))
+        A.set_sink(*sink)
+    for t in range(W + 3):  # wraps the ring; each eviction re-shifts by 3, one extra shift of 2 midway
+        if A.live == S:
+            mw.mw_kvcache_evict(A, 1)
+            mw.mw_kvcache_rope_shift(A, 3, 0, 44)
+        if t == W // 2:
+            mw.mw_kvcache_rope_shift(A, 2, 0, 44)
+        mw.mw_kvcache_append(A, to_gpu(synth.normal_bf16((B, H, L, D), seed + 10 + 2 * t)),
+                             to_gpu(synth.normal_bf16((B, H, L, D), seed + 11 + 2 * t)))
+    win = list(range(A.desc.head - W, A.desc.head))
+    kw = W * B * H * L * D
+    q2 = mw.mw_quantize_fp8(to_gpu(synth.normal_bf16((B, H, 256, D), seed + 50)), qs)
+    ws = torch.full((mw.mw_chunk_attn_cached_workspace_size(A, 1, 256, W),), 0xAB, dtype=torch.uint8, device="cuda")
+    mw.mw_chunk_attn_cached_fp8(q2, q2, q2, 1, 256, A, qs, window=W, workspace=ws)
+    sync()
+    rotated = ws[:kw].view(W, B, H, L, D).clone()
+    Bc = mw.KVCache(S, B, H, L, D, fp8=True, k_scale=ks, v_scale=vs)
+    for t in range(W):
+        mw.mw_kvcache_append(Bc, to_gpu(synth.normal_bf16((B, H, L, D), seed + 60 + t)),
+                             to_gpu(synth.normal_bf16((B, H, L, D), seed + 70 + t)))
+    for i, c in enumerate(win):
+        Bc.k_slots[Bc.slot_of(i)].copy_(rotated[i])
+        Bc.v_slots[Bc.slot_of(i)].copy_(A.v_slots[A.slot_of(c)])
+    if sink:
+        Bc.set_sink(*sink)
+    q8, k8, v8 = (mw.mw_quantize_fp8(to_gpu(synth.normal_bf16((B, H, nq * qlen, D), seed + 80 + i)), qs)
+                  for i in range(3))
+    ns, _ = mw.mw_chunk_attn_cached_plan(A, nq, qlen, W, mode)
+    print(f"[case] fp8 rotation sweep L={L} W={W} sink={sink_len} nq={nq} qlen={qlen} mode={mode} splits={ns}",
+          flush=True)
+    ws_a = torch.full((mw.mw_chunk_attn_cached_workspace_size(A, nq, qlen, W),), 0xAB, dtype=torch.uint8,
+                      device="cuda")
+    oa, la = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, nq, qlen, A, qs, window=W, flags=mode, workspace=ws_a,
+                                         want_lse=True)
+    ob, lb = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, nq, qlen, Bc, qs, window=W, flags=mode, want_lse=True)
+    sync()
+    assert bool((ws_a[:kw] == 0xAB).all())
+    assert bits_equal(oa, ob)
+    assert torch.equal(la, lb)
