@@ -611,6 +611,9 @@ def main():
     K = args.steps
     total_ms = t_start.elapsed_time(t_end)
     ph = {n: sum(e[i].elapsed_time(e[i + 1]) for e in recs) / K for i, n in enumerate(PH)}
+    per_step = {n: sorted(e[i].elapsed_time(e[i + 1]) for e in recs) for i, n in enumerate(PH)}
+    ph_median = {n: v[len(v) // 2] for n, v in per_step.items()}
+    ph_min = {n: v[0] for n, v in per_step.items()}
     ms_step = total_ms / K
     tfl = lambda F, ms: F / (ms * 1e-3) / 1e12
     gbs = lambda nb, ms: nb / (ms * 1e-3) / 1e9
@@ -674,6 +677,8 @@ def main():
                               "visibility": "queued-causal"}},
         "frac_bf16_peak": round(value / PEAK_BF16_TFLOPS, 4),
         "phases_ms": {n: round(t, 4) for n, t in ph.items()},
+        "phases_ms_median": {n: round(t, 4) for n, t in ph_median.items()},
+        "phases_ms_min": {n: round(t, 4) for n, t in ph_min.items()},
         "train_d128": {"fwd_tflops": round(tfl(t128.F_fwd, ph["fwd_d128"]), 2),
                        "bwd_tflops": round(tfl(t128.F_bwd, ph["bwd_d128"]), 2), "fwd_bwd_tflops": round(value, 2)},
         "train_d64": {"fwd_tflops": round(tfl(t64.F_fwd, ph["fwd_d64"]), 2),
