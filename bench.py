@@ -314,8 +314,8 @@ def fp8_stream(mw, torch, dev, st, reps=10):
     over the full window, Infinity Cache flushed before each call; algorithmic
     bytes = e4m3 window K and V + e4m3 Q, K_new, V_new + bf16 O), with nothing
     pending and with one re-shift pending (the window keys rotated as they are
-    loaded: in the attention kernel's staging at 64 and 128 rows, in a separate
-    pass over the window at 256), and the paper's
+    loaded, in the attention kernel's staging: one query tile per head), and
+    the paper's
     1B streaming shape (CFG batch 2, 8 in-flight 600-token chunks, 300-token sink)
     over 24 / 12 / 6 cached chunks.  HIP events on the launch stream."""
     import synth

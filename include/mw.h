@@ -388,10 +388,11 @@ int mw_kvcache_init_fp8(mw_kvcache* c, void* k_slots, void* v_slots, int S, int 
  * -(rope_total - rope_at_commit[slot]) positions on the recorded band: each
  * pair is decoded, rotated in fp32 (cos/sin of the angle computed in double),
  * clamped to +-448 and rounded to e4m3 (nearest even); the slots are not
- * modified.  Calls of at most 128 queued rows whose key ranges span few
- * window chunks (chunks of at least 64 keys) rotate each K tile as the
- * attention kernel stages it; the others first write the rotated window keys
- * to the start of the workspace and the attention reads them from there.
+ * modified.  Calls with one query tile per head (at most 256 queued rows)
+ * whose key ranges span few window chunks (chunks of at least 64 keys)
+ * rotate each K tile as the attention kernel stages it; the others first
+ * write the rotated window keys to the start of the workspace and the
+ * attention reads them from there.
  * Both routes give the same bytes.  Either way the call reserves
  * window * B * H * L * 128 bytes of workspace (rounded up to 256) before the
  * key-range partials; mw_chunk_attn_cached_workspace_size of an e4m3 cache

@@ -199,7 +199,7 @@ __device__ __forceinline__ void stage_kv8(const FwdParams& p, int bh, int k0, fp
 
 // RoPE re-shift of e4m3 keys when they are used (paper Sec. 3.5, re-indexing
 // the retained window after an eviction), shared by the separate rotation pass
-// and the rotation in the few-row kernel's staging so that both produce the
+// and the rotation in the attention kernel's staging so that both produce the
 // same bytes.  (cos, sin) of a rotation by -n positions of a pair whose
 // one-position rotation is (c1, s1): (c1 - i s1)^n by repeated squaring in
 // double (no device trigonometry; a relative error of a few 1e-15 for any n).
@@ -253,9 +253,10 @@ constexpr float kRescaleThreshold8 = 8.f;  // probabilities stay <= 2^8 < 448
 // NW waves of RB 32-row query blocks in KG key groups of NW / KG row waves;
 // each step stages KG * BN keys (BN a multiple of 64) and group g works on
 // its BN-key slice; the groups merge (m, l, O) through LDS at the end.  With
-// key groups (the few-row configurations) the tiles stream four stages deep,
-// and window keys with re-shifts pending are rotated in staging (rs).
-template <int NW, int RB, int BN, int KG>
+// key groups (the few-row configurations) the tiles stream four stages deep.
+// ROT: the instantiation that rotates window keys with re-shifts pending in
+// staging (rs), for calls with one query tile per head.
+template <int NW, int RB, int BN, int KG, bool ROT>
 __global__ __launch_bounds__(64 * NW, KG > 1 ? 1 : ((8 / NW) > 0 ? (8 / NW) : 1)) void attn_fwd_fp8_kernel(
     FwdParams p, const RopeStage rs) {  // (key-group configurations hold 132 KB of LDS: one workgroup per CU)
   static_assert(NW % KG == 0, "waves split evenly into key groups");
@@ -408,6 +409,73 @@ __global__ __launch_bounds__(64 * NW, KG > 1 ? 1 : ((8 / NW) > 0 ? (8 / NW) : 1)
     }
   };
 
+  // Rotation in staging (window keys with re-shifts pending, calls the host
+  // routes here): the window chunks this workgroup's key range spans (at most
+  // kRopeStageChunks, chunks of at least BK / 2 keys, as the host checks) get a
+  // cos/sin table of their band pairs in LDS, computed once the first tiles
+  // are in flight; each staged K tile's window rows are rotated in place after
+  // the tile lands, and a barrier publishes them.
+  static_assert(NT % BK == 0 && (BK & (BK - 1)) == 0, "rotation maps a thread to one row of the tile");
+  __shared__ float rtab[ROT ? kRopeStageChunks : 1][2][64];
+  const bool rot = ROT && rs.n_pairs > 0;  // (ROT = false: an instantiation without the rotation code)
+  int w_lo = 0, nwc = 0;
+  if (rot) {
+    const int a0 = max(kbeg, p.sink_len), a1 = min(((kend + BK - 1) / BK) * BK, p.wL);
+    if (a0 < a1) {
+      w_lo = (a0 - p.sink_len) / p.L;
+      nwc = min((a1 - 1 - p.sink_len) / p.L - w_lo + 1, kRopeStageChunks);
+    }
+  }
+  // window rows of the staged tile [k0, k0 + BK): their band pieces, rotated
+  // in place, thread t on row t mod BK (a uniform test says whether the tile
+  // has any); a tile spans at most three window chunks, whose first rows are
+  // found once per tile
+  auto rotate = [&](const int k0, const int buf) {
+    if constexpr (!ROT) return false;
+    const int r0 = max(p.sink_len - k0, 0), r1 = min(p.wL - k0, BK);
+    if (r0 >= r1 || nwc == 0) return false;
+    const int kw = k0 + r0 - p.sink_len;  // window index of row r0
+    const int wa = kw / p.L;
+    const int b1 = r0 + (wa + 1) * p.L - kw, b2 = b1 + p.L;  // first rows of the next two chunks
+    const int pc0 = rs.dim_offset >> 4, pc1 = (rs.dim_offset + 2 * rs.n_pairs - 1) >> 4;
+    const int row = tid & (BK - 1);
+    if (row >= r0 && row < r1) {
+      const int wi = min(max(wa - w_lo + (row >= b1) + (row >= b2), 0), nwc - 1);
+      const int p0 = rs.dim_offset >> 1;
+      fp8_t* kt = Ks[buf];
+      // the thread's first two pieces with both reads in flight, then any more
+      constexpr int G = NT / BK;
+      const int pa = pc0 + tid / BK, pb = pa + G;
+      u32x4* aa = reinterpret_cast<u32x4*>(kt + Tile8::off(row, 16 * min(pa, 7)));
+      u32x4* ab = reinterpret_cast<u32x4*>(kt + Tile8::off(row, 16 * min(pb, 7)));
+      const u32x4 va = *aa, vb = *ab;
+      if (pa <= pc1) *aa = rope_rotate_piece(va, pa, p0, rs.n_pairs, rtab[wi][0], rtab[wi][1]);
+      if (pb <= pc1) *ab = rope_rotate_piece(vb, pb, p0, rs.n_pairs, rtab[wi][0], rtab[wi][1]);
+      for (int pc = pb + G; pc <= pc1; pc += G) {
+        u32x4* a = reinterpret_cast<u32x4*>(kt + Tile8::off(row, 16 * pc));
+        *a = rope_rotate_piece(*a, pc, p0, rs.n_pairs, rtab[wi][0], rtab[wi][1]);
+      }
+    }
+    return true;
+  };
+  // the cos/sin table: lane i takes pair i's one-position rotation, read with
+  // scalar loads (a vector load here would be the only one the compiler
+  // tracks, and it would wait for the tiles in flight as well); wave w the
+  // chunks w, w + NW, ...
+  auto rope_table = [&]() {
+    if constexpr (!ROT) return;
+    if (!rot) return;
+    double c1 = 1.0, s1 = 0.0;
+    for (int i = 0; i < rs.n_pairs; ++i) {
+      const double ci = rs.a.c1[i], si = rs.a.s1[i];
+      c1 = lane == i ? ci : c1;
+      s1 = lane == i ? si : s1;
+    }
+    for (int wi = __builtin_amdgcn_readfirstlane(wave); wi < nwc; wi += NW) {
+      const long long n = rs.a.pend[w_lo + wi];
+      if (lane < rs.n_pairs) rope_cos_sin(n, c1, s1, rtab[wi][0][lane], rtab[wi][1][lane]);
+    }
+  };
   // this wave's slice of a staged step: keys [kg * BN, (kg + 1) * BN)
   auto slice = [&](auto masked, const int k0, const int st) {
     step(masked, k0 + kg * BN, Ks[st] + kg * BN * DH, Vs[st] + kg * BN * DH);
@@ -436,52 +504,6 @@ __global__ __launch_bounds__(64 * NW, KG > 1 ? 1 : ((8 / NW) > 0 ? (8 / NW) : 1)
       const fp8_t* src = qg + (long long)min(q0 + row, p.Tq - 1) * DH + 16 * ls;
       dma_lds_16(src, lds_addr(qs) + it * NT * 16 + wave_stage_off(tid));
     }
-    // Rotation in staging: the window chunks this workgroup's key range spans
-    // (at most kRopeStageChunks, chunks of at least BK / 2 keys, as the host
-    // checks) get a cos/sin table of their band pairs in LDS, computed once the
-    // first tiles are in flight.
-    static_assert(NT % BK == 0 && (BK & (BK - 1)) == 0, "rotation maps a thread to one row of the tile");
-    __shared__ float rtab[kRopeStageChunks][2][64];
-    const bool rot = rs.n_pairs > 0;
-    int w_lo = 0, nwc = 0;
-    if (rot) {
-      const int a0 = max(kbeg, p.sink_len), a1 = min(((kend + BK - 1) / BK) * BK, p.wL);
-      if (a0 < a1) {
-        w_lo = (a0 - p.sink_len) / p.L;
-        nwc = min((a1 - 1 - p.sink_len) / p.L - w_lo + 1, kRopeStageChunks);
-      }
-    }
-    // window rows of the staged tile [k0, k0 + BK): their band pieces, rotated
-    // in place, thread t on row t mod BK (a uniform test says whether the tile
-    // has any); a tile spans at most three window chunks, whose first rows are
-    // found once per tile
-    auto rotate = [&](const int k0, const int buf) {
-      const int r0 = max(p.sink_len - k0, 0), r1 = min(p.wL - k0, BK);
-      if (r0 >= r1 || nwc == 0) return false;
-      const int kw = k0 + r0 - p.sink_len;  // window index of row r0
-      const int wa = kw / p.L;
-      const int b1 = r0 + (wa + 1) * p.L - kw, b2 = b1 + p.L;  // first rows of the next two chunks
-      const int pc0 = rs.dim_offset >> 4, pc1 = (rs.dim_offset + 2 * rs.n_pairs - 1) >> 4;
-      const int row = tid & (BK - 1);
-      if (row >= r0 && row < r1) {
-        const int wi = min(max(wa - w_lo + (row >= b1) + (row >= b2), 0), nwc - 1);
-        const int p0 = rs.dim_offset >> 1;
-        fp8_t* kt = Ks[buf];
-        // the thread's first two pieces with both reads in flight, then any more
-        constexpr int G = NT / BK;
-        const int pa = pc0 + tid / BK, pb = pa + G;
-        u32x4* aa = reinterpret_cast<u32x4*>(kt + Tile8::off(row, 16 * min(pa, 7)));
-        u32x4* ab = reinterpret_cast<u32x4*>(kt + Tile8::off(row, 16 * min(pb, 7)));
-        const u32x4 va = *aa, vb = *ab;
-        if (pa <= pc1) *aa = rope_rotate_piece(va, pa, p0, rs.n_pairs, rtab[wi][0], rtab[wi][1]);
-        if (pb <= pc1) *ab = rope_rotate_piece(vb, pb, p0, rs.n_pairs, rtab[wi][0], rtab[wi][1]);
-        for (int pc = pb + G; pc <= pc1; pc += G) {
-          u32x4* a = reinterpret_cast<u32x4*>(kt + Tile8::off(row, 16 * pc));
-          *a = rope_rotate_piece(*a, pc, p0, rs.n_pairs, rtab[wi][0], rtab[wi][1]);
-        }
-      }
-      return true;
-    };
     int ki = kc, ib = 0, ahead = 0;  // next tile to issue, its buffer, tiles issued and not yet used
 #pragma unroll
     for (int s = 0; s < NSTG - 1; ++s) {
@@ -492,21 +514,7 @@ __global__ __launch_bounds__(64 * NW, KG > 1 ? 1 : ((8 / NW) > 0 ? (8 / NW) : 1)
         ++ahead;
       }
     }
-    if (rot) {
-      // lane i takes pair i's one-position rotation, read with scalar loads
-      // (a vector load here would be the only one the compiler tracks, and it
-      // would wait for the tiles in flight as well); wave w the chunks w, w + NW, ...
-      double c1 = 1.0, s1 = 0.0;
-      for (int i = 0; i < rs.n_pairs; ++i) {
-        const double ci = rs.a.c1[i], si = rs.a.s1[i];
-        c1 = lane == i ? ci : c1;
-        s1 = lane == i ? si : s1;
-      }
-      for (int wi = __builtin_amdgcn_readfirstlane(wave); wi < nwc; wi += NW) {
-        const long long n = rs.a.pend[w_lo + wi];
-        if (lane < rs.n_pairs) rope_cos_sin(n, c1, s1, rtab[wi][0][lane], rtab[wi][1][lane]);
-      }
-    }
+    rope_table();
     wait_vmem_upto<P, NSTG - 1>(ahead);  // the Q loads
     __syncthreads();
 #pragma unroll
@@ -538,8 +546,10 @@ __global__ __launch_bounds__(64 * NW, KG > 1 ? 1 : ((8 / NW) > 0 ? (8 / NW) : 1)
   } else {
     int buf = 0;
     if (kc < kend) stage_kv8<BK, NT>(p, bh, kc, Ks[0], Vs[0], ro, tid);
+    rope_table();
     wait_vmem();
     __syncthreads();
+    if (rot && kc < kend && rotate(kc, 0)) __syncthreads();
     auto run = [&](auto masked, const int kstop) {
       while (kc < kstop) {
         const int kn = advance(kc);
@@ -547,6 +557,7 @@ __global__ __launch_bounds__(64 * NW, KG > 1 ? 1 : ((8 / NW) > 0 ? (8 / NW) : 1)
         slice(masked, kc, buf);
         wait_vmem();
         __syncthreads();
+        if (rot && kn < kend && rotate(kn, buf ^ 1)) __syncthreads();  // the next tile's window rows
         buf ^= 1;
         kc = kn;
       }
@@ -741,11 +752,11 @@ struct Fwd8FewRows {
   static constexpr int KG = 2;
 };
 
-template <int NW, int RB, int BN, int KG>
+template <int NW, int RB, int BN, int KG, bool ROT>
 hipError_t launch_fp8_tpl(FwdParams p, const RopeStage& rs, hipStream_t stream) {
   constexpr int BM = 32 * RB * (NW / KG);
   const long long grid = fwd_prepare(p, BM, true);
-  hipLaunchKernelGGL((attn_fwd_fp8_kernel<NW, RB, BN, KG>), dim3((unsigned)grid), dim3(64 * NW), 0, stream, p, rs);
+  hipLaunchKernelGGL((attn_fwd_fp8_kernel<NW, RB, BN, KG, ROT>), dim3((unsigned)grid), dim3(64 * NW), 0, stream, p, rs);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.n_splits == 1) return e;
   return launch_combine(p, DH, stream);
@@ -760,9 +771,9 @@ FwdChoice fwd8_choice(int Tq) {
   using F2 = Fwd8FewRows<2>;
   using F4 = Fwd8FewRows<4>;
   using C = Fwd8Cfg;
-  static const int r64 = resident_workgroups(attn_fwd_fp8_kernel<F2::NW, F2::RB, F2::BN, F2::KG>, 64 * F2::NW, 1);
-  static const int r128 = resident_workgroups(attn_fwd_fp8_kernel<F4::NW, F4::RB, F4::BN, F4::KG>, 64 * F4::NW, 1);
-  static const int r256 = resident_workgroups(attn_fwd_fp8_kernel<C::NW, C::RB, C::BN, C::KG>, 64 * C::NW, 1);
+  static const int r64 = resident_workgroups(attn_fwd_fp8_kernel<F2::NW, F2::RB, F2::BN, F2::KG, true>, 64 * F2::NW, 1);
+  static const int r128 = resident_workgroups(attn_fwd_fp8_kernel<F4::NW, F4::RB, F4::BN, F4::KG, true>, 64 * F4::NW, 1);
+  static const int r256 = resident_workgroups(attn_fwd_fp8_kernel<C::NW, C::RB, C::BN, C::KG, false>, 64 * C::NW, 1);
   if (Tq <= 64) return {64, F2::BN * F2::KG, r64};
   if (Tq <= 128) return {128, F4::BN * F4::KG, r128};
   return {32 * C::RB * C::NW, C::BN, r256};
@@ -770,7 +781,9 @@ FwdChoice fwd8_choice(int Tq) {
 
 bool fwd8_rotates_in_staging(int Tq, int Tk, int L, const SplitPlan& sp) {
   const FwdChoice ch = fwd8_choice(Tq);
-  if (ch.bm > 128 || L < 1 || Tk < 1) return false;  // the 256-row configuration rotates in a separate pass
+  // with several query tiles per head each key tile is staged once per query
+  // tile: those calls rotate the window once, in the separate pass
+  if ((Tq + ch.bm - 1) / ch.bm > 1 || L < 1 || Tk < 1) return false;
   if (2 * L < ch.bk) return false;  // a staged tile spans at most three window chunks
   const long long ntiles = (Tk + ch.bk - 1) / ch.bk;
   const long long ns = std::max(sp.n_splits, 1);
@@ -784,12 +797,14 @@ hipError_t launch_fwd_fp8(FwdParams p, const RopeStage& rs, hipStream_t stream) 
   using F4 = Fwd8FewRows<4>;
   using C = Fwd8Cfg;
   const int bm = fwd8_choice(p.Tq).bm;
-  if (rs.n_pairs > 0 && (bm > 128 || rs.n_pairs > 64 || rs.dim_offset < 0 || rs.dim_offset % 2 != 0 ||
+  if (rs.n_pairs > 0 && (rs.n_pairs > 64 || rs.dim_offset < 0 || rs.dim_offset % 2 != 0 ||
                          rs.dim_offset + 2 * rs.n_pairs > DH))
     return hipErrorInvalidValue;
-  if (bm == 64) return launch_fp8_tpl<F2::NW, F2::RB, F2::BN, F2::KG>(p, rs, stream);
-  if (bm == 128) return launch_fp8_tpl<F4::NW, F4::RB, F4::BN, F4::KG>(p, rs, stream);
-  return launch_fp8_tpl<C::NW, C::RB, C::BN, C::KG>(p, rs, stream);
+  if (bm == 64) return launch_fp8_tpl<F2::NW, F2::RB, F2::BN, F2::KG, true>(p, rs, stream);
+  if (bm == 128) return launch_fp8_tpl<F4::NW, F4::RB, F4::BN, F4::KG, true>(p, rs, stream);
+  // the 256-row configuration without the rotation code unless this call rotates in staging
+  if (rs.n_pairs > 0) return launch_fp8_tpl<C::NW, C::RB, C::BN, C::KG, true>(p, rs, stream);
+  return launch_fp8_tpl<C::NW, C::RB, C::BN, C::KG, false>(p, rs, stream);
 }
 
 hipError_t launch_rope_load_fp8(const uint8_t* k_slots, uint8_t* k_win, long long slot_bytes, int S, int first_slot,

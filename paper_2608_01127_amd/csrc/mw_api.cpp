@@ -743,7 +743,7 @@ int mw_chunk_attn_cached_fp8(const void* q8, const void* k8_new, const void* v8_
   p.first_slot = (int)((c->head - w) % c->S);
   // Rotation on load of window keys with shifts pending: the start of the
   // workspace is reserved for the rotated window (the plan never depends on
-  // which of the two routes runs).  Few-row calls rotate each staged K tile
+  // which of the two routes runs).  Calls with one query tile per head rotate each staged K tile
   // inside the attention kernel; the others rotate the window into the
   // reserved bytes first and the attention reads the keys from there.
   long long pend[MW_MAX_WINDOW];

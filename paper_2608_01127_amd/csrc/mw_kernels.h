@@ -182,7 +182,7 @@ struct RopeLoadArgs {
   double s1[64];
 };
 // The same rotation done inside the e4m3 attention kernel's staging, on each
-// staged K tile in LDS (the few-row configurations only): pend[w] for the
+// staged K tile in LDS (calls with one query tile per head): pend[w] for the
 // window chunks of the call, band as above; n_pairs = 0 rotates nothing.
 struct RopeStage {
   RopeLoadArgs a;
@@ -193,7 +193,7 @@ struct RopeStage {
 // cos/sin tables live in LDS).
 constexpr int kRopeStageChunks = 8;
 // Whether a call (Tq queued rows over Tk keys, window chunks of L keys, split
-// plan sp) runs a few-row configuration whose every workgroup's key range
+// plan sp) has one query tile per head and every workgroup's key range
 // spans at most kRopeStageChunks window chunks, with chunks of at least half
 // a staged tile, so that it can rotate its window keys in staging instead of
 // in a separate pass.

@@ -240,7 +240,7 @@ def test_fp8_decode_full_window(mw, q_len, shift):
     """The e4m3 cache-bound decode shapes the benchmark times: one queued chunk of q_len tokens
     over the full window of the streaming shape (6 committed 2640-token chunks of an 8-slot ring,
     B1 H16 D128), with the call's own key-range split, with nothing pending and after one
-    re-shift of 3 positions (rotated in staging at 64 rows, in the separate pass at 256); every
+    re-shift of 3 positions (rotated in staging: one query tile per head); every
     head against the oracle on the dequantized codes (the window keys rotated and rounded once)."""
     s = synth.STREAM
     print(f"[case] fp8 decode q_len={q_len} shift={shift} over {s.window} x {s.chunk_len}", flush=True)
@@ -406,10 +406,10 @@ def _rotated_window_rollout(mw, L, seed):
 
 
 def test_fp8_rotation_in_staging_bit_identical_to_separate_pass(mw):
-    """Few-row e4m3 calls with re-shifts pending rotate each staged K tile inside the attention
-    kernel; calls of more rows rotate the window in a separate pass into the start of the
-    workspace.  Both run the same arithmetic, so: a 256-row call leaves the rotated window in its
-    workspace; a second cache holding those rotated codes in its slots, with nothing pending,
+    """e4m3 calls with re-shifts pending and one query tile per head rotate each staged K tile
+    inside the attention kernel; calls of more query tiles rotate the window in a separate pass
+    into the start of the workspace.  Both run the same arithmetic, so: a 300-row call leaves the
+    rotated window in its workspace; a second cache holding those rotated codes in its slots, with nothing pending,
     gives a 64-row call bit for bit the output the shifted cache gives it; and the shifted
     cache's 64-row call (split into key ranges) leaves the workspace's rotated-window bytes
     untouched, i.e. no separate pass ran."""
@@ -420,9 +420,9 @@ def test_fp8_rotation_in_staging_bit_identical_to_separate_pass(mw):
     assert len(set(pend)) > 1 and max(pend) > 0  # (the newest chunk has nothing pending: identity rotation)
     qs = 0.0105
     kw = W * B * H * L * D
-    q2, k2, v2 = (mw.mw_quantize_fp8(to_gpu(synth.normal_bf16((B, H, 256, D), 9560 + i)), qs) for i in range(3))
-    ws = torch.full((mw.mw_chunk_attn_cached_workspace_size(A, 1, 256, W),), 0xAB, dtype=torch.uint8, device="cuda")
-    mw.mw_chunk_attn_cached_fp8(q2, k2, v2, 1, 256, A, qs, window=W, workspace=ws)
+    q2, k2, v2 = (mw.mw_quantize_fp8(to_gpu(synth.normal_bf16((B, H, 300, D), 9560 + i)), qs) for i in range(3))
+    ws = torch.full((mw.mw_chunk_attn_cached_workspace_size(A, 1, 300, W),), 0xAB, dtype=torch.uint8, device="cuda")
+    mw.mw_chunk_attn_cached_fp8(q2, k2, v2, 1, 300, A, qs, window=W, workspace=ws)
     sync()
     rotated = ws[:kw].view(W, B, H, L, D).clone()
     assert not bool((rotated == 0xAB).all())
@@ -487,11 +487,13 @@ def test_fp8_rotation_route_vs_oracle(mw, L, in_staging):
     (256, 3, 300, 1, 33, 0),     # a sink longer than two tiles, ragged 33 rows
     (128, 4, 40, 2, 50, 1),      # two queued chunks (100 rows, 128-row configuration), isolated
     (100, 6, 5, 1, 128, 0),      # 128 rows, the whole ring's window after wrapping
+    (256, 4, 40, 1, 200, 0),     # 200 rows: the 256-row configuration, one query tile per head
 ])
 def test_fp8_rotation_in_staging_sweep(mw, L, W, sink_len, nq, qlen, mode):
     """Rotation in staging against the separate pass, bit for bit, over shapes that move the
     window's chunk edges, the sink and the ragged end around the staged tiles: the separate pass
-    of a 256-row call on the shifted cache writes the rotated window into its workspace; a second
+    of a 300-row call (two query tiles) on the shifted cache writes the rotated window into its
+    workspace; a second
     cache holds those codes with nothing pending; a few-row call gives both caches the same output
     and LSE, and leaves the shifted call's workspace bytes of the rotated window untouched."""
     import torch
@@ -515,9 +517,9 @@ def test_fp8_rotation_in_staging_sweep(mw, L, W, sink_len, nq, qlen, mode):
                              to_gpu(synth.normal_bf16((B, H, L, D), seed + 11 + 2 * t)))
     win = list(range(A.desc.head - W, A.desc.head))
     kw = W * B * H * L * D
-    q2 = mw.mw_quantize_fp8(to_gpu(synth.normal_bf16((B, H, 256, D), seed + 50)), qs)
-    ws = torch.full((mw.mw_chunk_attn_cached_workspace_size(A, 1, 256, W),), 0xAB, dtype=torch.uint8, device="cuda")
-    mw.mw_chunk_attn_cached_fp8(q2, q2, q2, 1, 256, A, qs, window=W, workspace=ws)
+    q2 = mw.mw_quantize_fp8(to_gpu(synth.normal_bf16((B, H, 300, D), seed + 50)), qs)
+    ws = torch.full((mw.mw_chunk_attn_cached_workspace_size(A, 1, 300, W),), 0xAB, dtype=torch.uint8, device="cuda")
+    mw.mw_chunk_attn_cached_fp8(q2, q2, q2, 1, 300, A, qs, window=W, workspace=ws)
     sync()
     rotated = ws[:kw].view(W, B, H, L, D).clone()
     Bc = mw.KVCache(S, B, H, L, D, fp8=True, k_scale=ks, v_scale=vs)
