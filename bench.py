@@ -17,7 +17,8 @@ Prints one JSON line.  `value` is the D=128 training forward+backward
 throughput in useful TFLOP/s (4 P D forward + 10 P D backward, P = visible
 query-key pairs), timed with HIP events on the launch stream over the K timed
 steps.  Outside the timed steps: the cache-bound decode shapes, a 200-step
-rollout, the paper's own shapes, the e4m3 variant and the CPU oracle baseline.
+rollout, the paper's own shapes, the e4m3 variant, what the vendor libraries
+reach on this card (a copy, a read, a bf16 GEMM) and the CPU oracle baseline.
 """
 from __future__ import annotations
 
@@ -227,6 +228,47 @@ def decode_shapes(mw, torch, cache, st, dev, reps=20):
         out.append({"q_len": ql, "us": round(ms * 1e3, 2), "gbs": round(gbs, 1),
                     "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4), "bytes": nbytes})
     return out
+
+
+def library_ceilings(torch, dev, reps=20):
+    """What the vendor libraries reach on this card, measured live beside the kernels (context for the
+    rooflines, which stay on the published peaks): a 1 GiB device-to-device copy (bytes read plus
+    written), a 1 GiB read (a sum), and a bf16 GEMM of 8192 x 8192 x 8192 through torch.matmul
+    (hipBLASLt).  Each is the median of `reps` event-timed calls after 3 warm-up calls."""
+    def med(fn):
+        for _ in range(3):
+            fn()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return sorted(ts)[len(ts) // 2]
+
+    n = 1 << 28  # fp32 elements: 1 GiB
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    ms_copy = med(lambda: dst.copy_(src))
+    ms_read = med(lambda: src.sum())
+    del dst
+    m = 8192
+    g = torch.Generator(device=dev).manual_seed(4321)
+    a = torch.randn(m, m, device=dev, generator=g).to(torch.bfloat16)
+    b = torch.randn(m, m, device=dev, generator=g).to(torch.bfloat16)
+    ms_gemm = med(lambda: torch.matmul(a, b))
+    del src, a, b
+    copy_gbs = 2 * 4 * n / (ms_copy * 1e-3) / 1e9
+    read_gbs = 4 * n / (ms_read * 1e-3) / 1e9
+    gemm_tf = 2.0 * m ** 3 / (ms_gemm * 1e-3) / 1e12
+    return {"copy_1gib": {"gbs": round(copy_gbs, 1), "frac_hbm_peak": round(copy_gbs / PEAK_HBM_GBS, 4),
+                          "us": round(ms_copy * 1e3, 1)},
+            "read_1gib_sum": {"gbs": round(read_gbs, 1), "frac_hbm_peak": round(read_gbs / PEAK_HBM_GBS, 4),
+                              "us": round(ms_read * 1e3, 1)},
+            "gemm_bf16_8192": {"tflops": round(gemm_tf, 1), "frac_bf16_peak": round(gemm_tf / PEAK_BF16_TFLOPS, 4),
+                               "us": round(ms_gemm * 1e3, 1)}}
 
 
 def paper_shapes(mw, torch, dev, reps=5):
@@ -698,6 +740,7 @@ def main():
     res["rollout"] = rollout(mw, torch, dev, st)
     res["paper_1b"] = paper_shapes(mw, torch, dev)
     res["fp8_stream"] = fp8_stream(mw, torch, dev, st)
+    res["library_ceilings"] = library_ceilings(torch, dev)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(args.cpu_seconds, bits128)
     else:

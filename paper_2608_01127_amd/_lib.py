@@ -434,6 +434,7 @@ def mw_chunk_attn_cached(q, k_new, v_new, n_queued: int, q_len: int, cache: KVCa
         workspace = torch.empty(need, dtype=torch.uint8, device=dev) if need > 0 else None
     if not split:
         workspace = None
+    _same_device(q, o, workspace)
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(load().mw_chunk_attn_cached_strided(_ptr(q), _ptr(k_new), _ptr(v_new), int(n_queued), int(q_len),
                                                ctypes.byref(d), int(window), int(flags), _ptr(o), _ptr(lse), scale,
@@ -484,6 +485,7 @@ def mw_chunk_attn_cached_fp8(q8, k8_new, v8_new, n_queued: int, q_len: int, cach
         workspace = torch.empty(need, dtype=torch.uint8, device=dev) if need > 0 else None
     if not split:
         workspace = None
+    _same_device(q8, o, workspace)
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(load().mw_chunk_attn_cached_fp8(_ptr(q8), _ptr(k8_new), _ptr(v8_new), int(n_queued), int(q_len),
                                            ctypes.byref(d), int(window), int(flags), _ptr(o), _ptr(lse), scale,

@@ -190,6 +190,28 @@ def test_cached_rejects_bad_lse(mw):
     sync()
 
 
+def test_host_workspace_rejected(mw):
+    """A workspace in host memory raises before any launch (the kernels would write their
+    partials through it), for the bf16 and e4m3 cached calls and the training backward."""
+    import torch
+    B, H, D, L, S, nq = 1, 2, 128, 64, 3, 1
+    q = to_gpu(synth.normal_bf16((B, H, nq * L, D), 6))
+    q8 = mw.mw_quantize_fp8(q, 0.01)
+    host_ws = torch.empty(1 << 22, dtype=torch.uint8)
+    for fp8 in (False, True):
+        cache = mw.KVCache(S, B, H, L, D, fp8=fp8, k_scale=0.01, v_scale=0.01)
+        mw.mw_kvcache_append(cache, q, q)
+        with pytest.raises(ValueError):
+            if fp8:
+                mw.mw_chunk_attn_cached_fp8(q8, q8, q8, nq, L, cache, 0.01, workspace=host_ws)
+            else:
+                mw.mw_chunk_attn_cached(q, q, q, nq, L, cache, workspace=host_ws)
+    o, lse = mw.mw_block_causal_attn_fwd(q, q, q, L)
+    with pytest.raises(ValueError):
+        mw.mw_block_causal_attn_bwd(q, q, q, o, o, lse, L, workspace=host_ws)
+    sync()
+
+
 @pytest.mark.parametrize("q_len", [64, 128, 256, 300, 512])
 def test_decode_shape_split_vs_oracle(mw, q_len):
     """One short queued chunk over a full 6-chunk window (B1 H16 D128, 2640-token chunks):
