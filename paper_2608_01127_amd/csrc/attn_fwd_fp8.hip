@@ -82,14 +82,18 @@ __device__ __forceinline__ i32x8 lds_v8(const fp8_t* tile, int db, int lane) {
 }
 
 // Probabilities of two 32-key accumulator blocks -> e4m3 B operand (RNE; the
-// values lie in [0, 2^8], inside the e4m3 range).
+// values lie in [0, 2^8], inside the e4m3 range).  Each conversion writes one
+// 16-bit half of its destination and keeps the other; the high-half
+// conversion overwrites what the low-half one kept, so the low-half one takes
+// its first input's register as the kept value instead of a zeroed register
+// (a zero costs a move each).
 __device__ __forceinline__ i32x8 pack_p8(const f32x16& s0, const f32x16& s1) {
   i32x8 r;
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
-    int x = __builtin_amdgcn_cvt_pk_fp8_f32(s0[4 * w], s0[4 * w + 1], 0, false);
+    int x = __builtin_amdgcn_cvt_pk_fp8_f32(s0[4 * w], s0[4 * w + 1], __float_as_int(s0[4 * w]), false);
     r[w] = __builtin_amdgcn_cvt_pk_fp8_f32(s0[4 * w + 2], s0[4 * w + 3], x, true);
-    x = __builtin_amdgcn_cvt_pk_fp8_f32(s1[4 * w], s1[4 * w + 1], 0, false);
+    x = __builtin_amdgcn_cvt_pk_fp8_f32(s1[4 * w], s1[4 * w + 1], __float_as_int(s1[4 * w]), false);
     r[4 + w] = __builtin_amdgcn_cvt_pk_fp8_f32(s1[4 * w + 2], s1[4 * w + 3], x, true);
   }
   return r;
@@ -390,7 +394,7 @@ __global__ __launch_bounds__(64 * NW, KG > 1 ? 1 : ((8 / NW) > 0 ? (8 / NW) : 1)
         for (int i = 0; i < 16; ++i) {
           const float pv = fast_exp2(fmaf(s[rb][kb][i], c, nm));
           s[rb][kb][i] = pv;
-          ls += pv;
+          ls = (kb == 0 && i == 0) ? pv : ls + pv;  // (no add of the zero start)
         }
       }
       lsum[rb] += ls;
