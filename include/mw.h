@@ -20,7 +20,13 @@
  *     backward workspace; the library never allocates or frees device memory.
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = the legacy default
  *     stream) and the call returns without waiting.  Faults during kernel
- *     execution surface at the caller's next synchronisation.
+ *     execution surface at the caller's next synchronisation.  Only kernel
+ *     launches are enqueued (no memset, copy or allocation), so the attention
+ *     calls and mw_quantize_fp8 may be recorded into a HIP graph; the
+ *     mw_kvcache_* calls that change a ring's host descriptor (init, append,
+ *     evict, set_sink, rope_shift) must run outside it, and a recorded
+ *     attention call keeps the ring state (window, pending re-shifts) it was
+ *     recorded with.
  *   - Arguments are validated before anything is enqueued; on error nothing
  *     is enqueued, no state changes, and a negative mw_status is returned.
  *     mw_last_error() then describes the problem (per-thread message).
