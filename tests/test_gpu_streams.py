@@ -27,7 +27,7 @@ def _path(mw, t, L):
     mw.mw_kvcache_evict(cache, 1)
     mw.mw_kvcache_rope_shift(cache, 3, 0, 44)
     oc, lc = mw.mw_chunk_attn_cached(qn, kn, vn, 1, L, cache, want_lse=True)
-    out += [cache.k_slots, cache.v_slots, oc, lc]
+    out += [cache.k_slots[:nc], cache.v_slots[:nc], oc, lc]  # (slot nc is never written)
     c8 = mw.KVCache(nc + 1, B, H, L, D, fp8=True, k_scale=0.02, v_scale=0.02)
     for c in range(nc):
         mw.mw_kvcache_append(c8, t["k"][:, :, c * L:(c + 1) * L], t["v"][:, :, c * L:(c + 1) * L])
@@ -35,7 +35,7 @@ def _path(mw, t, L):
     mw.mw_kvcache_rope_shift(c8, 3, 0, 44)
     q8, k8, v8 = (mw.mw_quantize_fp8(x, 0.02) for x in (qn, kn, vn))
     o8, l8 = mw.mw_chunk_attn_cached_fp8(q8, k8, v8, 1, L, c8, 0.02, want_lse=True)
-    out += [c8.k_slots, c8.v_slots, q8, o8, l8]
+    out += [c8.k_slots[:nc], c8.v_slots[:nc], q8, o8, l8]
     return [x.view(torch.int16) if x.dtype == torch.bfloat16 else x for x in out]
 
 
