@@ -665,13 +665,13 @@ def main():
     n_splits, n_whole = mw.mw_chunk_attn_cached_plan(cache, st.n_queued, st.q_len, st.window, 0, ws_c.numel())
 
     # Dominant launch of the step: the D128 training backward call
-    # (mw_block_causal_attn_bwd: row terms, then dK/dV, then dQ).  Its
-    # algorithmic FLOPs are the backward's useful 10 P D; the events bracket
-    # the three kernels, so the duration is the call's.
+    # (mw_block_causal_attn_bwd: the row terms, then the dK/dV and dQ work in
+    # one grid).  Its algorithmic FLOPs are the backward's useful 10 P D; the
+    # events bracket both kernels, so the duration is the call's.
     bwd_digest = source_digest(["paper_2608_01127_amd/csrc/attn_bwd.hip", "paper_2608_01127_amd/csrc/mw_device.h",
                                 "paper_2608_01127_amd/csrc/mw_kernels.h", "paper_2608_01127_amd/build.py"])
     roofline = {"kernel": "mw_block_causal_attn_bwd at B1 H16 T42240 D128 L2640 = bwd_rowterms_kernel<128> + "
-                          "bwd_dkdv_kernel<128, 4, 64, 1> + bwd_dq_kernel<128, 4, 1, 64>",
+                          "bwd_grad_kernel<128, 4, 32, 4, 1, 64, true>",
                 "bound": "mfma", "achieved": round(tfl(t128.F_bwd, ph["bwd_d128"]), 2), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(tfl(t128.F_bwd, ph["bwd_d128"]) / PEAK_BF16_TFLOPS, 4),
                 "traffic": read_traffic("train_bwd_d128", bwd_digest),

@@ -57,11 +57,14 @@ __global__ __launch_bounds__(256) void bwd_rowterms_kernel(BwdParams p, long lon
 }
 
 // LDS of the dK/dV work: Q and dO tiles (two stages each), then LSE and -Delta
-// of the tile's rows (two stages each).
-template <int D, int NW, int BM>
+// of the tile's rows (two stages each, staged 64 rows at a time), then with
+// VLDS the workgroup's V tile.
+template <int D, int NW, int BM, int KBW, bool VLDS>
 struct DkdvLds {
   static constexpr int TE = stage_elems<D, BM, 64 * NW>();
-  static constexpr int BYTES = 2 * 2 * TE * 2 + 2 * 2 * BM * 4;
+  static constexpr int RT = BM < 64 ? 64 : BM;  // row-term entries per stage
+  static constexpr int TEV = VLDS ? stage_elems<D, 32 * NW * KBW, 64 * NW>() : 0;
+  static constexpr int BYTES = 2 * 2 * TE * 2 + 2 * 2 * RT * 4 + TEV * 2;
 };
 
 // NW waves, each owning KBW blocks of 32 keys (K and V fragments and the dK,
@@ -70,17 +73,22 @@ struct DkdvLds {
 // MFMA; the register state then needs the full register file of one wave per
 // SIMD (measured slower than one key block at two waves per SIMD at D = 64,
 // where the in-order issue of a lone wave cannot overlap its MFMAs and its
-// softmax work).  Work item: key tile kt of (batch, head) bh.
-template <int D, int NW, int BM, int KBW>
+// softmax work).  With VLDS the V fragments (the dP products' B operand) are
+// read from the workgroup's V tile, staged in LDS once, instead of being held
+// in registers: 32 registers fewer per wave at D = 128 for one more 1 KB
+// fragment read per 32 x 32 block.  Work item: key tile kt of (batch, head) bh.
+template <int D, int NW, int BM, int KBW, bool VLDS>
 __device__ __forceinline__ void dkdv_body(const BwdParams& p, const int bh, const int kt, unsigned char* lds) {
   constexpr int BN = 32 * NW * KBW, NT = 64 * NW;
-  static_assert(BM % 64 == 0, "row terms are staged 64 at a time");
+  static_assert(BM % 32 == 0, "32-row query blocks");
   constexpr int KK = (D + 15) / 16, DB = (D + 31) / 32;  // D = 72: 80 and 96 columns
-  constexpr int TE = DkdvLds<D, NW, BM>::TE;
+  using LD = DkdvLds<D, NW, BM, KBW, VLDS>;
+  constexpr int TE = LD::TE, RT = LD::RT;
   bf16_t(*Qs)[TE] = reinterpret_cast<bf16_t(*)[TE]>(lds);
   bf16_t(*dOs)[TE] = reinterpret_cast<bf16_t(*)[TE]>(lds + 2 * TE * 2);
-  float(*lse_s)[BM] = reinterpret_cast<float(*)[BM]>(lds + 4 * TE * 2);
-  float(*dlt_s)[BM] = reinterpret_cast<float(*)[BM]>(lds + 4 * TE * 2 + 2 * BM * 4);
+  float(*lse_s)[RT] = reinterpret_cast<float(*)[RT]>(lds + 4 * TE * 2);
+  float(*dlt_s)[RT] = reinterpret_cast<float(*)[RT]>(lds + 4 * TE * 2 + 2 * RT * 4);
+  bf16_t* Vs = reinterpret_cast<bf16_t*>(lds + 4 * TE * 2 + 4 * RT * 4);  // (VLDS) the workgroup's V tile
   const FragOffsets<D> fo(threadIdx.x & 63, 0);  // Q and dO tiles share the layout
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -107,7 +115,7 @@ __device__ __forceinline__ void dkdv_body(const BwdParams& p, const int bh, cons
     for (int kk = 0; kk < KK; ++kk) {
       if (D % 16 == 0 || 16 * kk + 8 * (lane >> 5) < D) {
         kf[kb][kk] = *reinterpret_cast<const bf16x8*>(ka + 16 * kk);
-        vf[kb][kk] = *reinterpret_cast<const bf16x8*>(va + 16 * kk);
+        if constexpr (!VLDS) vf[kb][kk] = *reinterpret_cast<const bf16x8*>(va + 16 * kk);
       } else {  // columns past D (D = 72): zeros
 #pragma unroll
         for (int j = 0; j < 8; ++j) kf[kb][kk][j] = vf[kb][kk][j] = (__bf16)0.f;
@@ -139,9 +147,9 @@ __device__ __forceinline__ void dkdv_body(const BwdParams& p, const int bh, cons
     }
     // row terms of the tile: 64 fp32 per wave, LSE then -Delta
 #pragma unroll
-    for (int c = wave; c < 2 * (BM / 64); c += NW) {
-      const int part = c % (BM / 64);
-      if (c < BM / 64) {
+    for (int c = wave; c < 2 * (RT / 64); c += NW) {
+      const int part = c % (RT / 64);
+      if (c < RT / 64) {
         stage_f32x64_direct(lse_s[b] + 64 * part, lse2_bh, q0 + 64 * part, T, lane);
       } else {
         stage_f32x64_direct(dlt_s[b] + 64 * part, dlt_bh, q0 + 64 * part, T, lane);
@@ -176,7 +184,11 @@ __device__ __forceinline__ void dkdv_body(const BwdParams& p, const int bh, cons
 #pragma unroll
         for (int kb = 0; kb < KBW; ++kb) {
           s[kb] = mfma32(qa, kf[kb][kk], s[kb]);
-          dp[kb] = mfma32(da, vf[kb][kk], dp[kb]);
+          if constexpr (VLDS) {
+            dp[kb] = mfma32(da, fo.row8(Vs, (wave * KBW + kb) * 32, kk), dp[kb]);
+          } else {
+            dp[kb] = mfma32(da, vf[kb][kk], dp[kb]);
+          }
         }
       }
 #pragma unroll
@@ -226,6 +238,14 @@ __device__ __forceinline__ void dkdv_body(const BwdParams& p, const int bh, cons
   const int qfe = max(qfb, (T / BM) * BM);
   int buf = 0;
   int q0 = qstart;
+  if constexpr (VLDS) {  // the workgroup's V rows, read as the dP products' B operand
+    const bf16_t* vb = p.v + bi * p.sv.b + hi * p.sv.h;
+    if (k0 + BN <= T) {
+      stage_rows_s<D, BN, NT>(Vs, vb + (long long)k0 * p.sv.t, RowOffsets<D, BN, NT>(p.sv.t, tid), tid);
+    } else {
+      stage_rows_direct<D, BN, NT>(Vs, [&](int r) { return vb + (long long)min(k0 + r, T - 1) * p.sv.t; }, tid);
+    }
+  }
   if (q0 < T) stage(q0, 0);
   wait_vmem();
   __syncthreads();
@@ -264,15 +284,6 @@ __device__ __forceinline__ void dkdv_body(const BwdParams& p, const int bh, cons
       }
     }
   }
-}
-
-template <int D, int NW, int BM, int KBW>
-__global__ __launch_bounds__(64 * NW, (D == 128 || KBW > 1 ? 4 : 8) / NW) void bwd_dkdv_kernel(BwdParams p,
-                                                                                            int n_ktiles) {
-  __shared__ __attribute__((aligned(16))) unsigned char lds[DkdvLds<D, NW, BM>::BYTES];
-  int bh, kt, split;  // early keys are seen by the most queries: heaviest first
-  tile_item(blockIdx.x, gridDim.x, p.BH, n_ktiles, 1, bh, kt, split);
-  dkdv_body<D, NW, BM, KBW>(p, bh, kt, lds);
 }
 
 // LDS of the dQ work: K and V tiles, two stages each.
@@ -437,74 +448,61 @@ __device__ __forceinline__ void dq_body(const BwdParams& p, const int bh, const 
   }
 }
 
-template <int D, int NW, int RB, int BN>
-__global__ __launch_bounds__(64 * NW, 8 / NW) void bwd_dq_kernel(BwdParams p, int n_qtiles) {
-  __shared__ __attribute__((aligned(16))) unsigned char lds[DqLds<D, NW, BN>::BYTES];
-  int bh, r, split;  // late queries see the most keys: heaviest first
-  tile_item(blockIdx.x, gridDim.x, p.BH, n_qtiles, 1, bh, r, split);
-  dq_body<D, NW, RB, BN>(p, bh, n_qtiles - 1 - r, lds);
-}
-
 // dK/dV and dQ work in one grid (both run two waves per SIMD with four-wave
 // workgroups): the first n_dkdv workgroups take key tiles, the rest query
 // tiles, so the query tiles fill the CUs that the key tiles' tail leaves idle
 // and no kernel boundary separates them.  Each part keeps its own XCD-aware,
 // heaviest-first order (tile_item; exact when n_dkdv is a multiple of the XCD
-// count).
-template <int D, int NK, int BMK, int NQ, int RQ, int BNQ>
+// count).  Early keys are seen by the most queries and late queries see the
+// most keys: both parts run their heaviest tiles first.
+template <int D, int NK, int BMK, int NQ, int RQ, int BNQ, bool VLDS>
 __global__ __launch_bounds__(256, 2) void bwd_grad_kernel(BwdParams p, int n_dkdv, int n_ktiles, int n_qtiles) {
   static_assert(NK == 4 && NQ == 4, "four-wave workgroups");
-  constexpr int B1 = DkdvLds<D, NK, BMK>::BYTES, B2 = DqLds<D, NQ, BNQ>::BYTES;
+  constexpr int B1 = DkdvLds<D, NK, BMK, 1, VLDS>::BYTES, B2 = DqLds<D, NQ, BNQ>::BYTES;
   __shared__ __attribute__((aligned(16))) unsigned char lds[B1 > B2 ? B1 : B2];
   const int id = blockIdx.x;
   int bh, r, split;
   if (id < n_dkdv) {
     tile_item(id, n_dkdv, p.BH, n_ktiles, 1, bh, r, split);
-    dkdv_body<D, NK, BMK, 1>(p, bh, r, lds);
+    dkdv_body<D, NK, BMK, 1, VLDS>(p, bh, r, lds);
   } else {
     tile_item(id - n_dkdv, (int)gridDim.x - n_dkdv, p.BH, n_qtiles, 1, bh, r, split);
     dq_body<D, NQ, RQ, BNQ>(p, bh, n_qtiles - 1 - r, lds);
   }
 }
 
-// Waves per workgroup of the dK/dV kernel (32 keys each) and of the dQ kernel
-// (32 queries each).
+// Waves per workgroup of the dK/dV work (32 keys each) and of the dQ work (32
+// queries each).
 template <int D>
 struct BwdCfg {
   static constexpr int NW_DKV = 4;
-  static constexpr int KBW_DKV = 1;  // 32-key blocks per wave of the dK/dV kernel
   static constexpr int NW_DQ = 4;
-  // 32-row query blocks per wave in the dQ kernel (two measured no faster at
+  // 32-row query blocks per wave in the dQ work (two measured no faster at
   // D = 64 and spill at D = 128)
   static constexpr int RB_DQ = 1;
-  static constexpr int BM_DKV = 64;  // queries per step of the dK/dV kernel
-  static constexpr int BN_DQ = D == 64 ? 128 : 64;  // keys per step of the dQ kernel
-  // dK/dV and dQ work in one grid where both run two waves per SIMD (at
-  // D = 128 the dK/dV work needs one wave per SIMD)
-  static constexpr bool ONE_GRID = D != 128;
+  // D = 128: the V tile in LDS and 32-query steps bring the dK/dV work under
+  // 256 registers (248), so it runs two waves per SIMD beside the dQ work in
+  // one grid; holding V in registers needed 448 registers, one wave per SIMD,
+  // in a grid of its own (the backward 5% slower, results bit-identical)
+  static constexpr bool VLDS_DKV = D == 128;
+  static constexpr int BM_DKV = D == 128 ? 32 : 64;  // queries per step of the dK/dV work
+  static constexpr int BN_DQ = D == 64 ? 128 : 64;   // keys per step of the dQ work
 };
 
 template <int D>
 static hipError_t launch_bwd_d(const BwdParams& p, hipStream_t stream) {
   constexpr int NK = BwdCfg<D>::NW_DKV, NQ = BwdCfg<D>::NW_DQ, RQ = BwdCfg<D>::RB_DQ;
-  constexpr int BMK = BwdCfg<D>::BM_DKV, BNQ = BwdCfg<D>::BN_DQ, KBW = BwdCfg<D>::KBW_DKV;
+  constexpr int BMK = BwdCfg<D>::BM_DKV, BNQ = BwdCfg<D>::BN_DQ;
   const long long rows = (long long)p.BH * p.T;
   const long long threads = rows * (D == 64 ? 8 : 16);
   hipLaunchKernelGGL(bwd_rowterms_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p,
                      rows);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int nkt = (p.T + 32 * NK * KBW - 1) / (32 * NK * KBW);
+  const int nkt = (p.T + 32 * NK - 1) / (32 * NK);
   const int nqt = (p.T + 32 * RQ * NQ - 1) / (32 * RQ * NQ);
-  if constexpr (BwdCfg<D>::ONE_GRID) {
-    hipLaunchKernelGGL((bwd_grad_kernel<D, NK, BMK, NQ, RQ, BNQ>), dim3(nkt * p.BH + nqt * p.BH), dim3(256), 0,
-                       stream, p, nkt * p.BH, nkt, nqt);
-    return hipGetLastError();
-  }
-  hipLaunchKernelGGL((bwd_dkdv_kernel<D, NK, BMK, KBW>), dim3(nkt * p.BH), dim3(64 * NK), 0, stream, p, nkt);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((bwd_dq_kernel<D, NQ, RQ, BNQ>), dim3(nqt * p.BH), dim3(64 * NQ), 0, stream, p, nqt);
+  hipLaunchKernelGGL((bwd_grad_kernel<D, NK, BMK, NQ, RQ, BNQ, BwdCfg<D>::VLDS_DKV>), dim3(nkt * p.BH + nqt * p.BH),
+                     dim3(256), 0, stream, p, nkt * p.BH, nkt, nqt);
   return hipGetLastError();
 }
 
