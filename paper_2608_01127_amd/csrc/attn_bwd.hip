@@ -1,19 +1,21 @@
 // Block-causal attention backward (gfx950): the analytic softmax gradient of
 // paper Sec. 3.2's attention, with P recomputed from Q, K and the forward LSE.
 //
-//   delta kernel : Delta_i = sum_d dO_id O_id                    (HBM-bound)
-//   dK/dV kernel : one workgroup owns 128 or 256 keys (32 or 64 per wave, K and
-//                  V held in registers); it walks the query tiles that can see those
-//                  keys -- queries of the same or a later chunk -- staging Q,
-//                  dO, LSE and Delta in LDS.  Per 32 queries and wave:
-//                    S = Q K^T, dP = dO V^T     (keys on the lane axis)
-//                    P = exp(S - LSE), dS = P (dP - Delta)
-//                    dV^T += dO^T P, dK^T += Q^T dS   (transposing LDS reads)
-//   dQ kernel    : one workgroup owns 128 queries (Q and dO in registers) and
-//                  walks the key tiles below the chunk diagonal:
-//                    S^T = K Q^T, dP^T = V dO^T, dS^T = P^T (dP^T - Delta)
-//                    dQ^T += K^T dS^T
-// Recomputing S and dP in the dQ kernel costs 1.4x the MFMA work of a fused
+//   row-term kernel : Delta_i = sum_d dO_id O_id                 (HBM-bound)
+//   one grid of two kinds of workgroups:
+//   dK/dV work : a workgroup owns 128 keys (32 per wave, K held in registers,
+//                V in registers or, at D = 128, in an LDS tile); it walks the
+//                query tiles that can see those keys -- queries of the same or
+//                a later chunk -- staging Q, dO, LSE and Delta in LDS.  Per 32
+//                queries and wave:
+//                  S = Q K^T, dP = dO V^T     (keys on the lane axis)
+//                  P = exp(S - LSE), dS = P (dP - Delta)
+//                  dV^T += dO^T P, dK^T += Q^T dS   (transposing LDS reads)
+//   dQ work    : a workgroup owns 128 queries (Q and dO in registers) and
+//                walks the key tiles below the chunk diagonal:
+//                  S^T = K Q^T, dP^T = V dO^T, dS^T = P^T (dP^T - Delta)
+//                  dQ^T += K^T dS^T
+// Recomputing S and dP in the dQ work costs 1.4x the MFMA work of a fused
 // kernel with atomic dQ updates, but needs no fp32 dQ buffer and gives a
 // deterministic result.
 #include <type_traits>
