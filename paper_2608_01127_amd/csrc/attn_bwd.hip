@@ -83,6 +83,7 @@ template <int D, int NW, int BM, int KBW, bool VLDS>
 __device__ __forceinline__ void dkdv_body(const BwdParams& p, const int bh, const int kt, unsigned char* lds) {
   constexpr int BN = 32 * NW * KBW, NT = 64 * NW;
   static_assert(BM % 32 == 0, "32-row query blocks");
+  static_assert(!VLDS || D % 16 == 0, "the V tile in LDS has no zero columns past D");
   constexpr int KK = (D + 15) / 16, DB = (D + 31) / 32;  // D = 72: 80 and 96 columns
   using LD = DkdvLds<D, NW, BM, KBW, VLDS>;
   constexpr int TE = LD::TE, RT = LD::RT;
