@@ -30,3 +30,16 @@ def test_d128_training_pairs_closed_form():
     P = bench.pairs_block_causal(s.B, s.H, s.T, s.chunk_len)
     assert P == 16 * 2640 ** 2 * 136
     assert abs(14.0 * P * s.D - 2.718e13) / 2.718e13 < 1e-3
+
+
+def test_bench_refuses_several_gpus():
+    """One GPU only: --gpus above 1 exits with a message before touching a device."""
+    import json
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode != 0
+    assert "one GPU" in json.loads(r.stdout.strip().splitlines()[-1])["error"]
