@@ -484,7 +484,7 @@ struct BwdCfg {
   // D = 64 and spill at D = 128)
   static constexpr int RB_DQ = 1;
   // D = 128: the V tile in LDS and 32-query steps bring the dK/dV work under
-  // 256 registers (248), so it runs two waves per SIMD beside the dQ work in
+  // 256 registers (247), so it runs two waves per SIMD beside the dQ work in
   // one grid; holding V in registers needed 448 registers, one wave per SIMD,
   // in a grid of its own (the backward 5% slower, results bit-identical)
   static constexpr bool VLDS_DKV = D == 128;
