@@ -45,6 +45,11 @@ SMALL = [
     (2, 4, 700, 64, 96),     # chunk edges inside tiles, ragged last chunk
     (1, 8, 520, 72, 130),
     (2, 4, 300, 128, 100),
+    # D = 128 (dK/dV work in 32-query steps with V staged in LDS): the degenerate chunkings
+    (1, 1, 333, 128, 1),     # token-causal
+    (1, 2, 130, 128, 1000),  # chunk longer than the sequence
+    (1, 1, 1, 128, 1),       # single token
+    (1, 2, 161, 128, 32),    # chunk edges on every 32-query step, ragged tail
 ]
 
 
